@@ -1,0 +1,220 @@
+"""Lynx CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, obviously correct CPU statement of the Lynx hot path (see
+``lynx_oracle.c`` for the definitions and the paper passages they follow).
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its Python binding) never imports, links or runs it, and this package imports
+nothing from the product.
+
+Arrays are numpy.  BF16 tensors travel as their raw uint16 bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from pathlib import Path
+
+import numpy as np
+
+from . import build as _build
+
+HEAD_DIM = 128
+K_GROUP = 128
+
+_LIB = None
+
+
+def _load():
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    override = os.environ.get("LYNX_ORACLE_LIB")  # mutation tests load a planted-bug build
+    if override:
+        path = Path(override)
+    else:
+        if not _build.LIBRARY.exists() or (
+                _build.LIBRARY.stat().st_mtime < _build.SOURCE.stat().st_mtime):
+            _build.build()
+        path = _build.LIBRARY
+    lib = ctypes.CDLL(str(path))
+    P = ctypes.c_void_p
+    I = ctypes.c_int
+    lib.oracle_encode.argtypes = [I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_encode.restype = I
+    lib.oracle_merge.argtypes = [P, P, P, ctypes.c_size_t]
+    lib.oracle_merge.restype = None
+    lib.oracle_dequant.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P]
+    lib.oracle_dequant.restype = I
+    lib.oracle_anchor_decode.argtypes = [I, I, I, I, I, I, P, P, P, P, P, P, P, P,
+                                         P, P, P, P, I]
+    lib.oracle_anchor_decode.restype = I
+    lib.oracle_verify.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P,
+                                  P, P, P, P, P, I]
+    lib.oracle_verify.restype = I
+    _LIB = lib
+    return lib
+
+
+def _ptr(a):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return a.ctypes.data
+
+
+def default_threads() -> int:
+    return max(1, len(os.sched_getaffinity(0)))
+
+
+@dataclass
+class Layout:
+    """Cache geometry: kv heads, tokens per block, block-table row stride and
+    the per-sequence token stride of the logical metadata arrays."""
+    Hkv: int
+    bt: int
+    max_blocks: int
+    max_tokens: int
+
+    @property
+    def n_groups(self) -> int:
+        return -(-self.max_tokens // K_GROUP)
+
+
+@dataclass
+class Meta:
+    k_scale: np.ndarray  # fp32 [B][Hkv][n_groups][128]
+    k_zero: np.ndarray
+    v_scale: np.ndarray  # fp32 [B][Hkv][max_tokens]
+    v_zero: np.ndarray
+
+    @staticmethod
+    def empty(L: Layout, B: int) -> "Meta":
+        kshape = (B, L.Hkv, L.n_groups, HEAD_DIM)
+        vshape = (B, L.Hkv, L.max_tokens)
+        return Meta(np.zeros(kshape, np.float32), np.zeros(kshape, np.float32),
+                    np.zeros(vshape, np.float32), np.zeros(vshape, np.float32))
+
+
+def plane_bytes(L: Layout, n_blocks: int, row_bytes: int) -> int:
+    return n_blocks * L.Hkv * L.bt * row_bytes
+
+
+def encode(L: Layout, b: int, T: int, block_table: np.ndarray, k_bits: np.ndarray,
+           v_bits: np.ndarray, planes: dict, meta: Meta) -> None:
+    """Quantize/split/pack sequence b (k_bits, v_bits: uint16 [T][Hkv][128])
+    into planes['k_anc'|'v_anc'|'k_res'|'v_res'] (uint8, flat) and meta row b."""
+    lib = _load()
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    k_bits = np.ascontiguousarray(k_bits, dtype=np.uint16)
+    v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
+    assert k_bits.shape == (T, L.Hkv, HEAD_DIM) and v_bits.shape == k_bits.shape
+    rc = lib.oracle_encode(L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T, _ptr(bt_arr),
+                           _ptr(k_bits), _ptr(v_bits), _ptr(planes["k_anc"]),
+                           _ptr(planes["v_anc"]), _ptr(planes["k_res"]),
+                           _ptr(planes["v_res"]), _ptr(meta.k_scale), _ptr(meta.k_zero),
+                           _ptr(meta.v_scale), _ptr(meta.v_zero))
+    if rc != 0:
+        raise ValueError(f"oracle_encode rejected its arguments ({rc})")
+
+
+def merge(anc: np.ndarray, res: np.ndarray) -> np.ndarray:
+    """Anchor + residual nibble planes (n bytes each) -> 2n code bytes."""
+    anc = np.ascontiguousarray(anc, dtype=np.uint8).reshape(-1)
+    res = np.ascontiguousarray(res, dtype=np.uint8).reshape(-1)
+    assert anc.size == res.size
+    codes = np.empty(2 * anc.size, np.uint8)
+    _load().oracle_merge(_ptr(anc), _ptr(res), _ptr(codes), anc.size)
+    return codes
+
+
+def dequant(mode: str, L: Layout, b: int, T: int, block_table: np.ndarray,
+            k_plane: np.ndarray, v_plane: np.ndarray, meta: Meta):
+    """Reconstructed K, V of sequence b as fp64 [T][Hkv][128].
+    mode 'anchor': nibble planes, zero + (16a + 7.5) scale;
+    mode 'full':   code planes, zero + c scale."""
+    m = {"anchor": 0, "full": 1}[mode]
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    k_hat = np.empty((T, L.Hkv, HEAD_DIM), np.float64)
+    v_hat = np.empty_like(k_hat)
+    rc = _load().oracle_dequant(m, L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T,
+                                _ptr(bt_arr), _ptr(k_plane), _ptr(v_plane),
+                                _ptr(meta.k_scale), _ptr(meta.k_zero),
+                                _ptr(meta.v_scale), _ptr(meta.v_zero), _ptr(k_hat),
+                                _ptr(v_hat))
+    if rc != 0:
+        raise ValueError(f"oracle_dequant rejected its arguments ({rc})")
+    return k_hat, v_hat
+
+
+def anchor_decode(L: Layout, Hq: int, seq_lens: np.ndarray, block_table: np.ndarray,
+                  k_anc: np.ndarray, v_anc: np.ndarray, meta: Meta, q_bits: np.ndarray,
+                  unit_mask: np.ndarray | None = None, nthreads: int | None = None):
+    """One query per sequence (q_bits uint16 [B][Hq][128]) over the Anchor-only
+    cache.  Returns (out fp64 [B][Hq][128], lse fp64 [B][Hq]); units left out
+    by unit_mask ([B][Hkv] flags) come back as NaN."""
+    seq_lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    B = seq_lens.size
+    q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
+    assert q_bits.shape == (B, Hq, HEAD_DIM)
+    out = np.full((B, Hq, HEAD_DIM), np.nan)
+    lse = np.full((B, Hq), np.nan)
+    mask = None if unit_mask is None else np.ascontiguousarray(unit_mask, dtype=np.uint8)
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    rc = _load().oracle_anchor_decode(
+        L.Hkv, L.bt, L.max_blocks, L.max_tokens, B, Hq, _ptr(seq_lens), _ptr(bt_arr),
+        _ptr(k_anc), _ptr(v_anc), _ptr(meta.k_scale), _ptr(meta.k_zero),
+        _ptr(meta.v_scale), _ptr(meta.v_zero), _ptr(q_bits), _ptr(out), _ptr(lse),
+        _ptr(mask), nthreads or default_threads())
+    if rc != 0:
+        raise ValueError(f"oracle_anchor_decode failed ({rc})")
+    return out, lse
+
+
+def verify(L: Layout, Hq: int, seq_lens: np.ndarray, block_table: np.ndarray,
+           k_codes: np.ndarray, v_codes: np.ndarray, meta: Meta, q_bits: np.ndarray,
+           k_new_bits: np.ndarray | None = None, v_new_bits: np.ndarray | None = None,
+           unit_mask: np.ndarray | None = None, nthreads: int | None = None):
+    """nq draft queries per sequence (q_bits uint16 [B][nq][Hq][128]) over the
+    merged 8-bit cache plus, if given, the BF16 draft K/V ([B][nq][Hkv][128]),
+    causal among drafts.  Returns (out fp64 [B][nq][Hq][128], lse [B][nq][Hq])."""
+    seq_lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    B = seq_lens.size
+    q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
+    nq = q_bits.shape[1]
+    assert q_bits.shape == (B, nq, Hq, HEAD_DIM)
+    if k_new_bits is not None:
+        k_new_bits = np.ascontiguousarray(k_new_bits, dtype=np.uint16)
+        v_new_bits = np.ascontiguousarray(v_new_bits, dtype=np.uint16)
+        assert k_new_bits.shape == (B, nq, L.Hkv, HEAD_DIM)
+        assert v_new_bits.shape == k_new_bits.shape
+    out = np.full((B, nq, Hq, HEAD_DIM), np.nan)
+    lse = np.full((B, nq, Hq), np.nan)
+    mask = None if unit_mask is None else np.ascontiguousarray(unit_mask, dtype=np.uint8)
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    rc = _load().oracle_verify(
+        L.Hkv, L.bt, L.max_blocks, L.max_tokens, B, Hq, nq, _ptr(seq_lens), _ptr(bt_arr),
+        _ptr(k_codes), _ptr(v_codes), _ptr(meta.k_scale), _ptr(meta.k_zero),
+        _ptr(meta.v_scale), _ptr(meta.v_zero), _ptr(q_bits), _ptr(k_new_bits),
+        _ptr(v_new_bits), _ptr(out), _ptr(lse), _ptr(mask),
+        nthreads or default_threads())
+    if rc != 0:
+        raise ValueError(f"oracle_verify failed ({rc})")
+    return out, lse
+
+
+# --------------------------------------------------------------------------
+# Convenience: a whole batch in the contiguous layout, or a paged pool.
+# --------------------------------------------------------------------------
+
+def encode_batch(L: Layout, seq_lens, block_table, k_list, v_list, n_blocks: int):
+    """Encode every sequence b of a batch (k_list[b], v_list[b]: uint16
+    [T_b][Hkv][128]) into fresh planes of n_blocks blocks.  Returns (planes, meta)."""
+    B = len(seq_lens)
+    nbytes = plane_bytes(L, n_blocks, 64)
+    planes = {name: np.zeros(nbytes, np.uint8) for name in ("k_anc", "v_anc", "k_res", "v_res")}
+    meta = Meta.empty(L, B)
+    for b in range(B):
+        encode(L, b, int(seq_lens[b]), block_table, k_list[b], v_list[b], planes, meta)
+    return planes, meta

@@ -1,0 +1,464 @@
+/*
+ * Lynx CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, deliberately unoptimised CPU statement of what the Lynx hot
+ * path computes.  Only the test suite, the smoke check and the benchmark's CPU
+ * baseline leg load this library; the product path never does.  It shares no
+ * code, header, table or helper with the HIP implementation.
+ *
+ * What it implements (paper: "Lynx: Progressive Speculative Quantization for
+ * accelerating KV Transfer in Long-Context Inference"):
+ *
+ *   encode  -- grouped linear quantization to 8-bit codes (Sec. 2.3, the
+ *              linear map Q(X) = round(X/S + Z) with S taken from the group's
+ *              [x_min, x_max], and grouped quantization), then the
+ *              split-stream construction of Alg. 1 stage 4 / Sec. 4.1: the 4
+ *              most significant bits form the Anchor stream, the 4 least
+ *              significant bits the Residual stream, two 4-bit values packed
+ *              per byte (Sec. 5, Compression Kernel).
+ *   merge   -- the Residual phase of Sec. 4.2: Anchor and Residual recombine
+ *              into the full 8-bit code Q_full.
+ *   dequant -- value reconstruction from the 8-bit code, or from the Anchor
+ *              alone (Anchor phase of Sec. 4.2).
+ *   attention -- O = softmax(Q K^T / sqrt(d_k)) V (Sec. 2, attention
+ *              equation): decode of one query over the Anchor-only cache
+ *              (Sec. 4.2 Anchor phase, Speculative Decoder) and the single
+ *              parallel verification pass of k draft queries over the merged
+ *              cache, causal among the drafts (Sec. 4.3).
+ *
+ * Readings where the paper is silent (each listed in the design notes):
+ *   - K is grouped per channel over 128 consecutive tokens, V per token over
+ *     its 128 dims.
+ *   - zero = group minimum (the value of code 0); scale = (max - min) / 255;
+ *     the code is rint((x - zero) * inv) with inv = 255 / (max - min), all in
+ *     IEEE fp32, rint = round half to even, clamped to [0, 255].
+ *   - A group whose range is not a positive finite number, or whose inverse
+ *     range overflows, gets scale = inv = 0 and all codes 0.
+ *   - -0 in a group's min/max is stored as +0.
+ *   - Split: anchor a = code >> 4, residual r = code & 15, so code = a*16 + r.
+ *   - Anchor-only reconstruction: zero + (16 a + 7.5) * scale (the centre of
+ *     the 16 codes an anchor value stands for).
+ *   - Packing: within a byte the low nibble holds the even element (dim 2j),
+ *     the high nibble the odd one (dim 2j+1).
+ *   - Plane layout: a token row of a nibble plane is 64 bytes; the row of
+ *     (sequence b, kv head h, token t) starts at
+ *        ((block_table[b][t / bt] * Hkv + h) * bt + t % bt) * 64.
+ *     Code planes use the same formula with 128-byte rows.
+ *   - Metadata is logical (never paged): k_scale/k_zero are
+ *     [B][Hkv][ceil(max_tokens/128)][128], v_scale/v_zero [B][Hkv][max_tokens].
+ *   - Query head hq reads kv head hq / (Hq / Hkv).
+ *   - Verification: draft query i sees the whole context plus draft tokens
+ *     0..i, whose K/V are BF16 and never quantized.
+ *
+ * Precision: the codec runs in fp32 because fp32 arithmetic decides the
+ * integer codes and the GPU path must take the same decision; attention runs
+ * in fp64 from the fp32 metadata and exact BF16->fp64 inputs.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fno-fast-math -shared -fPIC -pthread.
+ */
+#include <float.h>
+#include <math.h>
+#include <pthread.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define HEAD_DIM 128
+#define K_GROUP 128
+#define NIBBLE_ROW 64
+#define CODE_ROW 128
+
+/* ------------------------------------------------------------------------ */
+/* Scalar helpers                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* BF16 is the top half of an IEEE fp32; widening is exact. */
+static float bf16_bits_to_float(uint16_t bits)
+{
+    uint32_t u = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+/* Byte offset of token row (b, h, t) in a plane with `row_bytes` per row. */
+static size_t plane_row_offset(const int32_t *block_table_row, int Hkv, int bt,
+                               int h, int t, int row_bytes)
+{
+    size_t block = (size_t)block_table_row[t / bt];
+    return ((block * (size_t)Hkv + (size_t)h) * (size_t)bt + (size_t)(t % bt)) *
+           (size_t)row_bytes;
+}
+
+/* Group statistics of Sec. 2.3: zero = min, scale = (max-min)/255, and the
+ * reciprocal inv = 255/(max-min) used to map values onto 0..255. */
+static void group_stats(const float *x, int n, float *scale, float *zero,
+                        float *inv)
+{
+    float mn = x[0], mx = x[0];
+    for (int i = 1; i < n; ++i) {
+        if (x[i] < mn) mn = x[i];
+        if (x[i] > mx) mx = x[i];
+    }
+    if (mn == 0.0f) mn = 0.0f; /* store -0 as +0 */
+    if (mx == 0.0f) mx = 0.0f;
+    float range = mx - mn;
+    float r = 255.0f / range;
+    if (!(range > 0.0f) || !(range <= FLT_MAX) || !(r <= FLT_MAX)) {
+        *scale = 0.0f;
+        *inv = 0.0f;
+    } else {
+        *scale = range / 255.0f;
+        *inv = r;
+    }
+    *zero = mn;
+}
+
+/* Linear quantization of one value to an unsigned 8-bit code. */
+static int quantize(float x, float zero, float inv)
+{
+    float y = (x - zero) * inv;
+    float c = rintf(y);
+    if (!(c >= 0.0f)) c = 0.0f; /* also maps NaN to 0 */
+    if (c > 255.0f) c = 255.0f;
+    return (int)c;
+}
+
+/* Put 4-bit value `nib` as element `e` of a packed row (low nibble = even e). */
+static void put_nibble(uint8_t *row, int e, int nib)
+{
+    int j = e / 2;
+    int shift = (e % 2) * 4;
+    row[j] = (uint8_t)((row[j] & ~(0xF << shift)) | ((nib & 0xF) << shift));
+}
+
+static int get_nibble(const uint8_t *row, int e)
+{
+    return (row[e / 2] >> ((e % 2) * 4)) & 0xF;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Encode (quantize, split, pack) for one sequence b of one layer            */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * k, v: BF16 bits [T][Hkv][128].  Writes the four nibble planes for rows
+ * t < T of sequence b and metadata row b.  Returns 0, or -1 on bad sizes.
+ */
+int oracle_encode(int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
+                  const int32_t *block_table, const uint16_t *k,
+                  const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
+                  uint8_t *k_res, uint8_t *v_res, float *k_scale,
+                  float *k_zero, float *v_scale, float *v_zero)
+{
+    if (Hkv < 1 || bt < 1 || T < 0 || T > max_tokens ||
+        (size_t)(T + bt - 1) / (size_t)bt > (size_t)max_blocks)
+        return -1;
+    const int32_t *bt_row = block_table + (size_t)b * (size_t)max_blocks;
+    const int n_groups_max = (max_tokens + K_GROUP - 1) / K_GROUP;
+    float vals[K_GROUP > HEAD_DIM ? K_GROUP : HEAD_DIM];
+
+    for (int h = 0; h < Hkv; ++h) {
+        /* K: one group per (128-token window g, channel d). */
+        for (int g = 0; g * K_GROUP < T; ++g) {
+            int t0 = g * K_GROUP;
+            int t1 = t0 + K_GROUP < T ? t0 + K_GROUP : T;
+            for (int d = 0; d < HEAD_DIM; ++d) {
+                for (int t = t0; t < t1; ++t)
+                    vals[t - t0] = bf16_bits_to_float(
+                        k[((size_t)t * Hkv + h) * HEAD_DIM + d]);
+                float scale, zero, inv;
+                group_stats(vals, t1 - t0, &scale, &zero, &inv);
+                for (int t = t0; t < t1; ++t) {
+                    int c = quantize(vals[t - t0], zero, inv);
+                    size_t off = plane_row_offset(bt_row, Hkv, bt, h, t, NIBBLE_ROW);
+                    put_nibble(k_anc + off, d, c >> 4);
+                    put_nibble(k_res + off, d, c & 15);
+                }
+                size_t m = (((size_t)b * Hkv + h) * n_groups_max + g) * HEAD_DIM + d;
+                k_scale[m] = scale;
+                k_zero[m] = zero;
+            }
+        }
+        /* V: one group per token, over its 128 dims. */
+        for (int t = 0; t < T; ++t) {
+            for (int d = 0; d < HEAD_DIM; ++d)
+                vals[d] = bf16_bits_to_float(v[((size_t)t * Hkv + h) * HEAD_DIM + d]);
+            float scale, zero, inv;
+            group_stats(vals, HEAD_DIM, &scale, &zero, &inv);
+            size_t off = plane_row_offset(bt_row, Hkv, bt, h, t, NIBBLE_ROW);
+            for (int d = 0; d < HEAD_DIM; ++d) {
+                int c = quantize(vals[d], zero, inv);
+                put_nibble(v_anc + off, d, c >> 4);
+                put_nibble(v_res + off, d, c & 15);
+            }
+            size_t m = ((size_t)b * Hkv + h) * (size_t)max_tokens + t;
+            v_scale[m] = scale;
+            v_zero[m] = zero;
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Merge (Residual phase): code = anchor * 16 + residual, element by element */
+/* ------------------------------------------------------------------------ */
+
+/* n_packed bytes of each nibble plane -> 2 * n_packed code bytes. */
+void oracle_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes,
+                  size_t n_packed)
+{
+    for (size_t e = 0; e < 2 * n_packed; ++e) {
+        int a = (anc[e / 2] >> ((e % 2) * 4)) & 0xF;
+        int r = (res[e / 2] >> ((e % 2) * 4)) & 0xF;
+        codes[e] = (uint8_t)(a * 16 + r);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dequantization                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* One reconstructed element (b, h, t, d), fp64.
+ * mode 0: anchor-only, planes are nibble planes:  x = zero + (16 a + 7.5) scale
+ * mode 1: full 8-bit, planes are code planes:     x = zero + c * scale      */
+static void dequant_element(int mode, int Hkv, int bt, int max_tokens,
+                            const int32_t *bt_row, int b, int h, int t, int d,
+                            const uint8_t *k_plane, const uint8_t *v_plane,
+                            const float *k_scale, const float *k_zero,
+                            const float *v_scale, const float *v_zero,
+                            double *k_out, double *v_out)
+{
+    const int n_groups_max = (max_tokens + K_GROUP - 1) / K_GROUP;
+    const int row_bytes = mode == 0 ? NIBBLE_ROW : CODE_ROW;
+    size_t off = plane_row_offset(bt_row, Hkv, bt, h, t, row_bytes);
+    size_t km = (((size_t)b * Hkv + h) * n_groups_max + t / K_GROUP) * HEAD_DIM + d;
+    size_t vm = ((size_t)b * Hkv + h) * (size_t)max_tokens + t;
+    double kq, vq;
+    if (mode == 0) {
+        kq = 16.0 * get_nibble(k_plane + off, d) + 7.5;
+        vq = 16.0 * get_nibble(v_plane + off, d) + 7.5;
+    } else {
+        kq = (double)k_plane[off + d];
+        vq = (double)v_plane[off + d];
+    }
+    *k_out = (double)k_zero[km] + kq * (double)k_scale[km];
+    *v_out = (double)v_zero[vm] + vq * (double)v_scale[vm];
+}
+
+/*
+ * Fills k_hat, v_hat [T][Hkv][128] (fp64) for sequence b; mode as above.
+ * Returns 0 or -1.
+ */
+int oracle_dequant(int mode, int Hkv, int bt, int max_blocks, int max_tokens,
+                   int b, int T, const int32_t *block_table,
+                   const uint8_t *k_plane, const uint8_t *v_plane,
+                   const float *k_scale, const float *k_zero,
+                   const float *v_scale, const float *v_zero, double *k_hat,
+                   double *v_hat)
+{
+    if ((mode != 0 && mode != 1) || T < 0 || T > max_tokens) return -1;
+    const int32_t *bt_row = block_table + (size_t)b * (size_t)max_blocks;
+    for (int t = 0; t < T; ++t)
+        for (int h = 0; h < Hkv; ++h)
+            for (int d = 0; d < HEAD_DIM; ++d) {
+                size_t o = ((size_t)t * Hkv + h) * HEAD_DIM + d;
+                dequant_element(mode, Hkv, bt, max_tokens, bt_row, b, h, t, d,
+                                k_plane, v_plane, k_scale, k_zero, v_scale,
+                                v_zero, &k_hat[o], &v_hat[o]);
+            }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Attention: O = softmax(q K^T / sqrt(d)) V, fp64                           */
+/* ------------------------------------------------------------------------ */
+
+/* One query row over n key/value rows (row stride `stride` doubles).
+ * Writes o[128] and the log-sum-exp of the scaled scores. */
+static void attend(const double *q, const double *keys, const double *vals,
+                   size_t stride, int n, double *o, double *lse)
+{
+    const double sm_scale = 1.0 / sqrt((double)HEAD_DIM);
+    double *s = (double *)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    double m = -INFINITY;
+    for (int t = 0; t < n; ++t) {
+        double acc = 0.0;
+        for (int d = 0; d < HEAD_DIM; ++d) acc += q[d] * keys[(size_t)t * stride + d];
+        s[t] = acc * sm_scale;
+        if (s[t] > m) m = s[t];
+    }
+    double l = 0.0;
+    for (int t = 0; t < n; ++t) {
+        s[t] = exp(s[t] - m);
+        l += s[t];
+    }
+    for (int d = 0; d < HEAD_DIM; ++d) {
+        double acc = 0.0;
+        for (int t = 0; t < n; ++t) acc += s[t] * vals[(size_t)t * stride + d];
+        o[d] = n > 0 ? acc / l : 0.0;
+    }
+    if (lse) *lse = n > 0 ? m + log(l) : -INFINITY;
+    free(s);
+}
+
+typedef struct {
+    int mode; /* 0 anchor decode, 1 verify */
+    int Hkv, bt, max_blocks, max_tokens, B, Hq, nq;
+    const int32_t *seq_lens, *block_table;
+    const uint8_t *k_plane, *v_plane;
+    const float *k_scale, *k_zero, *v_scale, *v_zero;
+    const uint16_t *q, *k_new, *v_new;
+    const uint8_t *unit_mask;
+    double *out, *lse;
+    int nthreads;
+    int thread_id;
+    int status;
+} attn_job;
+
+/* Work unit u = b * Hkv + kvh: all G query heads of one kv head. */
+static void attention_unit(const attn_job *J, int u, double *keys, double *vals)
+{
+    const int Hkv = J->Hkv, G = J->Hq / J->Hkv;
+    const int b = u / Hkv, kvh = u % Hkv;
+    const int T = J->seq_lens[b];
+    const int32_t *bt_row = J->block_table + (size_t)b * (size_t)J->max_blocks;
+    for (int t = 0; t < T; ++t)
+        for (int d = 0; d < HEAD_DIM; ++d)
+            dequant_element(J->mode, Hkv, J->bt, J->max_tokens, bt_row, b, kvh, t,
+                            d, J->k_plane, J->v_plane, J->k_scale, J->k_zero,
+                            J->v_scale, J->v_zero, &keys[(size_t)t * HEAD_DIM + d],
+                            &vals[(size_t)t * HEAD_DIM + d]);
+    double qd[HEAD_DIM];
+    for (int i = 0; i < J->nq; ++i) {
+        int n = T;
+        if (J->mode == 1 && J->k_new) {
+            /* Draft tokens 0..i follow the context, in BF16. */
+            for (int j = 0; j <= i; ++j)
+                for (int d = 0; d < HEAD_DIM; ++d) {
+                    size_t src = ((((size_t)b * J->nq + j) * Hkv) + kvh) * HEAD_DIM + d;
+                    keys[(size_t)(T + j) * HEAD_DIM + d] = bf16_bits_to_float(J->k_new[src]);
+                    vals[(size_t)(T + j) * HEAD_DIM + d] = bf16_bits_to_float(J->v_new[src]);
+                }
+            n = T + i + 1;
+        }
+        for (int g = 0; g < G; ++g) {
+            int hq = kvh * G + g;
+            size_t row = (((size_t)b * J->nq + i) * J->Hq + hq);
+            for (int d = 0; d < HEAD_DIM; ++d)
+                qd[d] = bf16_bits_to_float(J->q[row * HEAD_DIM + d]);
+            attend(qd, keys, vals, HEAD_DIM, n, J->out + row * HEAD_DIM,
+                   J->lse ? J->lse + row : NULL);
+        }
+    }
+}
+
+static void *attention_worker(void *arg)
+{
+    attn_job *J = (attn_job *)arg;
+    int max_T = 0;
+    for (int b = 0; b < J->B; ++b)
+        if (J->seq_lens[b] > max_T) max_T = J->seq_lens[b];
+    size_t one = (size_t)(max_T + J->nq + 1) * HEAD_DIM;
+    double *keys = (double *)malloc(one * sizeof(double));
+    double *vals = (double *)malloc(one * sizeof(double));
+    if (!keys || !vals) {
+        J->status = -2;
+    } else {
+        int units = J->B * J->Hkv;
+        for (int u = J->thread_id; u < units; u += J->nthreads)
+            if (!J->unit_mask || J->unit_mask[u]) attention_unit(J, u, keys, vals);
+    }
+    free(keys);
+    free(vals);
+    return NULL;
+}
+
+static int run_attention(attn_job *base)
+{
+    if (base->Hkv < 1 || base->Hq < 1 || base->Hq % base->Hkv != 0 || base->B < 0 ||
+        base->nq < 1)
+        return -1;
+    for (int b = 0; b < base->B; ++b)
+        if (base->seq_lens[b] < 0 || base->seq_lens[b] > base->max_tokens) return -1;
+    int nt = base->nthreads < 1 ? 1 : base->nthreads;
+    attn_job *jobs = (attn_job *)calloc((size_t)nt, sizeof(attn_job));
+    pthread_t *th = (pthread_t *)calloc((size_t)nt, sizeof(pthread_t));
+    if (!jobs || !th) {
+        free(jobs);
+        free(th);
+        return -2;
+    }
+    for (int i = 0; i < nt; ++i) {
+        jobs[i] = *base;
+        jobs[i].nthreads = nt;
+        jobs[i].thread_id = i;
+        jobs[i].status = 0;
+    }
+    for (int i = 1; i < nt; ++i) pthread_create(&th[i], NULL, attention_worker, &jobs[i]);
+    attention_worker(&jobs[0]);
+    int status = jobs[0].status;
+    for (int i = 1; i < nt; ++i) {
+        pthread_join(th[i], NULL);
+        if (jobs[i].status) status = jobs[i].status;
+    }
+    free(jobs);
+    free(th);
+    return status;
+}
+
+/*
+ * Anchor-phase decode: one query per sequence over the Anchor-only cache.
+ * q: BF16 bits [B][Hq][128]; out: fp64 [B][Hq][128]; lse: fp64 [B][Hq] or NULL.
+ * unit_mask: NULL, or B*Hkv flags selecting which (b, kv head) units to compute.
+ */
+int oracle_anchor_decode(int Hkv, int bt, int max_blocks, int max_tokens, int B,
+                         int Hq, const int32_t *seq_lens,
+                         const int32_t *block_table, const uint8_t *k_anc,
+                         const uint8_t *v_anc, const float *k_scale,
+                         const float *k_zero, const float *v_scale,
+                         const float *v_zero, const uint16_t *q, double *out,
+                         double *lse, const uint8_t *unit_mask, int nthreads)
+{
+    attn_job J;
+    memset(&J, 0, sizeof J);
+    J.mode = 0;
+    J.Hkv = Hkv; J.bt = bt; J.max_blocks = max_blocks; J.max_tokens = max_tokens;
+    J.B = B; J.Hq = Hq; J.nq = 1;
+    J.seq_lens = seq_lens; J.block_table = block_table;
+    J.k_plane = k_anc; J.v_plane = v_anc;
+    J.k_scale = k_scale; J.k_zero = k_zero; J.v_scale = v_scale; J.v_zero = v_zero;
+    J.q = q; J.out = out; J.lse = lse; J.unit_mask = unit_mask;
+    J.nthreads = nthreads;
+    return run_attention(&J);
+}
+
+/*
+ * Verification pass: nq draft queries per sequence over the merged 8-bit
+ * cache, plus (if k_new != NULL) the BF16 draft tokens, causal among drafts.
+ * q: BF16 bits [B][nq][Hq][128]; k_new, v_new: BF16 bits [B][nq][Hkv][128]
+ * or NULL; out: fp64 [B][nq][Hq][128]; lse: fp64 [B][nq][Hq] or NULL.
+ */
+int oracle_verify(int Hkv, int bt, int max_blocks, int max_tokens, int B, int Hq,
+                  int nq, const int32_t *seq_lens, const int32_t *block_table,
+                  const uint8_t *k_codes, const uint8_t *v_codes,
+                  const float *k_scale, const float *k_zero,
+                  const float *v_scale, const float *v_zero, const uint16_t *q,
+                  const uint16_t *k_new, const uint16_t *v_new, double *out,
+                  double *lse, const uint8_t *unit_mask, int nthreads)
+{
+    if ((k_new == NULL) != (v_new == NULL)) return -1;
+    attn_job J;
+    memset(&J, 0, sizeof J);
+    J.mode = 1;
+    J.Hkv = Hkv; J.bt = bt; J.max_blocks = max_blocks; J.max_tokens = max_tokens;
+    J.B = B; J.Hq = Hq; J.nq = nq;
+    J.seq_lens = seq_lens; J.block_table = block_table;
+    J.k_plane = k_codes; J.v_plane = v_codes;
+    J.k_scale = k_scale; J.k_zero = k_zero; J.v_scale = v_scale; J.v_zero = v_zero;
+    J.q = q; J.k_new = k_new; J.v_new = v_new;
+    J.out = out; J.lse = lse; J.unit_mask = unit_mask;
+    J.nthreads = nthreads;
+    return run_attention(&J);
+}

@@ -1,0 +1,59 @@
+"""The oracle's pins catch plausible mistakes.
+
+Each case plants one mistake in a copy of the oracle source (never in the
+oracle itself), builds it on the CPU, and runs the CPU pin tests against the
+planted build in a subprocess: they must fail.  Covered mistakes: wrong
+rounding, a dropped term, a wrong constant, a swapped nibble order, a wrong
+group size, a transposed metadata index, a wrong sign, a wrong head mapping,
+a missing causal mask, a swapped merge.
+"""
+import os
+import subprocess
+import sys
+from pathlib import Path
+
+import pytest
+
+ROOT = Path(__file__).resolve().parent.parent
+SRC = (ROOT / "oracle" / "lynx_oracle.c").read_text()
+
+MUTANTS = {
+    "floor_not_rint": ("float c = rintf(y);", "float c = floorf(y);"),
+    "round_half_away": ("float c = rintf(y);", "float c = roundf(y);"),
+    "dropped_zero_term": ("float y = (x - zero) * inv;", "float y = x * inv;"),
+    "scale_over_256": ("*scale = range / 255.0f;", "*scale = range / 256.0f;"),
+    "anchor_offset_8": ("kq = 16.0 * get_nibble(k_plane + off, d) + 7.5;\n        vq = 16.0 * get_nibble(v_plane + off, d) + 7.5;",
+                        "kq = 16.0 * get_nibble(k_plane + off, d) + 8.0;\n        vq = 16.0 * get_nibble(v_plane + off, d) + 8.0;"),
+    "nibble_order_swapped": ("    int shift = (e % 2) * 4;\n    row[j]", "    int shift = (1 - e % 2) * 4;\n    row[j]"),
+    "k_group_64": ("#define K_GROUP 128", "#define K_GROUP 64"),
+    "k_meta_transposed": ("size_t m = (((size_t)b * Hkv + h) * n_groups_max + g) * HEAD_DIM + d;",
+                          "size_t m = (((size_t)b * n_groups_max + g) * Hkv + h) * HEAD_DIM + d;"),
+    "softmax_sign": ("s[t] = exp(s[t] - m);", "s[t] = exp(m - s[t]);"),
+    "no_sm_scale": ("s[t] = acc * sm_scale;", "s[t] = acc;"),
+    "gqa_strided": ("int hq = kvh * G + g;", "int hq = g * Hkv + kvh;"),
+    "no_causal_mask": [("for (int j = 0; j <= i; ++j)", "for (int j = 0; j < J->nq; ++j)"),
+                       ("n = T + i + 1;", "n = T + J->nq;")],
+    "merge_swapped": ("codes[e] = (uint8_t)(a * 16 + r);", "codes[e] = (uint8_t)(r * 16 + a);"),
+    "v_meta_wrong_stride": ("size_t vm = ((size_t)b * Hkv + h) * (size_t)max_tokens + t;\n    double kq",
+                            "size_t vm = ((size_t)h * 1 + b) * (size_t)max_tokens + t;\n    double kq"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, tmp_path):
+    edits = MUTANTS[name]
+    edits = [edits] if isinstance(edits, tuple) else edits
+    text = SRC
+    for find, repl in edits:
+        assert text.count(find) == 1, f"mutation anchor for {name} not unique/present"
+        text = text.replace(find, repl)
+    src = tmp_path / "mutant.c"
+    src.write_text(text)
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-shared", "-fPIC",
+                    "-pthread", str(src), "-o", str(lib), "-lm"], check=True)
+    env = dict(os.environ, LYNX_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        "tests/test_oracle_codec.py", "tests/test_oracle_attention.py"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
