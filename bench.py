@@ -1,0 +1,255 @@
+#!/usr/bin/env python3
+"""Benchmark of the Lynx hot path on one MI355X.
+
+Workload (Llama-3-8B-shaped single sequence): 32 layers x (32 query heads,
+8 kv heads, head_dim 128), context 32768 tokens, batch 1, BF16 K/V ~ N(0,1)
+with 1% of K (kv head, channel) columns x8; k = 8 draft queries per layer for
+verification.  Synthetic data, seeded.
+
+One step = the whole hot path over all 32 layers:
+  1. encode (quantize, split, pack) every layer's K/V       [main stream]
+  2. residual transport: H2D copy of every layer's residual planes from
+     pinned host memory, standing in for the network          [side stream]
+     overlapped with
+  3. anchor-only decode attention, one query token per layer   [main stream]
+  4. wait for the residual, merge anchor + residual -> codes   [main stream]
+  5. verification attention of the 8 drafts over the codes    [main stream]
+
+Printed: one JSON line.  `value` is the anchor-decode attention throughput in
+GB/s of algorithmic KV bytes (144 bytes per token per kv head) over the timed
+steps, from HIP events on the stream the kernels run on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "anchor decode-attn KV GB/s (% HBM peak); encode/merge GB/s; verify µs @128k"
+WORKLOAD = "llama3-8b-32k"
+
+# algorithmic bytes per unit
+ENC_BYTES_PER_ELEM = 2.0 + 0.5 + 0.5 + 0.0625   # read BF16, write 2 nibbles, metadata
+MERGE_BYTES_PER_ELEM = 2.0                      # read 0.5 + 0.5, write 1
+DECODE_BYTES_PER_TOKEN_HEAD = 64 + 64 + 8 + 8   # K, V nibble rows + V meta + K meta (amortised)
+VERIFY_BYTES_PER_TOKEN_HEAD = 128 + 128 + 8 + 8  # K, V code rows + metadata
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--layers", type=int, default=None, help="override layer count (testing only)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-layers", type=int, default=4)
+    return p.parse_args()
+
+
+def cpu_baseline(w, layer_inputs, n_layers):
+    """The CPU oracle, untuned, timed on this host on a bounded sample: the
+    anchor decode of the first n_layers layers (all kv heads)."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    def bits(t):
+        return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+    threads = oracle.default_threads()
+    T, Hkv = w.context, w.Hkv
+    OL = oracle.Layout(Hkv=Hkv, bt=T, max_blocks=1, max_tokens=T)
+    table = np.zeros((1, 1), np.int32)
+    t_dec = 0.0
+    for l in range(n_layers):
+        k, v, q = layer_inputs(l)
+        planes, meta = oracle.encode_batch(OL, [T], table, [bits(k)], [bits(v)], 1)
+        t0 = time.perf_counter()
+        oracle.anchor_decode(OL, w.Hq, np.array([T]), table, planes["k_anc"], planes["v_anc"],
+                             meta, bits(q), nthreads=threads)
+        t_dec += time.perf_counter() - t0
+    nbytes = n_layers * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
+    return {"value": round(nbytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"anchor decode (fp64 oracle) of {n_layers} of {w.layers} layers, all "
+                      f"{Hkv} kv heads, {T} tokens; {t_dec:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              "layout of this path is described in DESIGN.md and is not launched here.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_01831_amd import inputs, lynx
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lynx.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = inputs.WORKLOADS[WORKLOAD]
+    n_layers = args.layers or w.layers
+    T, Hkv, Hq, nq = w.context, w.Hkv, w.Hq, w.drafts
+    L = lynx.contiguous_layout(Hkv, 1, T)
+    table = torch.zeros(1, 1, dtype=torch.int32, device=dev)
+    lens = torch.tensor([T], dtype=torch.int32, device=dev)
+
+    # ---------------- set-up (untimed) ----------------
+    t_setup = time.perf_counter()
+    K, V, Q, QV, KN, VN, pools = [], [], [], [], [], [], []
+    for l in range(n_layers):
+        K.append(inputs.kv(w, "k", layer=l, device=dev))
+        V.append(inputs.kv(w, "v", layer=l, device=dev))
+        Q.append(inputs.queries(w, layer=l, device=dev))
+        QV.append(inputs.queries(w, layer=l, step=1, nq=nq, device=dev))
+        kn, vn = inputs.drafts_kv(w, layer=l, device=dev)
+        KN.append(kn)
+        VN.append(vn)
+        pools.append(lynx.KVPool.allocate(L, 1, device=dev))
+    # decode-side residual buffers, filled only by the H2D transport
+    recv_k = [torch.empty_like(p.k_res) for p in pools]
+    recv_v = [torch.empty_like(p.v_res) for p in pools]
+    # the residual stream as it leaves the prefill side: pinned host staging
+    for l in range(n_layers):
+        pools[l].encode(0, T, table, K[l], V[l])
+    host_k = [p.k_res.cpu().pin_memory() for p in pools]
+    host_v = [p.v_res.cpu().pin_memory() for p in pools]
+    out = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device=dev)
+    outv = torch.empty(1, nq, Hq, 128, dtype=torch.bfloat16, device=dev)
+    ws = lynx.workspace(L, 1, Hq, nq, T)
+    torch.cuda.synchronize()
+    t_setup = time.perf_counter() - t_setup
+
+    main_s = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(rec):
+        e = {k: ev() for k in ("start", "enc", "dec0", "dec", "merge0", "merge", "ver")}
+        e["h2d0"], e["h2d"] = ev(), ev()
+        e["start"].record(main_s)
+        for l in range(n_layers):
+            pools[l].encode(0, T, table, K[l], V[l])
+        e["enc"].record(main_s)
+        # residual transport on the side stream, after the prefill side is done
+        side.wait_event(e["enc"])
+        with torch.cuda.stream(side):
+            e["h2d0"].record(side)
+            for l in range(n_layers):
+                recv_k[l].copy_(host_k[l], non_blocking=True)
+                recv_v[l].copy_(host_v[l], non_blocking=True)
+            e["h2d"].record(side)
+        e["dec0"].record(main_s)
+        for l in range(n_layers):
+            p = pools[l]
+            lynx.lynx_attn_anchor_decode(L, 1, Hq, T, lens, table, p.k_anc, p.v_anc, p.meta,
+                                         Q[l], out, None, ws)
+        e["dec"].record(main_s)
+        main_s.wait_event(e["h2d"])
+        e["merge0"].record(main_s)
+        for l in range(n_layers):
+            p = pools[l]
+            lynx.lynx_kv_merge(p.k_anc, recv_k[l], p.k_codes)
+            lynx.lynx_kv_merge(p.v_anc, recv_v[l], p.v_codes)
+        e["merge"].record(main_s)
+        for l in range(n_layers):
+            p = pools[l]
+            lynx.lynx_attn_verify(L, 1, Hq, nq, T, lens, table, p.k_codes, p.v_codes, p.meta,
+                                  QV[l], KN[l], VN[l], outv, ws)
+        e["ver"].record(main_s)
+        rec.append(e)
+
+    for _ in range(args.warmup):
+        step([])
+    torch.cuda.synchronize()
+    recs = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(recs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    def ms(a, b):
+        return sum(r[a].elapsed_time(r[b]) for r in recs) / len(recs)
+
+    t_step = ms("start", "ver")
+    t_enc = ms("start", "enc")
+    t_dec = ms("dec0", "dec")
+    t_h2d = ms("h2d0", "h2d")
+    t_merge = ms("merge0", "merge")
+    t_ver = ms("merge", "ver")
+
+    elems = n_layers * T * Hkv * 128 * 2  # K and V elements
+    enc_gbps = elems * ENC_BYTES_PER_ELEM / (t_enc * 1e-3) / 1e9
+    merge_gbps = elems * MERGE_BYTES_PER_ELEM / (t_merge * 1e-3) / 1e9
+    dec_bytes = n_layers * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
+    dec_gbps = dec_bytes / (t_dec * 1e-3) / 1e9
+    h2d_gbps = (sum(h.numel() for h in host_k) * 2) / (t_h2d * 1e-3) / 1e9
+    ver_us = t_ver * 1e3 / n_layers
+    overlap = max(0.0, min(1.0, (t_dec + t_h2d - (ms("dec0", "merge0"))) / min(t_dec, t_h2d)))
+
+    per_launch_bytes = T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
+    per_launch_s = t_dec * 1e-3 / n_layers
+    result = {
+        "metric": METRIC,
+        "value": round(dec_gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{WORKLOAD}: {n_layers} layers x ({Hq} q / {Hkv} kv heads, d=128), "
+                               f"context {T}, batch 1, k={nq} drafts", "layers": n_layers,
+                   "q_heads": Hq, "kv_heads": Hkv, "head_dim": 128, "context": T, "batch": 1,
+                   "drafts": nq},
+        "hbm_frac": round(dec_gbps / HBM_PEAK_GBPS, 4),
+        "stages": {
+            "encode_GBps": round(enc_gbps, 2), "encode_frac": round(enc_gbps / HBM_PEAK_GBPS, 4),
+            "anchor_decode_GBps": round(dec_gbps, 2),
+            "anchor_decode_us_per_layer": round(t_dec * 1e3 / n_layers, 3),
+            "merge_GBps": round(merge_gbps, 2), "merge_frac": round(merge_gbps / HBM_PEAK_GBPS, 4),
+            "verify_us_per_layer": round(ver_us, 2),
+            "residual_h2d_GBps": round(h2d_gbps, 2),
+            "decode_hidden_behind_h2d": round(overlap, 3),
+            "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
+            "setup_s": round(t_setup, 1),
+        },
+        "roofline": {
+            "kernel": "anchor decode (split + combine kernels of one lynx_attn_anchor_decode call)",
+            "bound": "hbm",
+            "achieved": round(per_launch_bytes / per_launch_s / 1e9, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(per_launch_bytes / per_launch_s / 1e9 / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        def layer_inputs(l):
+            return (inputs.kv(w, "k", layer=l, device=dev).cpu(),
+                    inputs.kv(w, "v", layer=l, device=dev).cpu(),
+                    inputs.queries(w, layer=l, device=dev).cpu())
+        result["cpu_baseline"] = cpu_baseline(w, layer_inputs, min(args.cpu_layers, n_layers))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * lynx.h -- C ABI of the Lynx split-stream KV codec and its attention kernels
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Lynx: Progressive Speculative Quantization for accelerating KV
+ * Transfer in Long-Context Inference".  The prefill side quantizes the KV
+ * cache to 8 bits and splits every code into a 4-bit Anchor (most significant
+ * bits, sent first) and a 4-bit Residual (least significant bits, sent
+ * second) (Sec. 4 overview; Alg. 1 stage 4; Sec. 5 Compression Kernel).  The
+ * decode side starts generating from the Anchor alone (Sec. 4.2 Anchor
+ * phase), merges the Residual back into the full 8-bit cache when it arrives
+ * (Sec. 4.2 Residual phase), and verifies the speculative tokens in one
+ * parallel pass over the full cache (Sec. 4.3).
+ *
+ * Conventions for every entry point
+ *   - Pointers named *_bf16, planes, codes, metadata, seq_lens, block_table,
+ *     q, out, lse and workspace are DEVICE pointers (hipMalloc'd or torch
+ *     CUDA tensors).  `L` and `meta` point to small HOST structs read during
+ *     the call.
+ *   - Every device pointer must be 16-byte aligned.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the legacy
+ *     default stream).  The library never allocates, never synchronizes and
+ *     keeps no mutable global state; it is safe to call from several threads.
+ *     Buffers must stay alive until the stream work completes.
+ *   - Arguments are validated before anything is launched; on an error
+ *     nothing is launched and a negative lynx_status is returned.  Faults in
+ *     device memory the caller described wrongly surface at the caller's next
+ *     stream synchronization.
+ *
+ * Data layout (all sizes in bytes; D = head_dim = 128; Hkv kv heads)
+ *   - K/V inputs of one sequence: BF16 [T][Hkv][128], contiguous.
+ *   - Codes: K is grouped per channel over windows of 128 consecutive tokens,
+ *     V per token over its 128 dims (grouped quantization, Sec. 2.3).  For a
+ *     group with minimum mn and maximum mx: zero = mn, scale = (mx-mn)/255,
+ *     code = rint((x - zero) * (255/(mx-mn))) in IEEE fp32 (round half to
+ *     even), clamped to [0, 255].  A group whose range is not a positive
+ *     finite number, or whose 255/(mx-mn) overflows, stores scale 0 and codes
+ *     0.  -0 is stored as +0.  Anchor a = code >> 4, residual r = code & 15.
+ *   - Nibble planes (k_anc, v_anc, k_res, v_res): one 64-byte row per
+ *     (token, kv head); byte j of a row holds dim 2j in its low nibble and dim
+ *     2j+1 in its high nibble.  The row of (sequence b, kv head h, token t)
+ *     starts at  ((block_table[b][t / bt] * Hkv + h) * bt + t % bt) * 64.
+ *     Code planes (k_codes, v_codes) use the same formula with 128-byte rows,
+ *     byte d = the code of dim d.  A contiguous cache is bt >= T with
+ *     block_table[b][0] = b.  Bytes of rows t >= T are never read.
+ *   - Metadata (fp32, logical, never paged), per sequence b:
+ *       k_scale, k_zero [B][Hkv][ceil(max_tokens/128)][128]
+ *       v_scale, v_zero [B][Hkv][max_tokens]
+ *   - Query head hq reads kv head hq / (Hq / Hkv).
+ *
+ * Reconstruction used by the attention kernels
+ *   - Anchor only: zero + (16 a + 7.5) * scale   (|error| <= 8 scale)
+ *   - Full 8-bit:  zero + code * scale           (|error| <= scale / 2)
+ */
+#ifndef LYNX_H
+#define LYNX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum lynx_status {
+    LYNX_OK = 0,
+    LYNX_EINVAL = -1,     /* NULL/misaligned pointer, bad size or count   */
+    LYNX_ENOTSUP = -2,    /* head_dim or k_group_tokens other than 128      */
+    LYNX_EWORKSPACE = -3, /* workspace missing or smaller than required     */
+    LYNX_EHIP = -4        /* the HIP runtime reported a launch error        */
+} lynx_status;
+
+/* Cache geometry shared by every call (host struct). */
+typedef struct lynx_layout {
+    int32_t num_kv_heads;       /* Hkv >= 1                                      */
+    int32_t head_dim;           /* must be 128                                   */
+    int32_t k_group_tokens;     /* must be 128: K group = 128 tokens x 1 channel */
+    int32_t block_tokens;       /* bt >= 1: tokens per plane block               */
+    int32_t max_blocks_per_seq; /* row stride of block_table, >= ceil(T/bt)      */
+    int32_t num_blocks;         /* blocks in the plane pool; block ids must be
+                                   in [0, num_blocks): kernels skip (encode) or
+                                   return NaN for (attention) rows whose block
+                                   id is outside that range                     */
+    int32_t max_tokens;         /* token stride of the metadata arrays, >= T     */
+} lynx_layout;
+
+/* Device pointers to the fp32 metadata of the whole batch (host struct). */
+typedef struct lynx_meta {
+    float *k_scale; /* [B][Hkv][ceil(max_tokens/128)][128] */
+    float *k_zero;
+    float *v_scale; /* [B][Hkv][max_tokens] */
+    float *v_zero;
+} lynx_meta;
+
+/*
+ * lynx_kv_encode -- the prefill-side compression of one sequence (Sec. 4.2
+ * Prefill workflow: the quantization kernel turns a KV object into the Anchor
+ * and Residual streams and their metadata; Alg. 1 stage 4; Sec. 5).
+ *
+ *   b            sequence index: selects block_table row b and metadata row b
+ *   T            tokens to encode, 0 <= T <= min(max_tokens,
+ *                max_blocks_per_seq * bt); T == 0 launches nothing
+ *   block_table  int32 [B][max_blocks_per_seq] (device)
+ *   k_bf16,v_bf16  BF16 [T][Hkv][128] (device, read)
+ *   k_anc, v_anc, k_res, v_res  nibble planes (device, written for rows t < T)
+ *   meta         metadata row b written (K groups 0..ceil(T/128)-1, V tokens < T)
+ * Returns LYNX_OK or an error; launches one kernel.
+ */
+int lynx_kv_encode(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
+                   const void *k_bf16, const void *v_bf16, uint8_t *k_anc, uint8_t *v_anc,
+                   uint8_t *k_res, uint8_t *v_res, const lynx_meta *meta, void *stream);
+
+/*
+ * lynx_kv_merge -- the decode-side Residual phase (Sec. 4.2): anchor and
+ * residual recombine into the full 8-bit code Q_full.  Elementwise and
+ * layout-agnostic: for byte j of the planes,
+ *   codes[2j]   = (anc[j] & 15) << 4 | (res[j] & 15)
+ *   codes[2j+1] = (anc[j] >> 4) << 4 | (res[j] >> 4)
+ * so a nibble-plane pool maps onto a code-plane pool with the same blocks.
+ *   anc, res     n_packed_bytes each (device, read)
+ *   codes        2 * n_packed_bytes (device, written); must not overlap inputs
+ * n_packed_bytes == 0 launches nothing.
+ */
+int lynx_kv_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes,
+                  size_t n_packed_bytes, void *stream);
+
+/*
+ * lynx_attn_workspace_bytes -- device workspace an attention call needs for
+ * its split-context partial results, for `num_queries` query tokens per
+ * sequence (1 for anchor decode, k for verify) and sequences of at most
+ * max_seq_len tokens.  Returns 0 on invalid arguments.
+ */
+size_t lynx_attn_workspace_bytes(const lynx_layout *L, int32_t B, int32_t Hq,
+                                 int32_t num_queries, int32_t max_seq_len);
+
+/*
+ * lynx_attn_anchor_decode -- decode attention over the Anchor-only cache
+ * (Sec. 4.2 Anchor phase; Speculative Decoder): for every sequence b and
+ * query head hq, O = softmax(q K^T / sqrt(128)) V (Sec. 2) with K, V
+ * reconstructed from the anchor nibbles as zero + (16 a + 7.5) scale.
+ *
+ *   B, Hq        batch size and query heads (Hq % Hkv == 0)
+ *   max_seq_len  host upper bound of seq_lens (sizes the launch); tokens at
+ *                or beyond it are ignored
+ *   seq_lens     int32 [B] (device): context length of each sequence
+ *   block_table  int32 [B][max_blocks_per_seq] (device)
+ *   k_anc, v_anc nibble planes (device); meta: metadata of the batch
+ *   q_bf16       BF16 [B][Hq][128] (device)
+ *   out_bf16     BF16 [B][Hq][128] (device, written)
+ *   lse          fp32 [B][Hq] natural-log sum of exp of the scaled scores,
+ *                or NULL (device, written)
+ *   workspace    >= lynx_attn_workspace_bytes(L, B, Hq, 1, max_seq_len)
+ * A sequence with no tokens yields zeros and lse = -inf.
+ */
+int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t max_seq_len,
+                            const int32_t *seq_lens, const int32_t *block_table,
+                            const uint8_t *k_anc, const uint8_t *v_anc, const lynx_meta *meta,
+                            const void *q_bf16, void *out_bf16, float *lse, void *workspace,
+                            size_t workspace_bytes, void *stream);
+
+/*
+ * lynx_attn_verify -- the verification pass (Sec. 4.3): the k speculative
+ * query tokens of every sequence attend, in one parallel pass, over the
+ * merged 8-bit cache (reconstructed as zero + code * scale) and over the
+ * draft tokens' own BF16 K/V, causally: draft query i sees the whole context
+ * and draft tokens 0..i.  k is capped at 64, the paper's limit on speculative
+ * tokens (Sec. 6.1).
+ *
+ *   k            draft queries per sequence, 1 <= k <= 64
+ *   k_codes, v_codes  code planes (device)
+ *   q_bf16       BF16 [B][k][Hq][128] (device)
+ *   k_new, v_new BF16 [B][k][Hkv][128] draft K/V (device), or both NULL to
+ *                attend over the context only
+ *   out_bf16     BF16 [B][k][Hq][128] (device, written)
+ *   workspace    >= lynx_attn_workspace_bytes(L, B, Hq, k, max_seq_len)
+ */
+int lynx_attn_verify(const lynx_layout *L, int32_t B, int32_t Hq, int32_t k,
+                     int32_t max_seq_len, const int32_t *seq_lens, const int32_t *block_table,
+                     const uint8_t *k_codes, const uint8_t *v_codes, const lynx_meta *meta,
+                     const void *q_bf16, const void *k_new, const void *v_new, void *out_bf16,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static, human-readable text for a lynx_status value. */
+const char *lynx_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LYNX_H */

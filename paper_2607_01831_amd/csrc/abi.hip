@@ -1,0 +1,175 @@
+// C ABI of liblynx.so (declared in include/lynx.h): argument validation,
+// workspace sizing and kernel launch.  Validation is synchronous and happens
+// before anything is launched.
+#include "../../include/lynx.h"
+#include "lynx_internal.h"
+
+namespace {
+
+using lynx::Geometry;
+using lynx::MetaPtrs;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Layout checks shared by every call; fills the kernel-side geometry.
+int check_layout(const lynx_layout *L, Geometry *g) {
+    if (!L) return LYNX_EINVAL;
+    if (L->head_dim != lynx::kHeadDim || L->k_group_tokens != lynx::kKGroup) return LYNX_ENOTSUP;
+    if (L->num_kv_heads < 1 || L->block_tokens < 1 || L->max_blocks_per_seq < 1 ||
+        L->num_blocks < 1 || L->max_tokens < 1)
+        return LYNX_EINVAL;
+    g->Hkv = L->num_kv_heads;
+    g->bt = L->block_tokens;
+    g->max_blocks = L->max_blocks_per_seq;
+    g->num_blocks = L->num_blocks;
+    g->max_tokens = L->max_tokens;
+    g->n_groups = (L->max_tokens + lynx::kKGroup - 1) / lynx::kKGroup;
+    return LYNX_OK;
+}
+
+int check_meta(const lynx_meta *meta, MetaPtrs *mp) {
+    if (!meta || !meta->k_scale || !meta->k_zero || !meta->v_scale || !meta->v_zero)
+        return LYNX_EINVAL;
+    if (!aligned16(meta->k_scale) || !aligned16(meta->k_zero) || !aligned16(meta->v_scale) ||
+        !aligned16(meta->v_zero))
+        return LYNX_EINVAL;
+    *mp = MetaPtrs{meta->k_scale, meta->k_zero, meta->v_scale, meta->v_zero};
+    return LYNX_OK;
+}
+
+// Tokens a sequence may hold under this layout.
+long long layout_capacity(const Geometry &g) {
+    const long long paged = (long long)g.max_blocks * g.bt;
+    return paged < g.max_tokens ? paged : g.max_tokens;
+}
+
+int check_attention_common(const lynx_layout *L, int32_t B, int32_t Hq, int32_t max_seq_len,
+                           const int32_t *seq_lens, const int32_t *block_table,
+                           const uint8_t *k_plane, const uint8_t *v_plane, const lynx_meta *meta,
+                           const void *q, void *out, Geometry *g, MetaPtrs *mp) {
+    int rc = check_layout(L, g);
+    if (rc != LYNX_OK) return rc;
+    if ((rc = check_meta(meta, mp)) != LYNX_OK) return rc;
+    if (B < 0 || Hq < 1 || Hq % g->Hkv != 0 || max_seq_len < 0) return LYNX_EINVAL;
+    if (max_seq_len > layout_capacity(*g)) return LYNX_EINVAL;
+    if (B == 0) return LYNX_OK;
+    const void *ptrs[] = {seq_lens, block_table, k_plane, v_plane, q, out};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    return LYNX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *lynx_strerror(int status) {
+    switch (status) {
+    case LYNX_OK: return "success";
+    case LYNX_EINVAL: return "invalid argument (NULL or misaligned pointer, bad size or count)";
+    case LYNX_ENOTSUP: return "unsupported geometry (head_dim and k_group_tokens must be 128)";
+    case LYNX_EWORKSPACE: return "workspace missing or smaller than lynx_attn_workspace_bytes()";
+    case LYNX_EHIP: return "HIP runtime reported a launch error";
+    default: return "unknown lynx status";
+    }
+}
+
+int lynx_kv_encode(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
+                   const void *k_bf16, const void *v_bf16, uint8_t *k_anc, uint8_t *v_anc,
+                   uint8_t *k_res, uint8_t *v_res, const lynx_meta *meta, void *stream) {
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_layout(L, &g);
+    if (rc != LYNX_OK) return rc;
+    if ((rc = check_meta(meta, &mp)) != LYNX_OK) return rc;
+    if (b < 0 || T < 0 || T > layout_capacity(g)) return LYNX_EINVAL;
+    if (T == 0) return LYNX_OK;
+    const void *ptrs[] = {block_table, k_bf16, v_bf16, k_anc, v_anc, k_res, v_res};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    hipError_t e = lynx::launch_encode(g, b, T, block_table,
+                                       static_cast<const uint16_t *>(k_bf16),
+                                       static_cast<const uint16_t *>(v_bf16), k_anc, v_anc, k_res,
+                                       v_res, mp, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_kv_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t n_packed_bytes,
+                  void *stream) {
+    if (n_packed_bytes == 0) return LYNX_OK;
+    if (!anc || !res || !codes || !aligned16(anc) || !aligned16(res) || !aligned16(codes))
+        return LYNX_EINVAL;
+    // the output must not overlap either input
+    const uintptr_t c0 = reinterpret_cast<uintptr_t>(codes), c1 = c0 + 2 * n_packed_bytes;
+    for (const uint8_t *in : {anc, res}) {
+        const uintptr_t i0 = reinterpret_cast<uintptr_t>(in), i1 = i0 + n_packed_bytes;
+        if (i0 < c1 && c0 < i1) return LYNX_EINVAL;
+    }
+    hipError_t e = lynx::launch_merge(anc, res, codes, n_packed_bytes,
+                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+size_t lynx_attn_workspace_bytes(const lynx_layout *L, int32_t B, int32_t Hq,
+                                 int32_t num_queries, int32_t max_seq_len) {
+    Geometry g;
+    if (check_layout(L, &g) != LYNX_OK) return 0;
+    if (B < 0 || Hq < 1 || Hq % g.Hkv != 0 || num_queries < 1 || num_queries > 64 ||
+        max_seq_len < 0)
+        return 0;
+    // sized for the larger plan, the one with a draft-tail split
+    const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, num_queries, max_seq_len, true);
+    return p.o_bytes + p.ml_bytes;
+}
+
+int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t max_seq_len,
+                            const int32_t *seq_lens, const int32_t *block_table,
+                            const uint8_t *k_anc, const uint8_t *v_anc, const lynx_meta *meta,
+                            const void *q_bf16, void *out_bf16, float *lse, void *workspace,
+                            size_t workspace_bytes, void *stream) {
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_attention_common(L, B, Hq, max_seq_len, seq_lens, block_table, k_anc, v_anc,
+                                    meta, q_bf16, out_bf16, &g, &mp);
+    if (rc != LYNX_OK) return rc;
+    if (B == 0) return LYNX_OK;
+    if (lse && !aligned16(lse)) return LYNX_EINVAL;
+    const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, 1, max_seq_len, false);
+    if (p.o_bytes + p.ml_bytes > 0 &&
+        (!workspace || !aligned16(workspace) || workspace_bytes < p.o_bytes + p.ml_bytes))
+        return LYNX_EWORKSPACE;
+    hipError_t e = lynx::launch_attention(
+        lynx::KvMode::kAnchor, g, p, B, Hq, 1, max_seq_len, seq_lens, block_table, k_anc, v_anc,
+        mp, static_cast<const uint16_t *>(q_bf16), nullptr, nullptr,
+        static_cast<uint16_t *>(out_bf16), lse, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_attn_verify(const lynx_layout *L, int32_t B, int32_t Hq, int32_t k,
+                     int32_t max_seq_len, const int32_t *seq_lens, const int32_t *block_table,
+                     const uint8_t *k_codes, const uint8_t *v_codes, const lynx_meta *meta,
+                     const void *q_bf16, const void *k_new, const void *v_new, void *out_bf16,
+                     void *workspace, size_t workspace_bytes, void *stream) {
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_attention_common(L, B, Hq, max_seq_len, seq_lens, block_table, k_codes,
+                                    v_codes, meta, q_bf16, out_bf16, &g, &mp);
+    if (rc != LYNX_OK) return rc;
+    if (k < 1 || k > 64) return LYNX_EINVAL;
+    if ((k_new == nullptr) != (v_new == nullptr)) return LYNX_EINVAL;
+    if (k_new && (!aligned16(k_new) || !aligned16(v_new))) return LYNX_EINVAL;
+    if (B == 0) return LYNX_OK;
+    const bool tail = k_new != nullptr;
+    const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, k, max_seq_len, tail);
+    if (p.o_bytes + p.ml_bytes > 0 &&
+        (!workspace || !aligned16(workspace) || workspace_bytes < p.o_bytes + p.ml_bytes))
+        return LYNX_EWORKSPACE;
+    hipError_t e = lynx::launch_attention(
+        lynx::KvMode::kCodes, g, p, B, Hq, k, max_seq_len, seq_lens, block_table, k_codes, v_codes,
+        mp, static_cast<const uint16_t *>(q_bf16), static_cast<const uint16_t *>(k_new),
+        static_cast<const uint16_t *>(v_new), static_cast<uint16_t *>(out_bf16), nullptr,
+        workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+}  // extern "C"

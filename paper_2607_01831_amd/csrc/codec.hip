@@ -1,0 +1,309 @@
+// Split-stream KV codec kernels for gfx950: encode (quantize, split, pack)
+// and merge (anchor + residual -> 8-bit codes).
+//
+// Encode follows the grouped linear quantization of Sec. 2.3 (zero = group
+// minimum, scale = range / 255) and the split-stream construction of Alg. 1
+// stage 4 (anchor = the 4 most significant bits, residual = the 4 least
+// significant bits), packing two 4-bit values per byte as the Compression
+// Kernel of Sec. 5 does.  Merge is the Residual phase of Sec. 4.2.
+//
+// The fp32 arithmetic that decides a code is spelled out operation by
+// operation (sub, mul, round-half-even, clamp; one IEEE division per group)
+// so that every code is the one the definition gives.
+#include "lynx_internal.h"
+
+#include <float.h>
+
+namespace lynx {
+namespace {
+
+constexpr int kEncodeThreads = 256;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Eight BF16 values held in a uint4 -> floats.
+__device__ __forceinline__ void unpack8(const uint4 &u, float *x) {
+    x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x);
+    x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
+    x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z);
+    x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
+}
+
+// Group statistics from the group's min and max: zero, scale, inverse range.
+__device__ __forceinline__ void group_params(float mn, float mx, float &zero, float &scale,
+                                             float &inv) {
+    if (mn == 0.0f) mn = 0.0f;  // -0 -> +0
+    if (mx == 0.0f) mx = 0.0f;
+    const float range = mx - mn;
+    const float r = 255.0f / range;  // correctly rounded IEEE division
+    if (!(range > 0.0f) || !(range <= FLT_MAX) || !(r <= FLT_MAX)) {
+        scale = 0.0f;
+        inv = 0.0f;
+    } else {
+        scale = range / 255.0f;
+        inv = r;
+    }
+    zero = mn;
+}
+
+__device__ __forceinline__ uint32_t quantize(float x, float zero, float inv) {
+    const float y = (x - zero) * inv;
+    float c = rintf(y);
+    c = (c >= 0.0f) ? c : 0.0f;  // NaN -> 0
+    c = (c > 255.0f) ? 255.0f : c;
+    return (uint32_t)c;
+}
+
+// Eight codes (dims 8m..8m+7) -> one 32-bit word of anchor nibbles and one of
+// residual nibbles; nibble j of the word is dim 8m+j (low nibble = even dim).
+__device__ __forceinline__ void split_pack8(const uint32_t *c, uint32_t &anc, uint32_t &res) {
+    anc = 0;
+    res = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        anc |= (c[j] >> 4) << (4 * j);
+        res |= (c[j] & 15u) << (4 * j);
+    }
+}
+
+__device__ __forceinline__ float wave_min_xor(float v, int lane_mask) {
+    return fminf(v, __shfl_xor(v, lane_mask));
+}
+__device__ __forceinline__ float wave_max_xor(float v, int lane_mask) {
+    return fmaxf(v, __shfl_xor(v, lane_mask));
+}
+
+// One workgroup encodes one 128-token window of one kv head for K and V.
+// Thread (tr = tid / 16, m = tid % 16) owns dims 8m..8m+7 of the window's
+// tokens tr, tr+16, ..., tr+112: every 16-byte load is part of a fully used
+// 256-byte token row, and a token's 16 owners are 16 adjacent lanes.
+__global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
+    Geometry geo, int b, int T, const int32_t *__restrict__ block_table,
+    const uint16_t *__restrict__ k, const uint16_t *__restrict__ v, uint8_t *__restrict__ k_anc,
+    uint8_t *__restrict__ v_anc, uint8_t *__restrict__ k_res, uint8_t *__restrict__ v_res,
+    MetaPtrs meta) {
+    const int g = blockIdx.x;
+    const int h = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int m = tid & 15;
+    const int tr = tid >> 4;
+    const int wave = tid >> 6;
+    const int t0 = g * kKGroup;
+    const int n = min(kKGroup, T - t0);
+    const int Hkv = geo.Hkv;
+
+    __shared__ float s_min[4][kHeadDim];
+    __shared__ float s_max[4][kHeadDim];
+    __shared__ float s_zero[kHeadDim];
+    __shared__ float s_inv[kHeadDim];
+
+    // ---- load the window: 8 tokens x 8 dims per thread, for K and V ----
+    uint4 kraw[8], vraw[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int tl = tr + 16 * i;
+        if (tl < n) {
+            const size_t e = ((size_t)(t0 + tl) * Hkv + h) * kHeadDim + 8 * m;
+            kraw[i] = *reinterpret_cast<const uint4 *>(k + e);
+            vraw[i] = *reinterpret_cast<const uint4 *>(v + e);
+        } else {
+            kraw[i] = make_uint4(0, 0, 0, 0);
+            vraw[i] = make_uint4(0, 0, 0, 0);
+        }
+    }
+
+    // ---- K: per-channel min/max over the window's valid tokens ----
+    float kmin[8], kmax[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        kmin[j] = FLT_MAX * 2.0f;   // +inf
+        kmax[j] = -FLT_MAX * 2.0f;  // -inf
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        if (tr + 16 * i < n) {
+            float x[8];
+            unpack8(kraw[i], x);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                kmin[j] = fminf(kmin[j], x[j]);
+                kmax[j] = fmaxf(kmax[j], x[j]);
+            }
+        }
+    }
+    // lanes m, m+16, m+32, m+48 of a wave hold the same channels
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        kmin[j] = wave_min_xor(wave_min_xor(kmin[j], 16), 32);
+        kmax[j] = wave_max_xor(wave_max_xor(kmax[j], 16), 32);
+    }
+    if ((tid & 63) < 16) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            s_min[wave][8 * m + j] = kmin[j];
+            s_max[wave][8 * m + j] = kmax[j];
+        }
+    }
+    __syncthreads();
+    if (tid < kHeadDim) {
+        const int d = tid;
+        const float mn = fminf(fminf(s_min[0][d], s_min[1][d]), fminf(s_min[2][d], s_min[3][d]));
+        const float mx = fmaxf(fmaxf(s_max[0][d], s_max[1][d]), fmaxf(s_max[2][d], s_max[3][d]));
+        float zero, scale, inv;
+        group_params(mn, mx, zero, scale, inv);
+        s_zero[d] = zero;
+        s_inv[d] = inv;
+        const size_t mi = (((size_t)b * Hkv + h) * geo.n_groups + g) * kHeadDim + d;
+        meta.k_scale[mi] = scale;
+        meta.k_zero[mi] = zero;
+    }
+    __syncthreads();
+
+    float kz[8], ki[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        kz[j] = s_zero[8 * m + j];
+        ki[j] = s_inv[8 * m + j];
+    }
+
+    const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
+
+    // ---- K codes -> planes ----
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int tl = tr + 16 * i;
+        if (tl < n) {
+            const int t = t0 + tl;
+            const int blk = bt_row[t / geo.bt];
+            if (blk >= 0 && blk < geo.num_blocks) {
+                float x[8];
+                uint32_t c[8];
+                unpack8(kraw[i], x);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) c[j] = quantize(x[j], kz[j], ki[j]);
+                uint32_t a, r;
+                split_pack8(c, a, r);
+                const size_t off =
+                    (((size_t)blk * Hkv + h) * geo.bt + (t % geo.bt)) * kNibbleRow + 4 * m;
+                *reinterpret_cast<uint32_t *>(k_anc + off) = a;
+                *reinterpret_cast<uint32_t *>(k_res + off) = r;
+            }
+        }
+    }
+
+    // ---- V: per-token groups over 128 dims (16 adjacent lanes per token) ----
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int tl = tr + 16 * i;
+        float x[8];
+        unpack8(vraw[i], x);
+        float mn = x[0], mx = x[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) {
+            mn = fminf(mn, x[j]);
+            mx = fmaxf(mx, x[j]);
+        }
+#pragma unroll
+        for (int s = 1; s < 16; s <<= 1) {
+            mn = wave_min_xor(mn, s);
+            mx = wave_max_xor(mx, s);
+        }
+        if (tl < n) {
+            const int t = t0 + tl;
+            float zero, scale, inv;
+            group_params(mn, mx, zero, scale, inv);
+            if (m == 0) {
+                const size_t mi = ((size_t)b * Hkv + h) * geo.max_tokens + t;
+                meta.v_scale[mi] = scale;
+                meta.v_zero[mi] = zero;
+            }
+            const int blk = bt_row[t / geo.bt];
+            if (blk >= 0 && blk < geo.num_blocks) {
+                uint32_t c[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) c[j] = quantize(x[j], zero, inv);
+                uint32_t a, r;
+                split_pack8(c, a, r);
+                const size_t off =
+                    (((size_t)blk * Hkv + h) * geo.bt + (t % geo.bt)) * kNibbleRow + 4 * m;
+                *reinterpret_cast<uint32_t *>(v_anc + off) = a;
+                *reinterpret_cast<uint32_t *>(v_res + off) = r;
+            }
+        }
+    }
+}
+
+// Interleave the nibbles of 4 anchor bytes and 4 residual bytes into 8 codes:
+// code[2j] = (a_j & 15) << 4 | (r_j & 15), code[2j+1] = (a_j & 0xF0) | (r_j >> 4).
+__device__ __forceinline__ uint2 merge4(uint32_t a, uint32_t r) {
+    // spread bytes 0,1 (lo) and 2,3 (hi) into 16-bit lanes
+    const uint32_t alo = (a & 0xffu) | ((a & 0xff00u) << 8);
+    const uint32_t ahi = ((a >> 16) & 0xffu) | ((a >> 8) & 0xff0000u);
+    const uint32_t rlo = (r & 0xffu) | ((r & 0xff00u) << 8);
+    const uint32_t rhi = ((r >> 16) & 0xffu) | ((r >> 8) & 0xff0000u);
+    uint2 o;
+    o.x = ((alo & 0x000F000Fu) << 4) | ((alo & 0x00F000F0u) << 8) | (rlo & 0x000F000Fu) |
+          ((rlo & 0x00F000F0u) << 4);
+    o.y = ((ahi & 0x000F000Fu) << 4) | ((ahi & 0x00F000F0u) << 8) | (rhi & 0x000F000Fu) |
+          ((rhi & 0x00F000F0u) << 4);
+    return o;
+}
+
+constexpr int kMergeThreads = 256;
+
+// Each thread merges 16 anchor + 16 residual bytes into 32 code bytes per
+// iteration of a grid-stride loop; 16-byte loads, two 16-byte stores.
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(
+    const uint4 *__restrict__ anc, const uint4 *__restrict__ res, uint4 *__restrict__ codes,
+    size_t n16, const uint8_t *__restrict__ anc_b, const uint8_t *__restrict__ res_b,
+    uint8_t *__restrict__ codes_b, size_t n_packed) {
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) {
+        const uint4 a = anc[i];
+        const uint4 r = res[i];
+        const uint2 c0 = merge4(a.x, r.x);
+        const uint2 c1 = merge4(a.y, r.y);
+        const uint2 c2 = merge4(a.z, r.z);
+        const uint2 c3 = merge4(a.w, r.w);
+        codes[2 * i] = make_uint4(c0.x, c0.y, c1.x, c1.y);
+        codes[2 * i + 1] = make_uint4(c2.x, c2.y, c3.x, c3.y);
+    }
+    // ragged tail (< 16 bytes)
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        for (size_t j = n16 * 16; j < n_packed; ++j) {
+            const uint32_t a = anc_b[j], r = res_b[j];
+            codes_b[2 * j] = (uint8_t)(((a & 15u) << 4) | (r & 15u));
+            codes_b[2 * j + 1] = (uint8_t)((a & 0xF0u) | (r >> 4));
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_table,
+                         const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
+                         uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream) {
+    if (T <= 0) return hipSuccess;
+    dim3 grid((T + kKGroup - 1) / kKGroup, g.Hkv);
+    hipLaunchKernelGGL(encode_kernel, grid, dim3(kEncodeThreads), 0, stream, g, b, T,
+                       block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
+    return hipGetLastError();
+}
+
+hipError_t launch_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t n_packed,
+                        hipStream_t stream) {
+    if (n_packed == 0) return hipSuccess;
+    const size_t n16 = n_packed / 16;
+    // enough workgroups to cover the device several times over; each thread
+    // then loops over the rest
+    size_t blocks = (n16 + kMergeThreads - 1) / kMergeThreads;
+    if (blocks > 256 * 32) blocks = 256 * 32;
+    if (blocks == 0) blocks = 1;
+    hipLaunchKernelGGL(merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, stream,
+                       reinterpret_cast<const uint4 *>(anc), reinterpret_cast<const uint4 *>(res),
+                       reinterpret_cast<uint4 *>(codes), n16, anc, res, codes, n_packed);
+    return hipGetLastError();
+}
+
+}  // namespace lynx

@@ -1,0 +1,61 @@
+// Internal declarations shared by the HIP translation units of liblynx.so.
+// Not part of the public ABI (include/lynx.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lynx {
+
+constexpr int kHeadDim = 128;    // D
+constexpr int kKGroup = 128;     // tokens per K quantization group
+constexpr int kNibbleRow = 64;   // bytes per token row of a nibble plane
+constexpr int kCodeRow = 128;    // bytes per token row of a code plane
+
+// Geometry of a plane pool as the kernels see it.
+struct Geometry {
+    int Hkv;
+    int bt;            // tokens per block
+    int max_blocks;    // block_table row stride
+    int num_blocks;    // valid block ids are [0, num_blocks)
+    int max_tokens;    // metadata token stride
+    int n_groups;      // ceil(max_tokens / 128): K metadata group stride
+};
+
+struct MetaPtrs {
+    float *k_scale, *k_zero, *v_scale, *v_zero;
+};
+
+// ---- encode / merge (codec.hip) ---------------------------------------------
+hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_table,
+                         const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
+                         uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream);
+
+hipError_t launch_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t n_packed,
+                        hipStream_t stream);
+
+// ---- attention (attention.hip) ----------------------------------------------
+enum class KvMode : int { kAnchor = 0, kCodes = 1 };
+
+struct AttnPlan {
+    int rows_total;   // nq * G query rows per (sequence, kv head)
+    int rows_chunk;   // rows handled by one workgroup (1, 2, 4 or 8)
+    int n_chunks;     // ceil(rows_total / rows_chunk)
+    int split_tokens; // context tokens per split
+    int n_ctx_splits; // ceil(max_seq_len / split_tokens)
+    int n_splits;     // n_ctx_splits (+1 when a BF16 draft tail is attended)
+    size_t o_bytes;   // workspace bytes for the partial outputs
+    size_t ml_bytes;  // workspace bytes for the partial (max, sum) pairs
+};
+
+AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_len, bool tail);
+
+hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan, int B, int Hq,
+                            int nq, int max_seq_len, const int32_t *seq_lens,
+                            const int32_t *block_table, const uint8_t *k_plane,
+                            const uint8_t *v_plane, MetaPtrs meta, const uint16_t *q,
+                            const uint16_t *k_new, const uint16_t *v_new, uint16_t *out,
+                            float *lse, void *workspace, hipStream_t stream);
+
+}  // namespace lynx

@@ -1,0 +1,239 @@
+"""Python binding of liblynx.so (include/lynx.h): argument marshalling only.
+
+Every function has the name and argument order of its C entry point.  Tensors
+are torch CUDA tensors; their device pointers and the current HIP stream are
+passed through ctypes.  Nothing here computes any part of the method: if the
+library is missing the binding raises instead of falling back to anything.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from pathlib import Path
+
+import torch
+
+LIBRARY = Path(__file__).resolve().parent / "liblynx.so"
+
+LYNX_OK, LYNX_EINVAL, LYNX_ENOTSUP, LYNX_EWORKSPACE, LYNX_EHIP = 0, -1, -2, -3, -4
+HEAD_DIM = 128
+K_GROUP = 128
+MAX_DRAFTS = 64
+
+
+class LynxError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {lynx_strerror(status)} ({status})")
+
+
+class lynx_layout(ctypes.Structure):
+    _fields_ = [("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("k_group_tokens", ctypes.c_int32), ("block_tokens", ctypes.c_int32),
+                ("max_blocks_per_seq", ctypes.c_int32), ("num_blocks", ctypes.c_int32),
+                ("max_tokens", ctypes.c_int32)]
+
+
+class lynx_meta(ctypes.Structure):
+    _fields_ = [("k_scale", ctypes.c_void_p), ("k_zero", ctypes.c_void_p),
+                ("v_scale", ctypes.c_void_p), ("v_zero", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load():
+    """Load liblynx.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not LIBRARY.exists():
+        raise RuntimeError(f"{LIBRARY} is not built: run `python -m paper_2607_01831_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(str(LIBRARY))
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    LP, MP = ctypes.POINTER(lynx_layout), ctypes.POINTER(lynx_meta)
+    sigs = {
+        "lynx_kv_encode": ([LP, I32, I32, P, P, P, P, P, P, P, MP, P], ctypes.c_int),
+        "lynx_kv_merge": ([P, P, P, SZ, P], ctypes.c_int),
+        "lynx_attn_workspace_bytes": ([LP, I32, I32, I32, I32], SZ),
+        "lynx_attn_anchor_decode": ([LP, I32, I32, I32, P, P, P, P, MP, P, P, P, P, SZ, P],
+                                    ctypes.c_int),
+        "lynx_attn_verify": ([LP, I32, I32, I32, I32, P, P, P, P, MP, P, P, P, P, P, SZ, P],
+                             ctypes.c_int),
+        "lynx_strerror": ([ctypes.c_int], ctypes.c_char_p),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def lynx_strerror(status: int) -> str:
+    return load().lynx_strerror(status).decode()
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("liblynx takes device tensors")
+    if not t.is_contiguous():
+        raise ValueError("liblynx takes contiguous tensors")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return stream
+
+
+def _check(fn: str, status: int):
+    if status != LYNX_OK:
+        raise LynxError(fn, status)
+
+
+@dataclass
+class Layout:
+    """Cache geometry (see lynx_layout in include/lynx.h)."""
+    num_kv_heads: int
+    block_tokens: int
+    max_blocks_per_seq: int
+    num_blocks: int
+    max_tokens: int
+    head_dim: int = HEAD_DIM
+    k_group_tokens: int = K_GROUP
+
+    def c(self) -> lynx_layout:
+        return lynx_layout(self.num_kv_heads, self.head_dim, self.k_group_tokens,
+                           self.block_tokens, self.max_blocks_per_seq, self.num_blocks,
+                           self.max_tokens)
+
+    @property
+    def n_groups(self) -> int:
+        return -(-self.max_tokens // K_GROUP)
+
+    def plane_bytes(self, row_bytes: int = 64) -> int:
+        return self.num_blocks * self.num_kv_heads * self.block_tokens * row_bytes
+
+
+@dataclass
+class Meta:
+    """fp32 metadata tensors of a batch (device)."""
+    k_scale: torch.Tensor  # [B][Hkv][n_groups][128]
+    k_zero: torch.Tensor
+    v_scale: torch.Tensor  # [B][Hkv][max_tokens]
+    v_zero: torch.Tensor
+
+    @staticmethod
+    def empty(L: Layout, B: int, device="cuda") -> "Meta":
+        ks = (B, L.num_kv_heads, L.n_groups, HEAD_DIM)
+        vs = (B, L.num_kv_heads, L.max_tokens)
+        f = dict(dtype=torch.float32, device=device)
+        return Meta(torch.zeros(ks, **f), torch.zeros(ks, **f), torch.zeros(vs, **f),
+                    torch.zeros(vs, **f))
+
+    def c(self) -> lynx_meta:
+        return lynx_meta(_ptr(self.k_scale), _ptr(self.k_zero), _ptr(self.v_scale),
+                         _ptr(self.v_zero))
+
+
+def lynx_kv_encode(L: Layout, b: int, T: int, block_table, k, v, k_anc, v_anc, k_res, v_res,
+                   meta: Meta, stream=None) -> None:
+    lay, met = L.c(), meta.c()
+    _check("lynx_kv_encode", load().lynx_kv_encode(
+        ctypes.byref(lay), b, T, _ptr(block_table), _ptr(k), _ptr(v), _ptr(k_anc), _ptr(v_anc),
+        _ptr(k_res), _ptr(v_res), ctypes.byref(met), _stream(stream)))
+
+
+def lynx_kv_merge(anc, res, codes, n_packed_bytes: int | None = None, stream=None) -> None:
+    n = anc.numel() if n_packed_bytes is None else n_packed_bytes
+    _check("lynx_kv_merge", load().lynx_kv_merge(_ptr(anc), _ptr(res), _ptr(codes), n,
+                                                 _stream(stream)))
+
+
+def lynx_attn_workspace_bytes(L: Layout, B: int, Hq: int, num_queries: int,
+                              max_seq_len: int) -> int:
+    lay = L.c()
+    return int(load().lynx_attn_workspace_bytes(ctypes.byref(lay), B, Hq, num_queries,
+                                                 max_seq_len))
+
+
+def workspace(L: Layout, B: int, Hq: int, num_queries: int, max_seq_len: int,
+              device="cuda") -> torch.Tensor:
+    """A device buffer of lynx_attn_workspace_bytes() bytes (allocated by torch)."""
+    n = lynx_attn_workspace_bytes(L, B, Hq, num_queries, max_seq_len)
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+
+
+def lynx_attn_anchor_decode(L: Layout, B: int, Hq: int, max_seq_len: int, seq_lens,
+                            block_table, k_anc, v_anc, meta: Meta, q, out, lse=None,
+                            workspace_buf=None, stream=None) -> None:
+    lay, met = L.c(), meta.c()
+    ws = workspace_buf
+    _check("lynx_attn_anchor_decode", load().lynx_attn_anchor_decode(
+        ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table), _ptr(k_anc),
+        _ptr(v_anc), ctypes.byref(met), _ptr(q), _ptr(out), _ptr(lse), _ptr(ws),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def lynx_attn_verify(L: Layout, B: int, Hq: int, k: int, max_seq_len: int, seq_lens,
+                     block_table, k_codes, v_codes, meta: Meta, q, k_new, v_new, out,
+                     workspace_buf=None, stream=None) -> None:
+    lay, met = L.c(), meta.c()
+    ws = workspace_buf
+    _check("lynx_attn_verify", load().lynx_attn_verify(
+        ctypes.byref(lay), B, Hq, k, max_seq_len, _ptr(seq_lens), _ptr(block_table),
+        _ptr(k_codes), _ptr(v_codes), ctypes.byref(met), _ptr(q), _ptr(k_new), _ptr(v_new),
+        _ptr(out), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+# ----------------------------------------------------------------------------
+# Allocation helpers (torch device memory only)
+# ----------------------------------------------------------------------------
+
+@dataclass
+class KVPool:
+    """Nibble planes, metadata and (after merge) code planes of one layer."""
+    layout: Layout
+    B: int
+    k_anc: torch.Tensor
+    v_anc: torch.Tensor
+    k_res: torch.Tensor
+    v_res: torch.Tensor
+    meta: Meta
+    k_codes: torch.Tensor | None = None
+    v_codes: torch.Tensor | None = None
+
+    @staticmethod
+    def allocate(L: Layout, B: int, device="cuda", codes: bool = True) -> "KVPool":
+        n = L.plane_bytes(64)
+        u8 = dict(dtype=torch.uint8, device=device)
+        pool = KVPool(L, B, torch.zeros(n, **u8), torch.zeros(n, **u8), torch.zeros(n, **u8),
+                      torch.zeros(n, **u8), Meta.empty(L, B, device))
+        if codes:
+            pool.k_codes = torch.zeros(2 * n, **u8)
+            pool.v_codes = torch.zeros(2 * n, **u8)
+        return pool
+
+    def encode(self, b: int, T: int, block_table, k, v, stream=None) -> None:
+        lynx_kv_encode(self.layout, b, T, block_table, k, v, self.k_anc, self.v_anc, self.k_res,
+                       self.v_res, self.meta, stream)
+
+    def merge(self, stream=None) -> None:
+        lynx_kv_merge(self.k_anc, self.k_res, self.k_codes, stream=stream)
+        lynx_kv_merge(self.v_anc, self.v_res, self.v_codes, stream=stream)
+
+
+def contiguous_layout(Hkv: int, B: int, T: int) -> Layout:
+    """One block of T tokens per sequence; block_table[b] = [b]."""
+    return Layout(num_kv_heads=Hkv, block_tokens=T, max_blocks_per_seq=1, num_blocks=B,
+                  max_tokens=T)

@@ -1,0 +1,118 @@
+"""Host-side checks of liblynx.so that need no GPU: it loads, exports every
+entry point include/lynx.h declares, and its synchronous argument validation
+rejects bad calls before touching the device."""
+import ctypes
+import re
+import subprocess
+from pathlib import Path
+
+import pytest
+
+ROOT = Path(__file__).resolve().parent.parent
+HEADER = ROOT / "include" / "lynx.h"
+
+
+def declared_functions():
+    text = HEADER.read_text()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lynx_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2607_01831_amd import lynx
+    if not lynx.LIBRARY.exists():
+        from paper_2607_01831_amd import build
+        build.build()
+    return lynx.load()
+
+
+def test_header_declares_the_four_operations():
+    fns = declared_functions()
+    for name in ("lynx_kv_encode", "lynx_kv_merge", "lynx_attn_anchor_decode",
+                 "lynx_attn_verify", "lynx_attn_workspace_bytes", "lynx_strerror"):
+        assert name in fns
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", str(lib._name)], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\b(lynx_[a-z_]+)\b", out))
+    assert set(declared_functions()) <= exported
+    assert "oracle_" not in out  # the product library holds no oracle code
+
+
+def test_strerror(lib):
+    from paper_2607_01831_amd import lynx
+    assert lynx.lynx_strerror(0) == "success"
+    for s in (-1, -2, -3, -4):
+        assert "unknown" not in lynx.lynx_strerror(s)
+
+
+def _layout(**kw):
+    from paper_2607_01831_amd import lynx
+    base = dict(num_kv_heads=8, block_tokens=16, max_blocks_per_seq=4, num_blocks=64,
+                max_tokens=64)
+    base.update(kw)
+    return lynx.Layout(**base)
+
+
+def test_workspace_bytes_host_only(lib):
+    from paper_2607_01831_amd import lynx
+    L = _layout()
+    n1 = lynx.lynx_attn_workspace_bytes(L, 2, 32, 1, 64)
+    n8 = lynx.lynx_attn_workspace_bytes(L, 2, 32, 8, 64)
+    assert 0 < n1 < n8
+    assert lynx.lynx_attn_workspace_bytes(L, 2, 30, 1, 64) == 0       # Hq % Hkv != 0
+    assert lynx.lynx_attn_workspace_bytes(L, 2, 32, 65, 64) == 0      # k > 64
+    assert lynx.lynx_attn_workspace_bytes(_layout(head_dim=64), 2, 32, 1, 64) == 0
+
+
+def test_validation_rejects_before_launch(lib):
+    """Calls with bad arguments return an error code and launch nothing (the
+    pointers below are never dereferenced: validation fails first)."""
+    from paper_2607_01831_amd import lynx
+    L = _layout()
+    lay = L.c()
+    meta = lynx.lynx_meta(16, 32, 48, 64)
+    bad_meta = lynx.lynx_meta(16, 0, 48, 64)
+    E = lynx
+    # encode: NULL meta pointer, unsupported head_dim, T beyond capacity, misaligned input
+    assert lib.lynx_kv_encode(ctypes.byref(lay), 0, 10, 16, 16, 16, 16, 16, 16, 16,
+                              ctypes.byref(bad_meta), None) == E.LYNX_EINVAL
+    lay64 = _layout(head_dim=64).c()
+    assert lib.lynx_kv_encode(ctypes.byref(lay64), 0, 10, 16, 16, 16, 16, 16, 16, 16,
+                              ctypes.byref(meta), None) == E.LYNX_ENOTSUP
+    assert lib.lynx_kv_encode(ctypes.byref(lay), 0, 65, 16, 16, 16, 16, 16, 16, 16,
+                              ctypes.byref(meta), None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_encode(ctypes.byref(lay), 0, 10, 16, 18, 16, 16, 16, 16, 16,
+                              ctypes.byref(meta), None) == E.LYNX_EINVAL
+    # merge: NULL, misaligned, overlapping output
+    assert lib.lynx_kv_merge(None, 16, 4096, 64, None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_merge(16, 40, 4096, 64, None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_merge(4096, 16, 4096 + 32, 64, None) == E.LYNX_EINVAL  # codes overlap anc
+    assert lib.lynx_kv_merge(16, 4096, 4096 - 64, 64, None) == E.LYNX_EINVAL  # codes overlap res
+    assert lib.lynx_kv_merge(16, 32, 64, 0, None) == E.LYNX_OK  # nothing to do
+    # attention: Hq not a multiple of Hkv, k out of range, tail half given, workspace
+    args = (16, 16, 16, 16, ctypes.byref(meta), 16, 16)
+    assert lib.lynx_attn_anchor_decode(ctypes.byref(lay), 1, 12, 64, *args, None, None, 0,
+                                       None) == E.LYNX_EINVAL
+    assert lib.lynx_attn_anchor_decode(ctypes.byref(lay), 1, 32, 65, *args, None, None, 0,
+                                       None) == E.LYNX_EINVAL
+    assert lib.lynx_attn_anchor_decode(ctypes.byref(lay), 1, 32, 64, *args, None, None, 0,
+                                       None) == E.LYNX_EWORKSPACE
+    assert lib.lynx_attn_anchor_decode(ctypes.byref(lay), 1, 32, 64, *args, None, 16, 64,
+                                       None) == E.LYNX_EWORKSPACE
+    vargs = (16, 16, 16, 16, ctypes.byref(meta), 16)
+    assert lib.lynx_attn_verify(ctypes.byref(lay), 1, 32, 0, 64, *vargs, None, None, 16, 16,
+                                1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_attn_verify(ctypes.byref(lay), 1, 32, 65, 64, *vargs, None, None, 16, 16,
+                                1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_attn_verify(ctypes.byref(lay), 1, 32, 4, 64, *vargs, 16, None, 16, 16,
+                                1 << 20, None) == E.LYNX_EINVAL
+    # B == 0 is a valid empty call
+    assert lib.lynx_attn_anchor_decode(ctypes.byref(lay), 0, 32, 64, None, None, None, None,
+                                       ctypes.byref(meta), None, None, None, None, 0,
+                                       None) == E.LYNX_OK

@@ -1,0 +1,177 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.
+
+Codec and packed layouts must match bit for bit; attention outputs (BF16)
+must satisfy |gpu - ref| <= 2e-2 + 1e-2 |ref| elementwise against the fp64
+oracle.  Sizes span several 128-token groups and ragged tails; edge cases
+cover one-token and empty sequences, constant groups, signed zeros,
+denormals, G = 1..8 and k = 1..64.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_01831_amd import inputs, lynx
+from tests._util import assert_close
+from tests.gpu_cases import (bits, build_cache, gpu_anchor_decode, gpu_verify, note, random_bf16,
+                             random_kv)
+
+pytestmark = pytest.mark.gpu
+
+
+def assert_codec_equal(c):
+    for name in ("k_anc", "v_anc", "k_res", "v_res"):
+        got = getattr(c.pool, name).cpu().numpy()
+        assert np.array_equal(got, c.planes[name]), f"{name}: {np.count_nonzero(got != c.planes[name])} bytes differ"
+    m = c.pool.meta
+    for name in ("k_scale", "k_zero", "v_scale", "v_zero"):
+        got = getattr(m, name).cpu().numpy()
+        ref = getattr(c.meta, name)
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), f"{name} differs"
+
+
+# ------------------------------------------------------------------ codec --
+
+@pytest.mark.parametrize("T", [1, 15, 16, 17, 127, 128, 129, 300, 1000])
+@pytest.mark.parametrize("Hkv", [1, 4])
+def test_encode_bit_exact_contiguous(T, Hkv):
+    k, v = random_kv(T, Hkv, seed=T * 10 + Hkv)
+    c = build_cache([k], [v], Hkv, merge=False)
+    assert_codec_equal(c)
+
+
+def test_encode_bit_exact_paged_ragged():
+    lens = [37, 300, 129, 1, 16]
+    kv = [random_kv(T, 2, seed=100 + i) for i, T in enumerate(lens)]
+    c = build_cache([a for a, _ in kv], [b for _, b in kv], 2, bt=16, seed=5, merge=False,
+                    max_tokens=320)
+    assert_codec_equal(c)
+
+
+def test_encode_adversarial_groups():
+    """Constant groups, two-valued groups, +-0, denormals, huge values and exact
+    rounding ties decide the same codes on both sides."""
+    T, Hkv = 260, 2
+    g = torch.Generator().manual_seed(3)
+    x = torch.randn(T, Hkv, 128, generator=g)
+    x[:, 0, 0] = 3.25                                   # constant K column
+    x[:, 0, 1] = torch.where(torch.arange(T) % 3 == 0, -7.0, 9.0)
+    x[:, 0, 2] = -0.0
+    x[:, 0, 3] = torch.randn(T, generator=g) * 1e-39     # denormals
+    x[:, 1, 4] = torch.randn(T, generator=g) * 1e37      # huge
+    x[:, 1, 5] = torch.arange(T) % 256                   # integers: scale 1, ties
+    v = torch.randn(T, Hkv, 128, generator=g)
+    v[0] = 1.5                                           # constant V rows
+    v[1, :, :64] = -0.0
+    v[1, :, 64:] = 0.0
+    v[2, :, :4] = torch.tensor([0.0, 255.0, 126.5, 2.5]) # half-even ties
+    v[2, :, 4:] = 0.0
+    v[3] = torch.randn(Hkv, 128, generator=g) * 1e-38
+    c = build_cache([x.to(torch.bfloat16)], [v.to(torch.bfloat16)], Hkv, merge=False)
+    assert_codec_equal(c)
+
+
+@pytest.mark.parametrize("n", [1, 15, 16, 17, 4096, 4096 + 5, 1 << 20])
+def test_merge_bit_exact(n):
+    g = torch.Generator().manual_seed(n)
+    a = torch.randint(0, 256, (n,), generator=g, dtype=torch.uint8)
+    r = torch.randint(0, 256, (n,), generator=g, dtype=torch.uint8)
+    codes = torch.full((2 * n,), 0xA5, dtype=torch.uint8, device="cuda")
+    note(f"merge n={n}")
+    lynx.lynx_kv_merge(a.cuda(), r.cuda(), codes)
+    torch.cuda.synchronize()
+    assert np.array_equal(codes.cpu().numpy(), oracle.merge(a.numpy(), r.numpy()))
+
+
+def test_merge_of_encoded_planes():
+    k, v = random_kv(640, 4, seed=9)
+    c = build_cache([k], [v], 4)
+    assert np.array_equal(c.pool.k_codes.cpu().numpy(), oracle.merge(c.planes["k_anc"], c.planes["k_res"]))
+    assert np.array_equal(c.pool.v_codes.cpu().numpy(), oracle.merge(c.planes["v_anc"], c.planes["v_res"]))
+
+
+# -------------------------------------------------------------- attention --
+
+def oracle_decode(c, q, unit_mask=None):
+    return oracle.anchor_decode(c.OL, q.shape[1], np.array(c.lens), c.table.numpy(),
+                                c.planes["k_anc"], c.planes["v_anc"], c.meta, bits(q),
+                                unit_mask=unit_mask)
+
+
+def oracle_verify(c, q, k_new=None, v_new=None, unit_mask=None):
+    kc = oracle.merge(c.planes["k_anc"], c.planes["k_res"])
+    vc = oracle.merge(c.planes["v_anc"], c.planes["v_res"])
+    return oracle.verify(c.OL, q.shape[2], np.array(c.lens), c.table.numpy(), kc, vc, c.meta,
+                         bits(q), None if k_new is None else bits(k_new),
+                         None if v_new is None else bits(v_new), unit_mask=unit_mask)
+
+
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+@pytest.mark.parametrize("T", [1, 17, 300, 1500])
+def test_anchor_decode(G, T):
+    Hkv = 2
+    k, v = random_kv(T, Hkv, seed=G * 1000 + T)
+    c = build_cache([k], [v], Hkv, merge=False)
+    q = random_bf16((1, G * Hkv, 128), seed=T + G)
+    out, lse = gpu_anchor_decode(c, q)
+    ref, ref_lse = oracle_decode(c, q)
+    assert_close(out, ref, what=f"anchor decode G={G} T={T}")
+    np.testing.assert_allclose(lse, ref_lse, rtol=1e-4, atol=1e-4)
+
+
+def test_anchor_decode_paged_ragged_batch():
+    lens = [700, 33, 1, 1024, 129]
+    kv = [random_kv(T, 2, seed=200 + i) for i, T in enumerate(lens)]
+    c = build_cache([a for a, _ in kv], [b for _, b in kv], 2, bt=16, seed=7, merge=False)
+    q = random_bf16((len(lens), 8, 128), seed=77)
+    out, lse = gpu_anchor_decode(c, q)
+    ref, ref_lse = oracle_decode(c, q)
+    assert_close(out, ref, what="paged ragged decode")
+    np.testing.assert_allclose(lse, ref_lse, rtol=1e-4, atol=1e-4)
+
+
+def test_anchor_decode_empty_sequence():
+    lens = [0, 50]
+    kv = [random_kv(max(T, 1), 1, seed=300 + i) for i, T in enumerate(lens)]
+    ks = [kv[0][0][:0], kv[1][0]]
+    vs = [kv[0][1][:0], kv[1][1]]
+    c = build_cache(ks, vs, 1, merge=False)
+    q = random_bf16((2, 2, 128), seed=1)
+    out, lse = gpu_anchor_decode(c, q)
+    assert (out[0] == 0).all() and np.isneginf(lse[0]).all()
+    ref, _ = oracle_decode(c, q)
+    assert_close(out[1], ref[1], what="second sequence")
+
+
+@pytest.mark.parametrize("nq,tail", [(1, False), (1, True), (4, True), (8, True), (8, False), (64, True)])
+def test_verify(nq, tail):
+    Hkv, G = 2, 4
+    lens = [300, 129]
+    kv = [random_kv(T, Hkv, seed=400 + i + nq) for i, T in enumerate(lens)]
+    c = build_cache([a for a, _ in kv], [b for _, b in kv], Hkv)
+    q = random_bf16((2, nq, Hkv * G, 128), seed=nq)
+    kn = random_bf16((2, nq, Hkv, 128), seed=nq + 1) if tail else None
+    vn = random_bf16((2, nq, Hkv, 128), seed=nq + 2) if tail else None
+    out = gpu_verify(c, q, kn, vn)
+    ref, _ = oracle_verify(c, q, kn, vn)
+    assert_close(out, ref, what=f"verify k={nq} tail={tail}")
+
+
+def test_tiny_config_end_to_end():
+    """Tiny workload: 1 layer, 8 q / 4 kv heads, 4096 tokens, 4 K outlier
+    channels x10 per kv head; encode, merge, anchor decode, verify k = 1."""
+    w = inputs.WORKLOADS["tiny-gqa2-4k"]
+    k = inputs.kv(w, "k")
+    v = inputs.kv(w, "v")
+    c = build_cache([k], [v], w.Hkv)
+    assert_codec_equal(c)
+    assert np.array_equal(c.pool.k_codes.cpu().numpy(), oracle.merge(c.planes["k_anc"], c.planes["k_res"]))
+    q = inputs.queries(w)
+    out, lse = gpu_anchor_decode(c, q)
+    ref, ref_lse = oracle_decode(c, q)
+    assert_close(out, ref, what="tiny anchor decode")
+    qv = inputs.queries(w, nq=1).view(1, 1, w.Hq, 128)
+    outv = gpu_verify(c, qv)
+    refv, _ = oracle_verify(c, qv)
+    assert_close(outv, refv, what="tiny verify")
