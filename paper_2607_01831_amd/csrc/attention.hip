@@ -377,40 +377,96 @@ __global__ __launch_bounds__(kAttnThreads) void attn_split_kernel(AttnArgs a) {
     }
 }
 
-// One workgroup of 128 threads per (row, kv head, sequence): merge the
-// partials of all splits, normalise, round to BF16, write lse.
-__global__ __launch_bounds__(kHeadDim) void attn_combine_kernel(AttnArgs a, uint16_t *out,
-                                                                float *lse) {
+constexpr int kCombineThreads = 256;
+constexpr int kCombineLdsSplits = 4096;
+
+__device__ __forceinline__ float block_reduce(float v, bool is_max, float *red) {
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) {
+        const float o = __shfl_xor(v, s);
+        v = is_max ? fmaxf(v, o) : v + o;
+    }
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[w] = v;
+    __syncthreads();
+    v = red[0];
+#pragma unroll
+    for (int i = 1; i < kCombineThreads / 64; ++i) v = is_max ? fmaxf(v, red[i]) : v + red[i];
+    return v;
+}
+
+// One workgroup per (row, kv head, sequence): merge the partials of all
+// splits, normalise, round to BF16, write lse.  The splits are read in
+// parallel: 8 groups of 32 threads, each thread one float4 of dims.
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a, uint16_t *out,
+                                                                       float *lse) {
     const int gr = blockIdx.x;
     const int h = blockIdx.y;
     const int b = blockIdx.z;
-    const int d = threadIdx.x;
+    const int tid = threadIdx.x;
     const int Hkv = a.geo.Hkv;
-    const size_t base = (((size_t)b * Hkv + h) * a.rows_total + gr) * a.n_splits;
-    float M = -INFINITY;
+    const int n = a.n_splits;
+    const size_t base = (((size_t)b * Hkv + h) * a.rows_total + gr) * n;
+    __shared__ float s_w[kCombineLdsSplits];
+    __shared__ float s_red[kCombineThreads / 64];
+    __shared__ float4 s_acc[8][32];
+
+    float mloc = -INFINITY;
     bool nan = false;
-    for (int s = 0; s < a.n_splits; ++s) {
+    for (int s = tid; s < n; s += kCombineThreads) {
         const float2 ml = a.ws_ml[base + s];
         nan |= isnan(ml.y);
-        M = fmaxf(M, ml.x);
+        mloc = fmaxf(mloc, ml.x);
     }
-    float O = 0.0f, Lsum = 0.0f;
-    if (M != -INFINITY) {
-        for (int s = 0; s < a.n_splits; ++s) {
+    nan = __syncthreads_or(nan);
+    const float M = block_reduce(mloc, true, s_red);
+    float lloc = 0.0f;
+    for (int s = tid; s < n; s += kCombineThreads) {
+        const float2 ml = a.ws_ml[base + s];
+        const float wgt = (ml.x == -INFINITY || M == -INFINITY) ? 0.0f : exp2f(ml.x - M);
+        if (s < kCombineLdsSplits) s_w[s] = wgt;
+        lloc += ml.y * wgt;
+    }
+    const float L = block_reduce(lloc, false, s_red);  // also orders the s_w writes
+
+    const int d4 = tid & 31;
+    const int sg = tid >> 5;
+    const float4 *o4 = reinterpret_cast<const float4 *>(a.ws_o);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+    for (int s = sg; s < n; s += 8) {
+        float wgt;
+        if (s < kCombineLdsSplits) {
+            wgt = s_w[s];
+        } else {
             const float2 ml = a.ws_ml[base + s];
-            if (ml.x == -INFINITY) continue;
-            const float f = exp2f(ml.x - M);
-            O += a.ws_o[(base + s) * kHeadDim + d] * f;
-            Lsum += ml.y * f;
+            wgt = (ml.x == -INFINITY || M == -INFINITY) ? 0.0f : exp2f(ml.x - M);
+        }
+        const float4 v = o4[(base + s) * (kHeadDim / 4) + d4];
+        if (wgt != 0.0f) {
+            acc.x += v.x * wgt;
+            acc.y += v.y * wgt;
+            acc.z += v.z * wgt;
+            acc.w += v.w * wgt;
         }
     }
-    float res = Lsum > 0.0f ? O / Lsum : 0.0f;
-    if (nan) res = NAN;
-    const int i = gr / a.G;
-    const int g = gr % a.G;
-    const size_t row = ((size_t)b * a.nq + i) * a.Hq + (size_t)h * a.G + g;
-    out[row * kHeadDim + d] = f32_to_bf16_rne(res);
-    if (lse && d == 0) lse[row] = nan ? NAN : (Lsum > 0.0f ? (M + log2f(Lsum)) * kLn2 : -INFINITY);
+    s_acc[sg][d4] = acc;
+    __syncthreads();
+    if (tid < kHeadDim) {
+        const int d = tid;
+        float O = 0.0f;
+#pragma unroll
+        for (int g8 = 0; g8 < 8; ++g8) O += reinterpret_cast<const float *>(&s_acc[g8][d >> 2])[d & 3];
+        float res = L > 0.0f ? O / L : 0.0f;
+        if (nan) res = NAN;
+        const int i = gr / a.G;
+        const int g = gr % a.G;
+        const size_t row = ((size_t)b * a.nq + i) * a.Hq + (size_t)h * a.G + g;
+        out[row * kHeadDim + d] = f32_to_bf16_rne(res);
+        if (lse && d == 0)
+            lse[row] = nan ? NAN : (L > 0.0f ? (M + log2f(L)) * kLn2 : -INFINITY);
+    }
 }
 
 template <KvMode MODE>
@@ -434,7 +490,15 @@ AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_le
     p.rows_chunk = 1;
     while (p.rows_chunk < 8 && p.rows_chunk < p.rows_total) p.rows_chunk *= 2;
     p.n_chunks = (p.rows_total + p.rows_chunk - 1) / p.rows_chunk;
+    // Context tokens per split: 512, doubled (up to 1024) while the launch
+    // still has >= 1024 workgroups, so long contexts write fewer partials.
     p.split_tokens = kWaves * kKGroup;
+    const int max_split = (nq == 1 && G > 8) ? 512 : 1024;  // decode with 16-head chunks: 4 groups
+    while (p.split_tokens < max_split) {
+        const long long next = ((long long)max_seq_len + 2 * p.split_tokens - 1) / (2 * p.split_tokens);
+        if (next * g.Hkv * B < 1024) break;
+        p.split_tokens *= 2;
+    }
     // at least one split, so that empty sequences still get (zero) outputs
     p.n_ctx_splits = max_seq_len > 0 ? (max_seq_len + p.split_tokens - 1) / p.split_tokens : 1;
     p.n_splits = p.n_ctx_splits + (tail ? 1 : 0);
@@ -472,13 +536,43 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
     a.v_new = v_new;
     a.ws_o = reinterpret_cast<float *>(workspace);
     a.ws_ml = reinterpret_cast<float2 *>(reinterpret_cast<char *>(workspace) + plan.o_bytes);
-    dim3 grid(plan.n_splits, g.Hkv * plan.n_chunks, B);
-    hipError_t e = mode == KvMode::kAnchor
-                       ? launch_split<KvMode::kAnchor>(plan.rows_chunk, grid, a, stream)
-                       : launch_split<KvMode::kCodes>(plan.rows_chunk, grid, a, stream);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_combine_kernel, dim3(plan.rows_total, g.Hkv, B), dim3(kHeadDim), 0,
-                       stream, a, out, lse);
+    if (mode == KvMode::kAnchor && nq == 1 && k_new == nullptr) {
+        // matrix-core decode over the anchor nibbles
+        DecodeArgs d;
+        d.geo = g;
+        d.B = B;
+        d.Hq = Hq;
+        d.G = a.G;
+        d.max_seq_len = max_seq_len;
+        d.n_splits = plan.n_ctx_splits;
+        d.groups_per_split = plan.split_tokens / kKGroup;
+        d.chunk_heads = a.G < 16 ? a.G : 16;
+        d.bt_shift = -1;
+        for (int sh = 0; sh < 31; ++sh)
+            if ((1 << sh) == g.bt) d.bt_shift = sh;
+        d.meta_vec4 = (g.max_tokens % 4 == 0) ? 1 : 0;
+        d.seq_lens = seq_lens;
+        d.block_table = block_table;
+        d.k_anc = k_plane;
+        d.v_anc = v_plane;
+        d.meta = meta;
+        d.q = q;
+        d.ws_o = a.ws_o;
+        d.ws_ml = a.ws_ml;
+        d.rows_total = plan.rows_total;
+        d.ws_splits = plan.n_splits;
+        const int chunks = (a.G + d.chunk_heads - 1) / d.chunk_heads;
+        hipError_t e = launch_anchor_decode_mfma(d, chunks, stream);
+        if (e != hipSuccess) return e;
+    } else {
+        dim3 grid(plan.n_splits, g.Hkv * plan.n_chunks, B);
+        hipError_t e = mode == KvMode::kAnchor
+                           ? launch_split<KvMode::kAnchor>(plan.rows_chunk, grid, a, stream)
+                           : launch_split<KvMode::kCodes>(plan.rows_chunk, grid, a, stream);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(attn_combine_kernel, dim3(plan.rows_total, g.Hkv, B), dim3(kCombineThreads),
+                       0, stream, a, out, lse);
     return hipGetLastError();
 }
 

@@ -49,6 +49,26 @@ struct AttnPlan {
     size_t ml_bytes;  // workspace bytes for the partial (max, sum) pairs
 };
 
+// Arguments of the matrix-core anchor decode kernel (anchor_decode.hip).
+struct DecodeArgs {
+    Geometry geo;
+    int B, Hq, G, max_seq_len;
+    int n_splits, groups_per_split, chunk_heads;
+    int bt_shift;   // log2(block_tokens) when it is a power of two, else -1
+    int meta_vec4;  // max_tokens % 4 == 0: V metadata loads may be 16 bytes
+    const int32_t *seq_lens;
+    const int32_t *block_table;
+    const uint8_t *k_anc;
+    const uint8_t *v_anc;
+    MetaPtrs meta;
+    const uint16_t *q;
+    float *ws_o;    // split partials, same layout as the attention workspace
+    float2 *ws_ml;
+    int rows_total, ws_splits;
+};
+
+hipError_t launch_anchor_decode_mfma(const DecodeArgs &args, int chunks, hipStream_t stream);
+
 AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_len, bool tail);
 
 hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan, int B, int Hq,

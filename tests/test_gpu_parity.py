@@ -175,3 +175,23 @@ def test_tiny_config_end_to_end():
     outv = gpu_verify(c, qv)
     refv, _ = oracle_verify(c, qv)
     assert_close(outv, refv, what="tiny verify")
+
+
+@pytest.mark.parametrize("boost", [30.0, 400.0])
+def test_anchor_decode_dominant_late_token(boost):
+    """A late token whose score dwarfs every earlier one: exercises the
+    kernel's fallback that rescales when the first tile's maximum is far too
+    small a reference (boost 400 overflows it, boost 30 does not)."""
+    T, Hkv, G = 3000, 2, 4
+    g = torch.Generator().manual_seed(int(boost))
+    q = torch.randn(1, G * Hkv, 128, generator=g)
+    k = torch.randn(T, Hkv, 128, generator=g)
+    v = torch.randn(T, Hkv, 128, generator=g)
+    for h in range(Hkv):
+        k[2500, h] = boost * q[0, h * G] / q[0, h * G].norm()
+    c = build_cache([k.to(torch.bfloat16)], [v.to(torch.bfloat16)], Hkv, merge=False)
+    qb = q.to(torch.bfloat16)
+    out, lse = gpu_anchor_decode(c, qb)
+    ref, ref_lse = oracle_decode(c, qb)
+    assert_close(out, ref, what=f"dominant token x{boost}")
+    np.testing.assert_allclose(lse, ref_lse, rtol=1e-4, atol=1e-3)
