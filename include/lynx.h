@@ -129,6 +129,8 @@ int lynx_kv_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes,
  * its split-context partial results, for `num_queries` query tokens per
  * sequence (1 for anchor decode, k for verify) and sequences of at most
  * max_seq_len tokens.  Returns 0 on invalid arguments.
+ * Calls that share a workspace must not run concurrently; its contents need
+ * no initialisation.
  */
 size_t lynx_attn_workspace_bytes(const lynx_layout *L, int32_t B, int32_t Hq,
                                  int32_t num_queries, int32_t max_seq_len);

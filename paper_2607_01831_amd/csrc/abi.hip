@@ -119,7 +119,7 @@ size_t lynx_attn_workspace_bytes(const lynx_layout *L, int32_t B, int32_t Hq,
         return 0;
     // sized for the larger plan, the one with a draft-tail split
     const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, num_queries, max_seq_len, true);
-    return p.o_bytes + p.ml_bytes;
+    return p.workspace_bytes();
 }
 
 int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t max_seq_len,
@@ -135,8 +135,7 @@ int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t
     if (B == 0) return LYNX_OK;
     if (lse && !aligned16(lse)) return LYNX_EINVAL;
     const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, 1, max_seq_len, false);
-    if (p.o_bytes + p.ml_bytes > 0 &&
-        (!workspace || !aligned16(workspace) || workspace_bytes < p.o_bytes + p.ml_bytes))
+    if (!workspace || !aligned16(workspace) || workspace_bytes < p.workspace_bytes())
         return LYNX_EWORKSPACE;
     hipError_t e = lynx::launch_attention(
         lynx::KvMode::kAnchor, g, p, B, Hq, 1, max_seq_len, seq_lens, block_table, k_anc, v_anc,
@@ -161,8 +160,7 @@ int lynx_attn_verify(const lynx_layout *L, int32_t B, int32_t Hq, int32_t k,
     if (B == 0) return LYNX_OK;
     const bool tail = k_new != nullptr;
     const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, k, max_seq_len, tail);
-    if (p.o_bytes + p.ml_bytes > 0 &&
-        (!workspace || !aligned16(workspace) || workspace_bytes < p.o_bytes + p.ml_bytes))
+    if (!workspace || !aligned16(workspace) || workspace_bytes < p.workspace_bytes())
         return LYNX_EWORKSPACE;
     hipError_t e = lynx::launch_attention(
         lynx::KvMode::kCodes, g, p, B, Hq, k, max_seq_len, seq_lens, block_table, k_codes, v_codes,

@@ -170,7 +170,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     const int col = lane & 15;  // MFMA column / 16-lane row index
     const int kg = lane >> 4;   // MFMA row group
     const int heads = min(a.chunk_heads, a.G - chunk * a.chunk_heads);
-    const int T = min(a.seq_lens[b], a.max_seq_len);
+    const int T = max(0, min(a.seq_lens[b], a.max_seq_len));
     const int g0 = split * NG;
     // groups of this split that hold tokens (uniform across the workgroup)
     const int n_groups = max(0, min(NG, (T - g0 * kKGroup + kKGroup - 1) / kKGroup));
@@ -180,19 +180,22 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     // zero piece feeds the columns past the chunk's heads.
     constexpr int kBPieces = NG * 8 * 4 * GP;
     __shared__ u32x4_t s_b[kBPieces + 1];
-    __shared__ float s_bias[NG][GP];
+    __shared__ float s_bias[kWaves][NG][GP];  // per-wavefront partial biases
     __shared__ __attribute__((aligned(16))) float s_vs[NG * kKGroup];
     __shared__ __attribute__((aligned(16))) float s_vz[NG * kKGroup];
     __shared__ __attribute__((aligned(16))) uint8_t s_v[kWaves][kTile * kNibbleRow];
-    __shared__ float s_o[kWaves][GP][kHeadDim];
+    __shared__ __attribute__((aligned(16))) float s_o[kWaves][GP][kHeadDim];
     __shared__ float s_m[kWaves][GP], s_l[kWaves][GP], s_ob[kWaves][GP];
 
-    bool bad = false;
-    const int32_t *bt_row = a.block_table + (size_t)b * a.geo.max_blocks;
     const size_t vmeta = ((size_t)b * Hkv + h) * a.geo.max_tokens;
     const size_t kmeta = ((size_t)b * Hkv + h) * a.geo.n_groups * kHeadDim;
-    const u32x4_t c128 = {0x43004300u, 0x43004300u, 0x43004300u, 0x43004300u};
+    const size_t q_row0 = (size_t)b * a.Hq + (size_t)h * a.G + (size_t)chunk * a.chunk_heads;
     const float kscore = kLog2e * rsqrtf((float)kHeadDim);
+
+  if (n_groups > 0) {
+    bool bad = false;
+    const int32_t *bt_row = a.block_table + (size_t)b * a.geo.max_blocks;
+    const u32x4_t c128 = {0x43004300u, 0x43004300u, 0x43004300u, 0x43004300u};
 
     // block of a contiguous cache (LAYOUT 0)
     const size_t blk0_rows =
@@ -211,6 +214,54 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         }
         return ((size_t)blk * Hkv + h) * a.geo.bt + (size_t)(t - bi * a.geo.bt);
     };
+
+    // ---- prologue loads, all issued before the first tile loads so that the
+    // waits for them leave the tiles in flight ----
+    // V metadata of the split's tokens (zero past the context)
+    constexpr int kVmPer = NG * kKGroup / kThreads;
+    float vs_r[kVmPer], vz_r[kVmPer];
+#pragma unroll
+    for (int k = 0; k < kVmPer; ++k) {
+        const int t = g0 * kKGroup + tid + k * kThreads;
+        const size_t ti = vmeta + (size_t)min(t, max(T - 1, 0));
+        vs_r[k] = a.meta.v_scale[ti];
+        vz_r[k] = a.meta.v_zero[ti];
+        if (t >= T) vs_r[k] = vz_r[k] = 0.0f;
+    }
+    // K scales and query pieces of the fold: piece (gl, kk, dg, hh) covers
+    // dims 32 dg + 8 kk .. + 7 of head hh and group gl.  Indices are clamped
+    // into range; pieces past the heads or groups are zeroed below.
+    constexpr int kFoldPieces = NG * 4 * 4 * GP;
+    constexpr int kFoldPer = kFoldPieces / kThreads;
+    static_assert(kFoldPieces % kThreads == 0, "fold pieces must tile the workgroup");
+    float4 fs0[kFoldPer], fs1[kFoldPer];
+    uint4 fq[kFoldPer];
+#pragma unroll
+    for (int k = 0; k < kFoldPer; ++k) {
+        const int pidx = tid + k * kThreads;
+        const int hh = min(pidx % GP, heads - 1);
+        const int dg = (pidx / GP) % 4;
+        const int kk = (pidx / (4 * GP)) % 4;
+        const int gl = min(pidx / (16 * GP), n_groups - 1);
+        const int d0 = 32 * dg + 8 * kk;
+        const float *sp = a.meta.k_scale + kmeta + (size_t)(g0 + gl) * kHeadDim + d0;
+        fs0[k] = *reinterpret_cast<const float4 *>(sp);
+        fs1[k] = *reinterpret_cast<const float4 *>(sp + 4);
+        fq[k] = *reinterpret_cast<const uint4 *>(a.q + (q_row0 + hh) * kHeadDim + d0);
+    }
+    // bias operands: query of head col, K scale/zero of group col, dims 32 w + 8 kg ..
+    uint4 bqw;
+    float4 bs0, bs1, bz0, bz1;
+    {
+        const int hc = min(col, heads - 1);
+        const int gc = min(col, n_groups - 1);
+        bqw = *reinterpret_cast<const uint4 *>(a.q + (q_row0 + hc) * kHeadDim + 32 * w + 8 * kg);
+        const size_t mo = kmeta + (size_t)(g0 + gc) * kHeadDim + 32 * w + 8 * kg;
+        bs0 = *reinterpret_cast<const float4 *>(a.meta.k_scale + mo);
+        bs1 = *reinterpret_cast<const float4 *>(a.meta.k_scale + mo + 4);
+        bz0 = *reinterpret_cast<const float4 *>(a.meta.k_zero + mo);
+        bz1 = *reinterpret_cast<const float4 *>(a.meta.k_zero + mo + 4);
+    }
 
     // ---- this wavefront's tiles: groups w, w+4, ..; 4 tiles of 32 tokens each ----
     constexpr int kTilesPerWave = NG;  // (NG / 4) groups x 4 tiles
@@ -253,54 +304,39 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     };
 
     // Put the first tiles in flight before the fold below.
+    // Loads of tiles past the context read clamped rows and are never used;
+    // issuing them unconditionally keeps the wait counts exact.
     Tile tiles[kPrefetch + 1];
 #pragma unroll
     for (int j = 0; j < kPrefetch; ++j)
-        if (j < kTilesPerWave && tile_valid(j)) load_tile(j, tiles[j]);
+        if (j < kTilesPerWave) load_tile(j, tiles[j]);
 
-    // ---- prologue (whole workgroup): fold every group's K scale/zero into
-    // the query, stage the split's V metadata in LDS ----
-    {
-        const u32x4_t z = {0u, 0u, 0u, 0u};
-        for (int i = tid; i < kBPieces + 1; i += kThreads) s_b[i] = z;
-        for (int i = tid; i < NG * GP; i += kThreads) (&s_bias[0][0])[i] = 0.0f;
-    }
-    {
-        // V metadata of the split's tokens; zero past the context
-        for (int i = tid; i < NG * kKGroup; i += kThreads) {
-            const int t = g0 * kKGroup + i;
-            s_vs[i] = t < T ? a.meta.v_scale[vmeta + t] : 0.0f;
-            s_vz[i] = t < T ? a.meta.v_zero[vmeta + t] : 0.0f;
-        }
-    }
-    __syncthreads();  // zeroed operands and biases are in place
+    // ---- prologue (whole workgroup): fold every group's K scale into the
+    // query, per-wavefront bias partials, V metadata into LDS ----
     // (a) Folded operands, one 16-byte piece (8 dims) at a time: piece
     // (gl, kk, dg, hh) holds q'_d = 16 q_d s_d of dims 32 dg + 8 kk + pi(e),
     // as bf16 hi in s_b and bf16 lo 4 GP pieces further.
-    constexpr int kFoldPieces = NG * 4 * 4 * GP;
-    for (int pidx = tid; pidx < kFoldPieces; pidx += kThreads) {
+#pragma unroll
+    for (int k = 0; k < kFoldPer; ++k) {
+        const int pidx = tid + k * kThreads;
         const int hh = pidx % GP;
         const int dg = (pidx / GP) % 4;
         const int kk = (pidx / (4 * GP)) % 4;
         const int gl = pidx / (16 * GP);
-        if (hh >= heads || gl >= n_groups) continue;
-        const int d0 = 32 * dg + 8 * kk;
-        const float *sp = a.meta.k_scale + kmeta + (size_t)(g0 + gl) * kHeadDim + d0;
-        const float4 s0 = *reinterpret_cast<const float4 *>(sp);
-        const float4 s1 = *reinterpret_cast<const float4 *>(sp + 4);
-        const uint4 qw = *reinterpret_cast<const uint4 *>(
-            a.q + ((size_t)b * a.Hq + (size_t)h * a.G + chunk * a.chunk_heads + hh) * kHeadDim + d0);
+        const bool live = hh < heads && gl < n_groups;
+        const uint4 qw = fq[k];
         // dims d0 + (0, 2, 4, 6, 1, 3, 5, 7)
         const float qv[8] = {bf16_val(qw.x & 0xffffu), bf16_val(qw.y & 0xffffu),
                              bf16_val(qw.z & 0xffffu), bf16_val(qw.w & 0xffffu),
                              __uint_as_float(qw.x & 0xffff0000u), __uint_as_float(qw.y & 0xffff0000u),
                              __uint_as_float(qw.z & 0xffff0000u), __uint_as_float(qw.w & 0xffff0000u)};
+        const float4 s0 = fs0[k], s1 = fs1[k];
         const float sv[8] = {s0.x, s0.z, s1.x, s1.z, s0.y, s0.w, s1.y, s1.w};
         u32x4_t hi, lo;
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
-            const float q0 = 16.0f * qv[e] * sv[e];
-            const float q1 = 16.0f * qv[e + 1] * sv[e + 1];
+            const float q0 = live ? 16.0f * qv[e] * sv[e] : 0.0f;
+            const float q1 = live ? 16.0f * qv[e + 1] * sv[e + 1] : 0.0f;
             const uint32_t hp = pack2(q0, q1);
             hi[e / 2] = hp;
             lo[e / 2] = pack2(q0 - bf16_val(hp & 0xffffu), q1 - __uint_as_float(hp & 0xffff0000u));
@@ -309,28 +345,20 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         s_b[piece] = hi;
         s_b[piece + 4 * GP] = lo;
     }
+    if (tid == 0) s_b[kBPieces] = u32x4_t{0u, 0u, 0u, 0u};
     // (b) Biases bias[gl][hh] = sum_d q_d (z_d - 2040.5 s_d) as a small matrix
     // product on the matrix cores: rows = heads, columns = groups, wavefront w
-    // contracting dims 32 w..32 w+31 (zc carried as bf16 hi + lo).
+    // contracting dims 32 w..32 w+31 (zc carried as bf16 hi + lo); the four
+    // wavefront partials are summed when a group's operands are loaded.
     {
         u32x4_t qa = {0u, 0u, 0u, 0u};
-        if (col < heads) {
-            const uint4 qw = *reinterpret_cast<const uint4 *>(
-                a.q + ((size_t)b * a.Hq + (size_t)h * a.G + chunk * a.chunk_heads + col) * kHeadDim +
-                32 * w + 8 * kg);
-            qa = u32x4_t{qw.x, qw.y, qw.z, qw.w};
-        }
+        if (col < heads) qa = u32x4_t{bqw.x, bqw.y, bqw.z, bqw.w};
         u32x4_t zh = {0u, 0u, 0u, 0u}, zl = {0u, 0u, 0u, 0u};
         if (col < n_groups) {
-            const size_t mo = kmeta + (size_t)(g0 + col) * kHeadDim + 32 * w + 8 * kg;
-            const float4 s0 = *reinterpret_cast<const float4 *>(a.meta.k_scale + mo);
-            const float4 s1 = *reinterpret_cast<const float4 *>(a.meta.k_scale + mo + 4);
-            const float4 z0 = *reinterpret_cast<const float4 *>(a.meta.k_zero + mo);
-            const float4 z1 = *reinterpret_cast<const float4 *>(a.meta.k_zero + mo + 4);
-            const float zc[8] = {z0.x - 2040.5f * s0.x, z0.y - 2040.5f * s0.y,
-                                 z0.z - 2040.5f * s0.z, z0.w - 2040.5f * s0.w,
-                                 z1.x - 2040.5f * s1.x, z1.y - 2040.5f * s1.y,
-                                 z1.z - 2040.5f * s1.z, z1.w - 2040.5f * s1.w};
+            const float zc[8] = {bz0.x - 2040.5f * bs0.x, bz0.y - 2040.5f * bs0.y,
+                                 bz0.z - 2040.5f * bs0.z, bz0.w - 2040.5f * bs0.w,
+                                 bz1.x - 2040.5f * bs1.x, bz1.y - 2040.5f * bs1.y,
+                                 bz1.z - 2040.5f * bs1.z, bz1.w - 2040.5f * bs1.w};
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
                 const uint32_t hp = pack2(zc[e], zc[e + 1]);
@@ -342,10 +370,17 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         cb = mfma(qa, zh, cb);
         cb = mfma(qa, zl, cb);
         // lane (group col, row group kg) holds heads 4 kg + i
+        if (col < NG) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (4 * kg + i < heads && col < n_groups && 4 * kg + i < GP)
-                atomicAdd(&s_bias[col][4 * kg + i], cb[i] * kscore);
+            for (int i = 0; i < 4; ++i)
+                if (4 * kg + i < GP) s_bias[w][col][4 * kg + i] = cb[i] * kscore;
+        }
+    }
+    // (c) V metadata
+#pragma unroll
+    for (int k = 0; k < kVmPer; ++k) {
+        s_vs[tid + k * kThreads] = vs_r[k];
+        s_vz[tid + k * kThreads] = vz_r[k];
     }
     __syncthreads();  // folded operands, biases and V metadata are ready
 
@@ -376,7 +411,9 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
 #pragma unroll
         for (int i = 0; i < 8; ++i)
             bq[i] = b_piece >= 0 ? s_b[(gl * 8 + i) * 4 * GP + b_piece] : s_b[kBPieces];
-        bk = col < heads ? s_bias[gl][col] : 0.0f;
+        bk = col < heads ? (s_bias[0][gl][col] + s_bias[1][gl][col]) +
+                               (s_bias[2][gl][col] + s_bias[3][gl][col])
+                         : 0.0f;
     };
     // Scores of tile j (log2 units): lane (col, kg) gets token
     // t0 + 16 r + 4 kg + i in x[4 r + i]; tokens past the context get -inf.
@@ -455,7 +492,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
 #pragma unroll
     for (int j = 0; j < kTilesPerWave; ++j) {
         if (!tile_valid(j)) break;  // wavefront-uniform; later tiles are past the context too
-        if (j + kPrefetch < kTilesPerWave && tile_valid(j + kPrefetch))
+        if (j + kPrefetch < kTilesPerWave)
             load_tile(j + kPrefetch, tiles[(j + kPrefetch) % (kPrefetch + 1)]);
         if ((j & 3) == 0) load_group_operands(j);
         float x[8];
@@ -550,6 +587,14 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         a.ws_o[pi * kHeadDim + dd] = O;
         if (dd == 0) a.ws_ml[pi] = make_float2(M, L);
     }
+  } else {
+    // a split past the context: (max, sum) = (-inf, 0), no output
+    for (int hh = tid; hh < heads; hh += kThreads) {
+        const size_t pi =
+            (((size_t)b * Hkv + h) * a.rows_total + chunk * a.chunk_heads + hh) * a.ws_splits + split;
+        a.ws_ml[pi] = make_float2(-INFINITY, 0.0f);
+    }
+  }
 }
 
 template <int LAYOUT, int NG>

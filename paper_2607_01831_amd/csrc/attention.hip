@@ -378,27 +378,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_split_kernel(AttnArgs a) {
 }
 
 constexpr int kCombineThreads = 256;
-constexpr int kCombineLdsSplits = 4096;
-
-__device__ __forceinline__ float block_reduce(float v, bool is_max, float *red) {
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-        const float o = __shfl_xor(v, s);
-        v = is_max ? fmaxf(v, o) : v + o;
-    }
-    const int w = threadIdx.x >> 6;
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) red[w] = v;
-    __syncthreads();
-    v = red[0];
-#pragma unroll
-    for (int i = 1; i < kCombineThreads / 64; ++i) v = is_max ? fmaxf(v, red[i]) : v + red[i];
-    return v;
-}
 
 // One workgroup per (row, kv head, sequence): merge the partials of all
-// splits, normalise, round to BF16, write lse.  The splits are read in
-// parallel: 8 groups of 32 threads, each thread one float4 of dims.
+// splits, normalise, round to BF16, write lse.  Thread (split group sg,
+// float4 column d4) folds every 8th split into a running (max, sum, output),
+// loading 16 splits' partial outputs and (max, sum) pairs together so that
+// each step costs one round trip to memory; the 8 running triples meet in
+// LDS.
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a, uint16_t *out,
                                                                        float *lse) {
     const int gr = blockIdx.x;
@@ -408,64 +394,85 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     const int Hkv = a.geo.Hkv;
     const int n = a.n_splits;
     const size_t base = (((size_t)b * Hkv + h) * a.rows_total + gr) * n;
-    __shared__ float s_w[kCombineLdsSplits];
-    __shared__ float s_red[kCombineThreads / 64];
-    __shared__ float4 s_acc[8][32];
+    constexpr int kGroups = kCombineThreads / (kHeadDim / 4);  // 8 split groups
+    constexpr int kBatch = 16;
+    __shared__ float4 s_acc[kGroups][kHeadDim / 4];
+    __shared__ float s_m[kGroups][kHeadDim / 4], s_l[kGroups][kHeadDim / 4];
 
-    float mloc = -INFINITY;
-    bool nan = false;
-    for (int s = tid; s < n; s += kCombineThreads) {
-        const float2 ml = a.ws_ml[base + s];
-        nan |= isnan(ml.y);
-        mloc = fmaxf(mloc, ml.x);
-    }
-    nan = __syncthreads_or(nan);
-    const float M = block_reduce(mloc, true, s_red);
-    float lloc = 0.0f;
-    for (int s = tid; s < n; s += kCombineThreads) {
-        const float2 ml = a.ws_ml[base + s];
-        const float wgt = (ml.x == -INFINITY || M == -INFINITY) ? 0.0f : exp2f(ml.x - M);
-        if (s < kCombineLdsSplits) s_w[s] = wgt;
-        lloc += ml.y * wgt;
-    }
-    const float L = block_reduce(lloc, false, s_red);  // also orders the s_w writes
-
-    const int d4 = tid & 31;
-    const int sg = tid >> 5;
-    const float4 *o4 = reinterpret_cast<const float4 *>(a.ws_o);
+    const int d4 = tid % (kHeadDim / 4);
+    const int sg = tid / (kHeadDim / 4);
+    const float4 *o4 = reinterpret_cast<const float4 *>(a.ws_o) + base * (kHeadDim / 4) + d4;
+    float m_t = -INFINITY, l_t = 0.0f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 4
-    for (int s = sg; s < n; s += 8) {
-        float wgt;
-        if (s < kCombineLdsSplits) {
-            wgt = s_w[s];
-        } else {
-            const float2 ml = a.ws_ml[base + s];
-            wgt = (ml.x == -INFINITY || M == -INFINITY) ? 0.0f : exp2f(ml.x - M);
+    bool nan = false;
+    for (int s0 = sg; s0 < n; s0 += kGroups * kBatch) {
+        float4 v[kBatch];
+        float2 ml[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int s = min(s0 + kGroups * u, n - 1);
+            v[u] = o4[(size_t)s * (kHeadDim / 4)];
+            ml[u] = a.ws_ml[base + s];
         }
-        const float4 v = o4[(base + s) * (kHeadDim / 4) + d4];
-        if (wgt != 0.0f) {
-            acc.x += v.x * wgt;
-            acc.y += v.y * wgt;
-            acc.z += v.z * wgt;
-            acc.w += v.w * wgt;
+        float mb = m_t;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (s0 + kGroups * u >= n) ml[u] = make_float2(-INFINITY, 0.0f);
+            mb = fmaxf(mb, ml[u].x);
         }
+        const float sc = m_t == -INFINITY ? 0.0f : exp2f(m_t - mb);
+        acc.x *= sc;
+        acc.y *= sc;
+        acc.z *= sc;
+        acc.w *= sc;
+        l_t *= sc;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const float e = ml[u].x == -INFINITY ? 0.0f : exp2f(ml[u].x - mb);
+            nan |= isnan(ml[u].y);
+            l_t = fmaf(ml[u].y, e, l_t);
+            // a split with weight 0 may hold no partial output at all
+            const float4 x = e != 0.0f ? v[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+            acc.x = fmaf(x.x, e, acc.x);
+            acc.y = fmaf(x.y, e, acc.y);
+            acc.z = fmaf(x.z, e, acc.z);
+            acc.w = fmaf(x.w, e, acc.w);
+        }
+        m_t = mb;
     }
     s_acc[sg][d4] = acc;
+    s_m[sg][d4] = m_t;
+    s_l[sg][d4] = nan ? NAN : l_t;
     __syncthreads();
-    if (tid < kHeadDim) {
-        const int d = tid;
-        float O = 0.0f;
+    if (sg == 0) {
+        float M = -INFINITY;
 #pragma unroll
-        for (int g8 = 0; g8 < 8; ++g8) O += reinterpret_cast<const float *>(&s_acc[g8][d >> 2])[d & 3];
-        float res = L > 0.0f ? O / L : 0.0f;
-        if (nan) res = NAN;
+        for (int g = 0; g < kGroups; ++g) M = fmaxf(M, s_m[g][d4]);
+        float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+        float L = 0.0f;
+        bool any_nan = false;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const float f = s_m[g][d4] == -INFINITY ? 0.0f : exp2f(s_m[g][d4] - M);
+            const float4 o = s_acc[g][d4];
+            O.x = fmaf(o.x, f, O.x);
+            O.y = fmaf(o.y, f, O.y);
+            O.z = fmaf(o.z, f, O.z);
+            O.w = fmaf(o.w, f, O.w);
+            any_nan |= isnan(s_l[g][d4]);
+            L = fmaf(s_l[g][d4], f, L);
+        }
+        float r[4] = {O.x, O.y, O.z, O.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) r[i] = any_nan ? NAN : (L > 0.0f ? r[i] / L : 0.0f);
         const int i = gr / a.G;
         const int g = gr % a.G;
         const size_t row = ((size_t)b * a.nq + i) * a.Hq + (size_t)h * a.G + g;
-        out[row * kHeadDim + d] = f32_to_bf16_rne(res);
-        if (lse && d == 0)
-            lse[row] = nan ? NAN : (L > 0.0f ? (M + log2f(L)) * kLn2 : -INFINITY);
+        const uint32_t lo = f32_to_bf16_rne(r[0]) | ((uint32_t)f32_to_bf16_rne(r[1]) << 16);
+        const uint32_t hi = f32_to_bf16_rne(r[2]) | ((uint32_t)f32_to_bf16_rne(r[3]) << 16);
+        *reinterpret_cast<uint2 *>(out + row * kHeadDim + 4 * d4) = make_uint2(lo, hi);
+        if (lse && d4 == 0)
+            lse[row] = any_nan ? NAN : (L > 0.0f ? (M + log2f(L)) * kLn2 : -INFINITY);
     }
 }
 

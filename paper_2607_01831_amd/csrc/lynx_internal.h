@@ -47,6 +47,7 @@ struct AttnPlan {
     int n_splits;     // n_ctx_splits (+1 when a BF16 draft tail is attended)
     size_t o_bytes;   // workspace bytes for the partial outputs
     size_t ml_bytes;  // workspace bytes for the partial (max, sum) pairs
+    size_t workspace_bytes() const { return o_bytes + ml_bytes; }  // [outputs][(max, sum)]
 };
 
 // Arguments of the matrix-core anchor decode kernel (anchor_decode.hip).
