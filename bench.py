@@ -18,10 +18,19 @@ One step = the whole hot path over all 32 layers:
 Printed: one JSON line.  `value` is the anchor-decode attention throughput in
 GB/s of algorithmic KV bytes (144 bytes per token per kv head) over the timed
 steps, from HIP events on the stream the kernels run on.
+
+Offline helpers (no GPU) turn rocprofv3 output of this script into the text
+summaries kept under profiles/:
+  --summarize-trace DIR          kernel-trace CSVs -> per-kernel durations
+  --summarize-pmc FETCH WRITE    FETCH_SIZE / WRITE_SIZE CSVs of a run with
+                                 --copy-calibration -> HBM bytes per call
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -34,6 +43,10 @@ sys.path.insert(0, str(ROOT))
 HBM_PEAK_GBPS = 8000.0
 METRIC = "anchor decode-attn KV GB/s (% HBM peak); encode/merge GB/s; verify µs @128k"
 WORKLOAD = "llama3-8b-32k"
+COPY_CALIBRATION_BYTES = 512 << 20
+TRAFFIC_SUMMARY = ROOT / "profiles" / "anchor_decode_llama3-8b-32k_traffic.md"
+# sources whose kernels make up one anchor-decode call
+DECODE_SOURCES = ["anchor_decode.hip", "attention.hip", "lynx_internal.h"]
 
 # algorithmic bytes per unit
 ENC_BYTES_PER_ELEM = 2.0 + 0.5 + 0.5 + 0.0625   # read BF16, write 2 nibbles, metadata
@@ -49,9 +62,135 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--layers", type=int, default=None, help="override layer count (testing only)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=4)
+    p.add_argument("--cpu-layers", type=int, default=8)
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run one plain device copy of 512 MiB before the steps (counter calibration)")
+    p.add_argument("--summarize-trace", metavar="DIR")
+    p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     return p.parse_args()
 
+
+def decode_sources_hash() -> str:
+    h = hashlib.sha256()
+    for name in DECODE_SOURCES:
+        h.update((ROOT / "paper_2607_01831_amd" / "csrc" / name).read_bytes())
+    return h.hexdigest()
+
+
+def stored_traffic():
+    """HBM bytes per anchor-decode call from the committed counter summary,
+    or None when the decode kernels changed since it was taken."""
+    try:
+        text = TRAFFIC_SUMMARY.read_text()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        line = line.strip().strip("`")
+        if line.startswith(("kernel_sources_sha256:", "traffic_bytes_per_call:")):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("kernel_sources_sha256") != decode_sources_hash():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_call"])
+    except (KeyError, ValueError):
+        return None
+
+
+# ------------------------------------------------------------ rocprof summaries --
+
+def _csv(dirname, suffix):
+    files = glob.glob(os.path.join(dirname, "**", f"*{suffix}"), recursive=True)
+    if not files:
+        raise SystemExit(f"no *{suffix} under {dirname}")
+    with open(files[0], newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _short(name: str) -> str:
+    for key in ("anchor_decode_kernel", "attn_combine_kernel", "attn_split_kernel", "encode_kernel",
+                "merge_kernel", "copyBuffer"):
+        if key in name:
+            if key == "attn_split_kernel":
+                return "attn_split_kernel<codes>" if "(lynx::KvMode)1" in name else "attn_split_kernel<anchor>"
+            return key
+    return name.split("(")[0][:60]
+
+
+def _decode_calls(rows):
+    """Pair every anchor_decode_kernel dispatch with the attn_combine_kernel
+    dispatch that follows it: one lynx_attn_anchor_decode call."""
+    rows = sorted(rows, key=lambda r: int(r["Dispatch_Id"]))
+    calls, pending = [], None
+    for r in rows:
+        n = _short(r["Kernel_Name"])
+        if n == "anchor_decode_kernel":
+            pending = r
+        elif n == "attn_combine_kernel" and pending is not None:
+            calls.append((pending, r))
+            pending = None
+    return calls
+
+
+def summarize_trace(dirname):
+    rows = _csv(dirname, "kernel_trace.csv")
+    by = {}
+    for r in rows:
+        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        by.setdefault(_short(r["Kernel_Name"]), []).append(d)
+    print("| kernel | calls | avg us | min us | max us |\n|---|---|---|---|---|")
+    for n, ds in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| {n} | {len(ds)} | {sum(ds) / len(ds):.2f} | {min(ds):.2f} | {max(ds):.2f} |")
+    calls = _decode_calls(rows)
+    if calls:
+        split = [(int(a["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, _ in calls]
+        comb = [(int(b["End_Timestamp"]) - int(b["Start_Timestamp"])) / 1e3 for _, b in calls]
+        span = [(int(b["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, b in calls]
+        n = len(calls)
+        print(f"\nanchor-decode calls: {n}; per call: anchor_decode_kernel {sum(split) / n:.2f} us + "
+              f"attn_combine_kernel {sum(comb) / n:.2f} us = {(sum(split) + sum(comb)) / n:.2f} us of "
+              f"kernel time; first start to last end {sum(span) / n:.2f} us")
+
+
+def summarize_pmc(fetch_dir, write_dir):
+    def per_dispatch(dirname, counter):
+        return [(r, float(r["Counter_Value"])) for r in _csv(dirname, "counter_collection.csv")
+                if r["Counter_Name"] == counter]
+
+    fetch = per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = per_dispatch(write_dir, "WRITE_SIZE")
+
+    def copy_kib(table):
+        cands = [v for r, v in table if _short(r["Kernel_Name"]) == "copyBuffer"]
+        if not cands:
+            raise SystemExit("no copy kernel in the counter run (use --copy-calibration)")
+        return max(cands)
+
+    known_kib = COPY_CALIBRATION_BYTES / 1024
+    f_fetch = known_kib / copy_kib(fetch)
+    f_write = known_kib / copy_kib(write)
+
+    def decode_kib(table):
+        vals = {int(r["Dispatch_Id"]): v for r, v in table}
+        calls = _decode_calls([r for r, _ in table])
+        per = [vals[int(a["Dispatch_Id"])] + vals[int(b["Dispatch_Id"])] for a, b in calls]
+        return sum(per) / len(per), len(per)
+
+    fk, nf = decode_kib(fetch)
+    wk, nw = decode_kib(write)
+    traffic = fk * 1024 * f_fetch + wk * 1024 * f_write
+    print(f"copy calibration: a plain copy of {COPY_CALIBRATION_BYTES} bytes reads FETCH_SIZE "
+          f"{copy_kib(fetch):.0f} KiB and WRITE_SIZE {copy_kib(write):.0f} KiB; scale factors "
+          f"fetch {f_fetch:.4f}, write {f_write:.4f}")
+    print(f"anchor-decode calls measured: {nf} (FETCH), {nw} (WRITE)")
+    print(f"per call (anchor_decode_kernel + attn_combine_kernel): FETCH_SIZE {fk:.0f} KiB, "
+          f"WRITE_SIZE {wk:.0f} KiB")
+    print(f"kernel_sources_sha256: {decode_sources_hash()}")
+    print(f"traffic_bytes_per_call: {int(round(traffic))}")
+
+
+# --------------------------------------------------------------- CPU baseline --
 
 def cpu_baseline(w, layer_inputs, n_layers):
     """The CPU oracle, untuned, timed on this host on a bounded sample: the
@@ -79,16 +218,24 @@ def cpu_baseline(w, layer_inputs, n_layers):
     nbytes = n_layers * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
     return {"value": round(nbytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"anchor decode (fp64 oracle) of {n_layers} of {w.layers} layers, all "
-                      f"{Hkv} kv heads, {T} tokens; {t_dec:.2f} s"}
+            "sample": f"anchor decode (fp64 oracle, on its own encode of the same seeded inputs) "
+                      f"of {n_layers} of {w.layers} layers, all {Hkv} kv heads, {T} tokens; "
+                      f"{t_dec:.2f} s of decode"}
 
+
+# ----------------------------------------------------------------------- main --
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
-              "layout of this path is described in DESIGN.md and is not launched here.",
-              file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path (DESIGN.md describes how it would shard).", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -130,6 +277,14 @@ def main():
     outv = torch.empty(1, nq, Hq, 128, dtype=torch.bfloat16, device=dev)
     ws = lynx.workspace(L, 1, Hq, nq, T)
     torch.cuda.synchronize()
+    if args.copy_calibration:
+        # one plain device-to-device copy of known size, for the HBM counters
+        src = torch.ones(COPY_CALIBRATION_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     t_setup = time.perf_counter() - t_setup
 
     main_s = torch.cuda.current_stream()
@@ -197,12 +352,14 @@ def main():
     merge_gbps = elems * MERGE_BYTES_PER_ELEM / (t_merge * 1e-3) / 1e9
     dec_bytes = n_layers * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
     dec_gbps = dec_bytes / (t_dec * 1e-3) / 1e9
+    ver_bytes = n_layers * T * Hkv * VERIFY_BYTES_PER_TOKEN_HEAD
+    ver_gbps = ver_bytes / (t_ver * 1e-3) / 1e9
     h2d_gbps = (sum(h.numel() for h in host_k) * 2) / (t_h2d * 1e-3) / 1e9
     ver_us = t_ver * 1e3 / n_layers
     overlap = max(0.0, min(1.0, (t_dec + t_h2d - (ms("dec0", "merge0"))) / min(t_dec, t_h2d)))
 
-    per_launch_bytes = T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
-    per_launch_s = t_dec * 1e-3 / n_layers
+    per_call_bytes = T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
+    per_call_s = t_dec * 1e-3 / n_layers
     result = {
         "metric": METRIC,
         "value": round(dec_gbps, 2),
@@ -214,7 +371,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{WORKLOAD}: {n_layers} layers x ({Hq} q / {Hkv} kv heads, d=128), "
                                f"context {T}, batch 1, k={nq} drafts", "layers": n_layers,
@@ -223,30 +380,34 @@ def main():
         "hbm_frac": round(dec_gbps / HBM_PEAK_GBPS, 4),
         "stages": {
             "encode_GBps": round(enc_gbps, 2), "encode_frac": round(enc_gbps / HBM_PEAK_GBPS, 4),
+            "encode_us_per_layer": round(t_enc * 1e3 / n_layers, 2),
             "anchor_decode_GBps": round(dec_gbps, 2),
             "anchor_decode_us_per_layer": round(t_dec * 1e3 / n_layers, 3),
             "merge_GBps": round(merge_gbps, 2), "merge_frac": round(merge_gbps / HBM_PEAK_GBPS, 4),
+            "merge_us_per_layer": round(t_merge * 1e3 / n_layers, 2),
             "verify_us_per_layer": round(ver_us, 2),
+            "verify_GBps": round(ver_gbps, 2),
             "residual_h2d_GBps": round(h2d_gbps, 2),
             "decode_hidden_behind_h2d": round(overlap, 3),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
             "setup_s": round(t_setup, 1),
         },
         "roofline": {
-            "kernel": "anchor decode (split + combine kernels of one lynx_attn_anchor_decode call)",
+            "kernel": "one lynx_attn_anchor_decode call (anchor_decode_kernel + attn_combine_kernel)",
             "bound": "hbm",
-            "achieved": round(per_launch_bytes / per_launch_s / 1e9, 2),
+            "achieved": round(per_call_bytes / per_call_s / 1e9, 2),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
-            "frac": round(per_launch_bytes / per_launch_s / 1e9 / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "frac": round(per_call_bytes / per_call_s / 1e9 / HBM_PEAK_GBPS, 4),
+            "traffic": stored_traffic(),
+            "algorithmic_bytes_per_call": per_call_bytes,
+            "us_per_call": round(per_call_s * 1e6, 3),
         },
     }
     if not args.no_cpu_baseline:
         def layer_inputs(l):
-            return (inputs.kv(w, "k", layer=l, device=dev).cpu(),
-                    inputs.kv(w, "v", layer=l, device=dev).cpu(),
-                    inputs.queries(w, layer=l, device=dev).cpu())
+            return (inputs.kv(w, "k", layer=l), inputs.kv(w, "v", layer=l),
+                    inputs.queries(w, layer=l))
         result["cpu_baseline"] = cpu_baseline(w, layer_inputs, min(args.cpu_layers, n_layers))
     print(json.dumps(result), flush=True)
 
