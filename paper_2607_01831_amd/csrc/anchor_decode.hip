@@ -29,6 +29,7 @@
 // its own online softmax.  At the end the wavefronts are merged through LDS
 // into one partial (max, sum, output) per head, which the combine kernel of
 // attention.hip merges across splits.
+#include "lane_ops.h"
 #include "lynx_internal.h"
 
 #include <float.h>
@@ -39,9 +40,6 @@ namespace lynx {
 namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
-typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
-typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
-typedef __attribute__((__vector_size__(2 * sizeof(int)))) int intx2_t;
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
@@ -72,77 +70,6 @@ __device__ __forceinline__ u32x4_t nibbles_to_bf16(uint32_t w) {
     r[3] = __builtin_amdgcn_perm(c, hi, 0x04030402u);
     return r;
 }
-
-// 8 x 8 nibble transpose: in[i] holds 8 nibbles (element n at nibble n) of
-// row i; out[n] holds element n of rows 0..7 (row i at nibble i).
-__device__ __forceinline__ void transpose8x8_nibbles(const uint32_t *in, uint32_t *out) {
-    const uint32_t m = 0x0F0F0F0Fu;
-    uint32_t e[4], o[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const uint32_t a = in[2 * k], b = in[2 * k + 1];
-        e[k] = (a & m) | ((b << 4) & ~m);         // even elements, rows 2k | 2k+1
-        o[k] = ((a >> 4) & m) | (b & ~m);         // odd elements
-    }
-    uint32_t x[4][2];
-    // bytes -> 16-bit units of 4 rows
-    x[0][0] = __builtin_amdgcn_perm(e[1], e[0], 0x05010400u);  // elements 0, 2 ; rows 0-3
-    x[0][1] = __builtin_amdgcn_perm(e[1], e[0], 0x07030602u);  // elements 4, 6 ; rows 0-3
-    x[1][0] = __builtin_amdgcn_perm(e[3], e[2], 0x05010400u);  // elements 0, 2 ; rows 4-7
-    x[1][1] = __builtin_amdgcn_perm(e[3], e[2], 0x07030602u);  // elements 4, 6 ; rows 4-7
-    x[2][0] = __builtin_amdgcn_perm(o[1], o[0], 0x05010400u);  // elements 1, 3 ; rows 0-3
-    x[2][1] = __builtin_amdgcn_perm(o[1], o[0], 0x07030602u);  // elements 5, 7 ; rows 0-3
-    x[3][0] = __builtin_amdgcn_perm(o[3], o[2], 0x05010400u);  // elements 1, 3 ; rows 4-7
-    x[3][1] = __builtin_amdgcn_perm(o[3], o[2], 0x07030602u);  // elements 5, 7 ; rows 4-7
-    // 16-bit units -> 32-bit rows 0..7
-    out[0] = __builtin_amdgcn_perm(x[1][0], x[0][0], 0x05040100u);
-    out[2] = __builtin_amdgcn_perm(x[1][0], x[0][0], 0x07060302u);
-    out[4] = __builtin_amdgcn_perm(x[1][1], x[0][1], 0x05040100u);
-    out[6] = __builtin_amdgcn_perm(x[1][1], x[0][1], 0x07060302u);
-    out[1] = __builtin_amdgcn_perm(x[3][0], x[2][0], 0x05040100u);
-    out[3] = __builtin_amdgcn_perm(x[3][0], x[2][0], 0x07060302u);
-    out[5] = __builtin_amdgcn_perm(x[3][1], x[2][1], 0x05040100u);
-    out[7] = __builtin_amdgcn_perm(x[3][1], x[2][1], 0x07060302u);
-}
-
-// Cross-lane reductions on VALU permute paths (DPP inside a 16-lane row,
-// permlane16/32 swaps across rows), no LDS traffic.
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ float row16_sum(float v) {  // over the 16 lanes of a row
-    v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
-    v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
-    v += dpp<0x141>(v);  // row_half_mirror
-    return v + dpp<0x140>(v);  // row_mirror
-}
-// Over lanes l, l^16, l^32, l^48 (the four rows of one column).
-__device__ __forceinline__ float sum_kg(float v) {
-    auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
-    v = __int_as_float(r[0]) + __int_as_float(r[1]);
-    r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
-    return __int_as_float(r[0]) + __int_as_float(r[1]);
-}
-// Maximum of values that are finite or -inf (never NaN), without the NaN
-// canonicalisation the compiler adds around fmaxf.
-__device__ __forceinline__ float fmax2(float a, float b) {
-    float r;
-    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
-__device__ __forceinline__ float fmax3(float a, float b, float c) {
-    float r;
-    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-    return r;
-}
-__device__ __forceinline__ float max_kg(float v) {
-    auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
-    v = fmax2(__int_as_float(r[0]), __int_as_float(r[1]));
-    r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
-    return fmax2(__int_as_float(r[0]), __int_as_float(r[1]));
-}
-__device__ __forceinline__ float wave_sum(float v) { return sum_kg(row16_sum(v)); }
 
 // One wavefront's registers for one 32-token tile: 16-byte pieces of the K
 // and V nibble rows (row col and col + 16 of the tile, dims 32 kg..32 kg+31).

@@ -37,6 +37,7 @@ struct AttnArgs {
     Geometry geo;
     int B, Hq, nq, G, max_seq_len;
     int rows_total, n_ctx_splits, n_splits, split_tokens;
+    int split_base;  // split index of blockIdx.x == 0
     const int32_t *seq_lens;
     const int32_t *block_table;
     const uint8_t *k_plane;
@@ -112,7 +113,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_split_kernel(AttnArgs a) {
     constexpr int kRowBytes = MODE == KvMode::kAnchor ? kNibbleRow : kCodeRow;
 
     const int Hkv = a.geo.Hkv;
-    const int split = blockIdx.x;
+    const int split = blockIdx.x + a.split_base;
     const int h = blockIdx.y % Hkv;
     const int chunk = blockIdx.y / Hkv;
     const int b = blockIdx.z;
@@ -533,6 +534,7 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
     a.n_ctx_splits = plan.n_ctx_splits;
     a.n_splits = plan.n_splits;
     a.split_tokens = plan.split_tokens;
+    a.split_base = 0;
     a.seq_lens = seq_lens;
     a.block_table = block_table;
     a.k_plane = k_plane;
@@ -571,11 +573,41 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
         const int chunks = (a.G + d.chunk_heads - 1) / d.chunk_heads;
         hipError_t e = launch_anchor_decode_mfma(d, chunks, stream);
         if (e != hipSuccess) return e;
+    } else if (mode == KvMode::kCodes) {
+        // matrix-core verification over the context splits ...
+        VerifyArgs v;
+        v.geo = g;
+        v.B = B;
+        v.Hq = Hq;
+        v.G = a.G;
+        v.nq = nq;
+        v.max_seq_len = max_seq_len;
+        v.rows_total = plan.rows_total;
+        v.n_ctx_splits = plan.n_ctx_splits;
+        v.ws_splits = plan.n_splits;
+        v.bt_shift = -1;
+        for (int sh = 0; sh < 31; ++sh)
+            if ((1 << sh) == g.bt) v.bt_shift = sh;
+        v.seq_lens = seq_lens;
+        v.block_table = block_table;
+        v.k_codes = k_plane;
+        v.v_codes = v_plane;
+        v.meta = meta;
+        v.q = q;
+        v.ws_o = a.ws_o;
+        v.ws_ml = a.ws_ml;
+        hipError_t e = launch_verify_mfma(v, plan.split_tokens / kKGroup, stream);
+        if (e != hipSuccess) return e;
+        // ... and the BF16 draft tail as the last split, on the vector units
+        if (plan.n_splits > plan.n_ctx_splits) {
+            a.split_base = plan.n_ctx_splits;
+            dim3 grid(1, g.Hkv * plan.n_chunks, B);
+            e = launch_split<KvMode::kCodes>(plan.rows_chunk, grid, a, stream);
+            if (e != hipSuccess) return e;
+        }
     } else {
         dim3 grid(plan.n_splits, g.Hkv * plan.n_chunks, B);
-        hipError_t e = mode == KvMode::kAnchor
-                           ? launch_split<KvMode::kAnchor>(plan.rows_chunk, grid, a, stream)
-                           : launch_split<KvMode::kCodes>(plan.rows_chunk, grid, a, stream);
+        hipError_t e = launch_split<KvMode::kAnchor>(plan.rows_chunk, grid, a, stream);
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(attn_combine_kernel, dim3(plan.rows_total, g.Hkv, B), dim3(kCombineThreads),

@@ -70,6 +70,27 @@ struct DecodeArgs {
 
 hipError_t launch_anchor_decode_mfma(const DecodeArgs &args, int chunks, hipStream_t stream);
 
+// Arguments of the matrix-core verification kernel (verify.hip): context
+// splits only; the BF16 draft tail is the last split, computed elsewhere.
+struct VerifyArgs {
+    Geometry geo;
+    int B, Hq, G, nq, max_seq_len;
+    int rows_total;    // nq * G query rows per (sequence, kv head)
+    int n_ctx_splits;  // grid.x
+    int ws_splits;     // partial-row stride (context splits + tail)
+    int bt_shift;      // log2(block_tokens) when it is a power of two, else -1
+    const int32_t *seq_lens;
+    const int32_t *block_table;
+    const uint8_t *k_codes;
+    const uint8_t *v_codes;
+    MetaPtrs meta;
+    const uint16_t *q;  // BF16 [B][nq][Hq][128]
+    float *ws_o;
+    float2 *ws_ml;
+};
+
+hipError_t launch_verify_mfma(const VerifyArgs &args, int split_groups, hipStream_t stream);
+
 AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_len, bool tail);
 
 hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan, int B, int Hq,
