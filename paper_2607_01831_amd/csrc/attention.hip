@@ -38,6 +38,7 @@ struct AttnArgs {
     int B, Hq, nq, G, max_seq_len;
     int rows_total, n_ctx_splits, n_splits, split_tokens;
     int split_base;  // split index of blockIdx.x == 0
+    int tail_in_combine;  // the combine kernel attends the BF16 draft tail itself
     const int32_t *seq_lens;
     const int32_t *block_table;
     const uint8_t *k_plane;
@@ -393,12 +394,36 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     const int b = blockIdx.z;
     const int tid = threadIdx.x;
     const int Hkv = a.geo.Hkv;
-    const int n = a.n_splits;
-    const size_t base = (((size_t)b * Hkv + h) * a.rows_total + gr) * n;
+    const size_t base = (((size_t)b * Hkv + h) * a.rows_total + gr) * a.n_splits;
+    // splits with partials: every split, or the context ones when this kernel
+    // attends the draft tail itself
+    const int n = a.tail_in_combine ? a.n_ctx_splits : a.n_splits;
     constexpr int kGroups = kCombineThreads / (kHeadDim / 4);  // 8 split groups
     constexpr int kBatch = 16;
     __shared__ float4 s_acc[kGroups][kHeadDim / 4];
     __shared__ float s_m[kGroups][kHeadDim / 4], s_l[kGroups][kHeadDim / 4];
+    __shared__ float s_ts[64];  // draft-tail scores (log2 units)
+
+    // query row gr <-> (draft qi, head qg); with a tail, draft qi also sees
+    // the BF16 K/V of drafts 0..qi (causal among the drafts)
+    const int qi = gr / a.G;
+    const int qg = gr % a.G;
+    const size_t qrow = ((size_t)b * a.nq + qi) * a.Hq + (size_t)h * a.G + qg;
+    const int n_tail = a.tail_in_combine ? qi + 1 : 0;
+    if (n_tail > 0) {
+        const int lane = tid & 63, wv = tid >> 6;
+        const uint32_t qw = reinterpret_cast<const uint32_t *>(a.q + qrow * kHeadDim)[lane];
+        const float q0 = bf16_lo(qw), q1 = bf16_hi(qw);
+        const float sm = kLog2e * rsqrtf((float)kHeadDim);
+        for (int j = wv; j < n_tail; j += kCombineThreads / 64) {
+            const uint32_t kw = reinterpret_cast<const uint32_t *>(
+                a.k_new + (((size_t)b * a.nq + j) * Hkv + h) * kHeadDim)[lane];
+            float d = fmaf(q0, bf16_lo(kw), q1 * bf16_hi(kw));
+#pragma unroll
+            for (int s = 1; s < 64; s <<= 1) d += __shfl_xor(d, s);
+            if (lane == 0) s_ts[j] = d * sm;
+        }
+    }
 
     const int d4 = tid % (kHeadDim / 4);
     const int sg = tid / (kHeadDim / 4);
@@ -446,12 +471,31 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     s_l[sg][d4] = nan ? NAN : l_t;
     __syncthreads();
     if (sg == 0) {
-        float M = -INFINITY;
+        // the draft tail as one more partial: (tm, tl, to) over dims 4 d4 ..
+        float tm = -INFINITY, tl = 0.0f;
+        float4 to = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < n_tail; ++j) tm = fmaxf(tm, s_ts[j]);
+        for (int j = 0; j < n_tail; ++j) {
+            const float p = exp2f(s_ts[j] - tm);
+            const uint2 vw = *reinterpret_cast<const uint2 *>(
+                a.v_new + (((size_t)b * a.nq + j) * Hkv + h) * kHeadDim + 4 * d4);
+            tl += p;
+            to.x = fmaf(p, bf16_lo(vw.x), to.x);
+            to.y = fmaf(p, bf16_hi(vw.x), to.y);
+            to.z = fmaf(p, bf16_lo(vw.y), to.z);
+            to.w = fmaf(p, bf16_hi(vw.y), to.w);
+        }
+        float M = tm;
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) M = fmaxf(M, s_m[g][d4]);
         float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
         float L = 0.0f;
         bool any_nan = false;
+        if (n_tail > 0) {
+            const float f = exp2f(tm - M);
+            O = make_float4(to.x * f, to.y * f, to.z * f, to.w * f);
+            L = tl * f;
+        }
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
             const float f = s_m[g][d4] == -INFINITY ? 0.0f : exp2f(s_m[g][d4] - M);
@@ -466,9 +510,7 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
         float r[4] = {O.x, O.y, O.z, O.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) r[i] = any_nan ? NAN : (L > 0.0f ? r[i] / L : 0.0f);
-        const int i = gr / a.G;
-        const int g = gr % a.G;
-        const size_t row = ((size_t)b * a.nq + i) * a.Hq + (size_t)h * a.G + g;
+        const size_t row = qrow;
         const uint32_t lo = f32_to_bf16_rne(r[0]) | ((uint32_t)f32_to_bf16_rne(r[1]) << 16);
         const uint32_t hi = f32_to_bf16_rne(r[2]) | ((uint32_t)f32_to_bf16_rne(r[3]) << 16);
         *reinterpret_cast<uint2 *>(out + row * kHeadDim + 4 * d4) = make_uint2(lo, hi);
@@ -535,6 +577,7 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
     a.n_splits = plan.n_splits;
     a.split_tokens = plan.split_tokens;
     a.split_base = 0;
+    a.tail_in_combine = (mode == KvMode::kCodes && k_new != nullptr) ? 1 : 0;
     a.seq_lens = seq_lens;
     a.block_table = block_table;
     a.k_plane = k_plane;
@@ -598,13 +641,7 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
         v.ws_ml = a.ws_ml;
         hipError_t e = launch_verify_mfma(v, plan.split_tokens / kKGroup, stream);
         if (e != hipSuccess) return e;
-        // ... and the BF16 draft tail as the last split, on the vector units
-        if (plan.n_splits > plan.n_ctx_splits) {
-            a.split_base = plan.n_ctx_splits;
-            dim3 grid(1, g.Hkv * plan.n_chunks, B);
-            e = launch_split<KvMode::kCodes>(plan.rows_chunk, grid, a, stream);
-            if (e != hipSuccess) return e;
-        }
+        // the BF16 draft tail is attended by the combine kernel below
     } else {
         dim3 grid(plan.n_splits, g.Hkv * plan.n_chunks, B);
         hipError_t e = launch_split<KvMode::kAnchor>(plan.rows_chunk, grid, a, stream);
