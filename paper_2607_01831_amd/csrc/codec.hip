@@ -47,39 +47,86 @@ __device__ __forceinline__ void group_params(float mn, float mx, float &zero, fl
     zero = mn;
 }
 
-__device__ __forceinline__ uint32_t quantize(float x, float zero, float inv) {
-    const float y = (x - zero) * inv;
-    float c = rintf(y);
-    c = (c >= 0.0f) ? c : 0.0f;  // NaN -> 0
-    c = (c > 255.0f) ? 255.0f : c;
-    return (uint32_t)c;
+// Min / max without the NaN canonicalisation the compiler adds around
+// fminf / fmaxf (non-finite inputs give unspecified codes).
+__device__ __forceinline__ float vmin3(float a, float b, float c) {
+    float r;
+    asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+__device__ __forceinline__ float vmax3(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+__device__ __forceinline__ float vmin(float a, float b) {
+    float r;
+    asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ float vmax(float a, float b) {
+    float r;
+    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+// over the 16 lanes of a row
+__device__ __forceinline__ float row16_min(float v) {
+    v = vmin(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+    v = vmin(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+    v = vmin(v, dpp<0x141>(v));  // row_half_mirror
+    return vmin(v, dpp<0x140>(v));  // row_mirror
+}
+__device__ __forceinline__ float row16_max(float v) {
+    v = vmax(v, dpp<0xB1>(v));
+    v = vmax(v, dpp<0x4E>(v));
+    v = vmax(v, dpp<0x141>(v));
+    return vmax(v, dpp<0x140>(v));
+}
+// over lanes l, l^16, l^32, l^48
+__device__ __forceinline__ float rows_min(float v) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
+    v = vmin(__int_as_float(r[0]), __int_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
+    return vmin(__int_as_float(r[0]), __int_as_float(r[1]));
+}
+__device__ __forceinline__ float rows_max(float v) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
+    v = vmax(__int_as_float(r[0]), __int_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
+    return vmax(__int_as_float(r[0]), __int_as_float(r[1]));
 }
 
-// Eight codes (dims 8m..8m+7) -> one 32-bit word of anchor nibbles and one of
-// residual nibbles; nibble j of the word is dim 8m+j (low nibble = even dim).
-__device__ __forceinline__ void split_pack8(const uint32_t *c, uint32_t &anc, uint32_t &res) {
-    anc = 0;
-    res = 0;
+// Eight values -> eight codes clamp(rint((x - zero) * inv), 0, 255), then
+// the anchor word (nibble j = code_j >> 4) and the residual word (nibble j =
+// code_j & 15).  v_cvt_pk_u8_f32 rounds half to even and saturates to
+// [0, 255] (NaN -> 0), which is exactly the clamp-of-rint of the definition.
+__device__ __forceinline__ void quantize_split8(const float *x, const float *zero, const float *inv,
+                                                uint32_t &anc, uint32_t &res) {
+    uint32_t w[2] = {0u, 0u};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        anc |= (c[j] >> 4) << (4 * j);
-        res |= (c[j] & 15u) << (4 * j);
+        const float y = (x[j] - zero[j]) * inv[j];
+        w[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(y, (uint32_t)(j & 3), w[j >> 2]);
     }
-}
-
-__device__ __forceinline__ float wave_min_xor(float v, int lane_mask) {
-    return fminf(v, __shfl_xor(v, lane_mask));
-}
-__device__ __forceinline__ float wave_max_xor(float v, int lane_mask) {
-    return fmaxf(v, __shfl_xor(v, lane_mask));
+    // bytes (c0, c1, c2, c3) -> nibble pairs c0 | c1 << 4 in byte 0, c2 | c3 << 4 in byte 2
+    const uint32_t a0 = (w[0] >> 4) & 0x0F0F0F0Fu, a1 = (w[1] >> 4) & 0x0F0F0F0Fu;
+    const uint32_t r0 = w[0] & 0x0F0F0F0Fu, r1 = w[1] & 0x0F0F0F0Fu;
+    anc = __builtin_amdgcn_perm(a1 | (a1 >> 4), a0 | (a0 >> 4), 0x06040200u);
+    res = __builtin_amdgcn_perm(r1 | (r1 >> 4), r0 | (r0 >> 4), 0x06040200u);
 }
 
 // One workgroup encodes one 128-token window of one kv head for K and V.
 // Thread (tr = tid / 16, m = tid % 16) owns dims 8m..8m+7 of the window's
 // tokens tr, tr+16, ..., tr+112: every 16-byte load is part of a fully used
-// 256-byte token row, and a token's 16 owners are 16 adjacent lanes.
+// 256-byte token row, and a token's 16 owners are the 16 lanes of one DPP
+// row.  LAYOUT 0: one block per sequence; 1: paged.
+template <int LAYOUT>
 __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
-    Geometry geo, int b, int T, const int32_t *__restrict__ block_table,
+    Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
     const uint16_t *__restrict__ k, const uint16_t *__restrict__ v, uint8_t *__restrict__ k_anc,
     uint8_t *__restrict__ v_anc, uint8_t *__restrict__ k_res, uint8_t *__restrict__ v_res,
     MetaPtrs meta) {
@@ -102,41 +149,48 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     uint4 kraw[8], vraw[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const int tl = tr + 16 * i;
-        if (tl < n) {
-            const size_t e = ((size_t)(t0 + tl) * Hkv + h) * kHeadDim + 8 * m;
-            kraw[i] = *reinterpret_cast<const uint4 *>(k + e);
-            vraw[i] = *reinterpret_cast<const uint4 *>(v + e);
-        } else {
-            kraw[i] = make_uint4(0, 0, 0, 0);
-            vraw[i] = make_uint4(0, 0, 0, 0);
-        }
+        const int tl = min(tr + 16 * i, n - 1);  // rows past the window re-read its last token
+        const size_t e = ((size_t)(t0 + tl) * Hkv + h) * kHeadDim + 8 * m;
+        kraw[i] = *reinterpret_cast<const uint4 *>(k + e);
+        vraw[i] = *reinterpret_cast<const uint4 *>(v + e);
     }
 
-    // ---- K: per-channel min/max over the window's valid tokens ----
+    // Plane row of token t (the block lookup of a paged cache is checked).
+    const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
+    auto plane_row = [&](int t, bool &ok) -> size_t {
+        int blk, tb;
+        if (LAYOUT == 0) {
+            blk = bt_row[0];
+            tb = t;
+        } else {
+            const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
+            blk = bt_row[bi];
+            tb = t - bi * geo.bt;
+        }
+        ok = blk >= 0 && blk < geo.num_blocks;
+        return ((size_t)blk * Hkv + h) * geo.bt + tb;
+    };
+
+    // ---- K: per-channel min/max over the window's tokens (the re-read
+    // last token of a short window changes neither) ----
     float kmin[8], kmax[8];
+    {
+        float x[8][8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        kmin[j] = FLT_MAX * 2.0f;   // +inf
-        kmax[j] = -FLT_MAX * 2.0f;  // -inf
-    }
+        for (int i = 0; i < 8; ++i) unpack8(kraw[i], x[i]);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        if (tr + 16 * i < n) {
-            float x[8];
-            unpack8(kraw[i], x);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                kmin[j] = fminf(kmin[j], x[j]);
-                kmax[j] = fmaxf(kmax[j], x[j]);
-            }
+        for (int j = 0; j < 8; ++j) {
+            kmin[j] = vmin3(vmin3(x[0][j], x[1][j], x[2][j]), vmin3(x[3][j], x[4][j], x[5][j]),
+                            vmin(x[6][j], x[7][j]));
+            kmax[j] = vmax3(vmax3(x[0][j], x[1][j], x[2][j]), vmax3(x[3][j], x[4][j], x[5][j]),
+                            vmax(x[6][j], x[7][j]));
         }
     }
     // lanes m, m+16, m+32, m+48 of a wave hold the same channels
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        kmin[j] = wave_min_xor(wave_min_xor(kmin[j], 16), 32);
-        kmax[j] = wave_max_xor(wave_max_xor(kmax[j], 16), 32);
+        kmin[j] = rows_min(kmin[j]);
+        kmax[j] = rows_max(kmax[j]);
     }
     if ((tid & 63) < 16) {
 #pragma unroll
@@ -148,8 +202,8 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     __syncthreads();
     if (tid < kHeadDim) {
         const int d = tid;
-        const float mn = fminf(fminf(s_min[0][d], s_min[1][d]), fminf(s_min[2][d], s_min[3][d]));
-        const float mx = fmaxf(fmaxf(s_max[0][d], s_max[1][d]), fmaxf(s_max[2][d], s_max[3][d]));
+        const float mn = vmin(vmin(s_min[0][d], s_min[1][d]), vmin(s_min[2][d], s_min[3][d]));
+        const float mx = vmax(vmax(s_max[0][d], s_max[1][d]), vmax(s_max[2][d], s_max[3][d]));
         float zero, scale, inv;
         group_params(mn, mx, zero, scale, inv);
         s_zero[d] = zero;
@@ -158,77 +212,69 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
         meta.k_scale[mi] = scale;
         meta.k_zero[mi] = zero;
     }
+
+    // ---- V: per-token groups over 128 dims (the 16 lanes of a DPP row),
+    // computed while the K parameters are being published ----
+    float vzero[8], vinv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float x[8];
+        unpack8(vraw[i], x);
+        float mn = vmin3(vmin3(x[0], x[1], x[2]), vmin3(x[3], x[4], x[5]), vmin(x[6], x[7]));
+        float mx = vmax3(vmax3(x[0], x[1], x[2]), vmax3(x[3], x[4], x[5]), vmax(x[6], x[7]));
+        mn = row16_min(mn);
+        mx = row16_max(mx);
+        float scale;
+        group_params(mn, mx, vzero[i], scale, vinv[i]);
+        const int tl = tr + 16 * i;
+        if (m == 0 && tl < n) {
+            const size_t mi = ((size_t)b * Hkv + h) * geo.max_tokens + t0 + tl;
+            meta.v_scale[mi] = scale;
+            meta.v_zero[mi] = vzero[i];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int tl = tr + 16 * i;
+        if (tl < n) {
+            bool ok;
+            const size_t off = plane_row(t0 + tl, ok) * kNibbleRow + 4 * m;
+            if (ok) {
+                float x[8];
+                unpack8(vraw[i], x);
+                const float zv[8] = {vzero[i], vzero[i], vzero[i], vzero[i],
+                                     vzero[i], vzero[i], vzero[i], vzero[i]};
+                const float iv[8] = {vinv[i], vinv[i], vinv[i], vinv[i],
+                                     vinv[i], vinv[i], vinv[i], vinv[i]};
+                uint32_t a, r;
+                quantize_split8(x, zv, iv, a, r);
+                *reinterpret_cast<uint32_t *>(v_anc + off) = a;
+                *reinterpret_cast<uint32_t *>(v_res + off) = r;
+            }
+        }
+    }
     __syncthreads();
 
+    // ---- K codes -> planes ----
     float kz[8], ki[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         kz[j] = s_zero[8 * m + j];
         ki[j] = s_inv[8 * m + j];
     }
-
-    const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
-
-    // ---- K codes -> planes ----
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int tl = tr + 16 * i;
         if (tl < n) {
-            const int t = t0 + tl;
-            const int blk = bt_row[t / geo.bt];
-            if (blk >= 0 && blk < geo.num_blocks) {
+            bool ok;
+            const size_t off = plane_row(t0 + tl, ok) * kNibbleRow + 4 * m;
+            if (ok) {
                 float x[8];
-                uint32_t c[8];
                 unpack8(kraw[i], x);
-#pragma unroll
-                for (int j = 0; j < 8; ++j) c[j] = quantize(x[j], kz[j], ki[j]);
                 uint32_t a, r;
-                split_pack8(c, a, r);
-                const size_t off =
-                    (((size_t)blk * Hkv + h) * geo.bt + (t % geo.bt)) * kNibbleRow + 4 * m;
+                quantize_split8(x, kz, ki, a, r);
                 *reinterpret_cast<uint32_t *>(k_anc + off) = a;
                 *reinterpret_cast<uint32_t *>(k_res + off) = r;
-            }
-        }
-    }
-
-    // ---- V: per-token groups over 128 dims (16 adjacent lanes per token) ----
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int tl = tr + 16 * i;
-        float x[8];
-        unpack8(vraw[i], x);
-        float mn = x[0], mx = x[0];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) {
-            mn = fminf(mn, x[j]);
-            mx = fmaxf(mx, x[j]);
-        }
-#pragma unroll
-        for (int s = 1; s < 16; s <<= 1) {
-            mn = wave_min_xor(mn, s);
-            mx = wave_max_xor(mx, s);
-        }
-        if (tl < n) {
-            const int t = t0 + tl;
-            float zero, scale, inv;
-            group_params(mn, mx, zero, scale, inv);
-            if (m == 0) {
-                const size_t mi = ((size_t)b * Hkv + h) * geo.max_tokens + t;
-                meta.v_scale[mi] = scale;
-                meta.v_zero[mi] = zero;
-            }
-            const int blk = bt_row[t / geo.bt];
-            if (blk >= 0 && blk < geo.num_blocks) {
-                uint32_t c[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) c[j] = quantize(x[j], zero, inv);
-                uint32_t a, r;
-                split_pack8(c, a, r);
-                const size_t off =
-                    (((size_t)blk * Hkv + h) * geo.bt + (t % geo.bt)) * kNibbleRow + 4 * m;
-                *reinterpret_cast<uint32_t *>(v_anc + off) = a;
-                *reinterpret_cast<uint32_t *>(v_res + off) = r;
             }
         }
     }
@@ -286,8 +332,15 @@ hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_t
                          uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream) {
     if (T <= 0) return hipSuccess;
     dim3 grid((T + kKGroup - 1) / kKGroup, g.Hkv);
-    hipLaunchKernelGGL(encode_kernel, grid, dim3(kEncodeThreads), 0, stream, g, b, T,
-                       block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
+    int bt_shift = -1;
+    for (int sh = 0; sh < 31; ++sh)
+        if ((1 << sh) == g.bt) bt_shift = sh;
+    if (g.max_blocks == 1)
+        hipLaunchKernelGGL(encode_kernel<0>, grid, dim3(kEncodeThreads), 0, stream, g, b, T, bt_shift,
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
+    else
+        hipLaunchKernelGGL(encode_kernel<1>, grid, dim3(kEncodeThreads), 0, stream, g, b, T, bt_shift,
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
     return hipGetLastError();
 }
 
