@@ -45,7 +45,6 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kTile = 32;      // tokens per wavefront step
-constexpr int kPrefetch = 2;   // tiles in flight ahead of the one being computed
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ f32x4_t mfma(u32x4_t a, u32x4_t b, f32x4_t c) {
@@ -100,6 +99,9 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
     constexpr int NP = kWaves / RT;  // wavefronts sharing one row tile
     constexpr int TPG = 4 / NP;      // tiles of a group per wavefront
     constexpr int kTilesPerWave = SG * TPG;
+    // tiles in flight ahead of the one being computed (one for two row tiles:
+    // registers; each wavefront then still has 8 KB of K/V loads in flight)
+    constexpr int kPrefetch = RT == 1 ? 2 : 1;
     const int Hkv = a.geo.Hkv;
     const int split = blockIdx.x;
     const int h = blockIdx.y % Hkv;
