@@ -491,28 +491,44 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     }
     const bool any_bad = __syncthreads_or(bad);
 
-    // ---- merge the wavefronts, write this split's partial ----
-    for (int idx = tid; idx < heads * kHeadDim; idx += kThreads) {
-        const int hh = idx / kHeadDim;
-        const int dd = idx % kHeadDim;
+    // ---- merge the wavefronts, write this split's partial: per-head
+    // factors first, then float4 multiply-adds ----
+    __shared__ float s_f[kWaves][GP], s_ML[GP][2];
+    if (tid < heads) {
+        const int hh = tid;
         float M = -INFINITY;
 #pragma unroll
         for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, s_m[ww][hh]);
-        float O = 0.0f, L = 0.0f;
-        if (M != -INFINITY) {
+        float L = 0.0f;
 #pragma unroll
-            for (int ww = 0; ww < kWaves; ++ww) {
-                if (s_m[ww][hh] == -INFINITY) continue;
-                const float f = exp2f(s_m[ww][hh] - M);
-                O += (s_o[ww][hh][dd] + s_ob[ww][hh]) * f;
-                L += s_l[ww][hh] * f;
-            }
+        for (int ww = 0; ww < kWaves; ++ww) {
+            const float f = (M == -INFINITY || s_m[ww][hh] == -INFINITY) ? 0.0f : exp2f(s_m[ww][hh] - M);
+            s_f[ww][hh] = f;
+            L = fmaf(s_l[ww][hh], f, L);
         }
-        if (any_bad) O = L = NAN;
+        s_ML[hh][0] = M;
+        s_ML[hh][1] = any_bad ? NAN : L;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < heads * (kHeadDim / 4); idx += kThreads) {
+        const int hh = idx / (kHeadDim / 4);
+        const int d4 = idx % (kHeadDim / 4);
+        float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int ww = 0; ww < kWaves; ++ww) {
+            const float f = s_f[ww][hh];
+            const float ob = s_ob[ww][hh];
+            const float4 o = reinterpret_cast<const float4 *>(&s_o[ww][hh][0])[d4];
+            O.x = fmaf(o.x + ob, f, O.x);
+            O.y = fmaf(o.y + ob, f, O.y);
+            O.z = fmaf(o.z + ob, f, O.z);
+            O.w = fmaf(o.w + ob, f, O.w);
+        }
+        if (any_bad) O = make_float4(NAN, NAN, NAN, NAN);
         const int gr = chunk * a.chunk_heads + hh;  // row = head within the kv group
         const size_t pi = (((size_t)b * Hkv + h) * a.rows_total + gr) * a.ws_splits + split;
-        a.ws_o[pi * kHeadDim + dd] = O;
-        if (dd == 0) a.ws_ml[pi] = make_float2(M, L);
+        reinterpret_cast<float4 *>(a.ws_o + pi * kHeadDim)[d4] = O;
+        if (d4 == 0) a.ws_ml[pi] = make_float2(s_ML[hh][0], s_ML[hh][1]);
     }
   } else {
     // a split past the context: (max, sum) = (-inf, 0), no output

@@ -494,34 +494,50 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
             s_o[(w * 16 + 4 * kg + i) * kHeadDim + 16 * c + col] = acc[c][i] - acc_off[i];
     const bool any_bad = __syncthreads_or(bad);
 
-    // ---- merge the wavefronts of each row tile, write this split's partial ----
-    const float ev_scale = ldexpf(1.0f, Ev);
-    for (int idx = tid; idx < RT * 16 * kHeadDim; idx += kThreads) {
-        const int rr = idx / kHeadDim;  // row within the workgroup
-        const int dd = idx % kHeadDim;
-        const int rtile = rr / 16, r16 = rr % 16;
-        const int row = row_base + rr;
-        if (row >= a.rows_total) continue;
+    // ---- merge the wavefronts of each row tile, write this split's partial:
+    // per-row factors first, then float4 multiply-adds ----
+    __shared__ float s_f[kWaves][16], s_ML[RT * 16][2];
+    if (tid < RT * 16) {
+        const int rtile = tid / 16, r16 = tid % 16;
         float M = -INFINITY;
 #pragma unroll
         for (int p = 0; p < NP; ++p) M = fmaxf(M, s_m[p * RT + rtile][r16]);
-        float O = 0.0f, L = 0.0f;
-        if (M != -INFINITY) {
+        const float ev_scale = ldexpf(1.0f, Ev);
+        float L = 0.0f;
 #pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                const int ww = p * RT + rtile;
-                if (s_m[ww][r16] == -INFINITY) continue;
-                const float f = exp2f(s_m[ww][r16] - M);
-                O += (s_o[(ww * 16 + r16) * kHeadDim + dd] + s_ob[ww][r16]) * f;
-                L += s_l[ww][r16] * f;
-            }
+        for (int p = 0; p < NP; ++p) {
+            const int ww = p * RT + rtile;
+            const float f = (M == -INFINITY || s_m[ww][r16] == -INFINITY) ? 0.0f
+                                                                           : exp2f(s_m[ww][r16] - M) * ev_scale;
+            s_f[ww][r16] = f;
+            L = fmaf(s_l[ww][r16], f, L);
         }
-        O *= ev_scale;
-        L *= ev_scale;
-        if (any_bad) O = L = NAN;
+        s_ML[tid][0] = M;
+        s_ML[tid][1] = any_bad ? NAN : L;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < RT * 16 * (kHeadDim / 4); idx += kThreads) {
+        const int rr = idx / (kHeadDim / 4);  // row within the workgroup
+        const int d4 = idx % (kHeadDim / 4);
+        const int rtile = rr / 16, r16 = rr % 16;
+        const int row = row_base + rr;
+        if (row >= a.rows_total) continue;
+        float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const int ww = p * RT + rtile;
+            const float f = s_f[ww][r16];
+            const float ob = s_ob[ww][r16];
+            const float4 o = reinterpret_cast<const float4 *>(s_o + (ww * 16 + r16) * kHeadDim)[d4];
+            O.x = fmaf(o.x + ob, f, O.x);
+            O.y = fmaf(o.y + ob, f, O.y);
+            O.z = fmaf(o.z + ob, f, O.z);
+            O.w = fmaf(o.w + ob, f, O.w);
+        }
+        if (any_bad) O = make_float4(NAN, NAN, NAN, NAN);
         const size_t pi = partial_index(row);
-        a.ws_o[pi * kHeadDim + dd] = O;
-        if (dd == 0) a.ws_ml[pi] = make_float2(M, L);
+        reinterpret_cast<float4 *>(a.ws_o + pi * kHeadDim)[d4] = O;
+        if (d4 == 0) a.ws_ml[pi] = make_float2(s_ML[rr][0], s_ML[rr][1]);
     }
 }
 
