@@ -8,11 +8,13 @@ verification.  Synthetic data, seeded.
 
 One step = the whole hot path over all 32 layers:
   1. encode (quantize, split, pack) every layer's K/V       [main stream]
-  2. residual transport: H2D copy of every layer's residual planes from
-     pinned host memory, standing in for the network          [side stream]
+  2. residual transport: H2D copy of the residual planes of all layers (one
+     allocation per plane kind) from pinned host memory, standing in for
+     the network                                              [side stream]
      overlapped with
   3. anchor-only decode attention, one query token per layer   [main stream]
-  4. wait for the residual, merge anchor + residual -> codes   [main stream]
+  4. wait for the residual, merge anchor + residual -> codes, one call per
+     plane kind over all layers                               [main stream]
   5. verification attention of the 8 drafts over the codes    [main stream]
 
 Printed: one JSON line.  `value` is the anchor-decode attention throughput in
@@ -43,7 +45,7 @@ sys.path.insert(0, str(ROOT))
 HBM_PEAK_GBPS = 8000.0
 METRIC = "anchor decode-attn KV GB/s (% HBM peak); encode/merge GB/s; verify µs @128k"
 WORKLOAD = "llama3-8b-32k"
-COPY_CALIBRATION_BYTES = 512 << 20
+COPY_CALIBRATION_BYTES = 640 << 20
 TRAFFIC_SUMMARY = ROOT / "profiles" / "anchor_decode_llama3-8b-32k_traffic.md"
 # sources whose kernels make up one anchor-decode call
 DECODE_SOURCES = ["anchor_decode.hip", "attention.hip", "lynx_internal.h"]
@@ -64,7 +66,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=8)
     p.add_argument("--copy-calibration", action="store_true",
-                   help="run one plain device copy of 512 MiB before the steps (counter calibration)")
+                   help="run one plain device copy of 640 MiB before the steps (counter calibration)")
     p.add_argument("--summarize-trace", metavar="DIR")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     return p.parse_args()
@@ -255,7 +257,7 @@ def main():
 
     # ---------------- set-up (untimed) ----------------
     t_setup = time.perf_counter()
-    K, V, Q, QV, KN, VN, pools = [], [], [], [], [], [], []
+    K, V, Q, QV, KN, VN = [], [], [], [], [], []
     for l in range(n_layers):
         K.append(inputs.kv(w, "k", layer=l, device=dev))
         V.append(inputs.kv(w, "v", layer=l, device=dev))
@@ -264,15 +266,17 @@ def main():
         kn, vn = inputs.drafts_kv(w, layer=l, device=dev)
         KN.append(kn)
         VN.append(vn)
-        pools.append(lynx.KVPool.allocate(L, 1, device=dev))
+    # every layer's planes are slices of one allocation per plane kind: the
+    # residual stream of the whole cache moves and merges in one call each
+    pools, whole = lynx.KVPool.allocate_layers(L, 1, n_layers, device=dev)
     # decode-side residual buffers, filled only by the H2D transport
-    recv_k = [torch.empty_like(p.k_res) for p in pools]
-    recv_v = [torch.empty_like(p.v_res) for p in pools]
+    recv_k = torch.empty_like(whole.k_res)
+    recv_v = torch.empty_like(whole.v_res)
     # the residual stream as it leaves the prefill side: pinned host staging
     for l in range(n_layers):
         pools[l].encode(0, T, table, K[l], V[l])
-    host_k = [p.k_res.cpu().pin_memory() for p in pools]
-    host_v = [p.v_res.cpu().pin_memory() for p in pools]
+    host_k = whole.k_res.cpu().pin_memory()
+    host_v = whole.v_res.cpu().pin_memory()
     out = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device=dev)
     outv = torch.empty(1, nq, Hq, 128, dtype=torch.bfloat16, device=dev)
     ws = lynx.workspace(L, 1, Hq, nq, T)
@@ -302,9 +306,8 @@ def main():
         side.wait_event(e["enc"])
         with torch.cuda.stream(side):
             e["h2d0"].record(side)
-            for l in range(n_layers):
-                recv_k[l].copy_(host_k[l], non_blocking=True)
-                recv_v[l].copy_(host_v[l], non_blocking=True)
+            recv_k.copy_(host_k, non_blocking=True)
+            recv_v.copy_(host_v, non_blocking=True)
             e["h2d"].record(side)
         e["dec0"].record(main_s)
         for l in range(n_layers):
@@ -314,10 +317,8 @@ def main():
         e["dec"].record(main_s)
         main_s.wait_event(e["h2d"])
         e["merge0"].record(main_s)
-        for l in range(n_layers):
-            p = pools[l]
-            lynx.lynx_kv_merge(p.k_anc, recv_k[l], p.k_codes)
-            lynx.lynx_kv_merge(p.v_anc, recv_v[l], p.v_codes)
+        lynx.lynx_kv_merge(whole.k_anc, recv_k, whole.k_codes)
+        lynx.lynx_kv_merge(whole.v_anc, recv_v, whole.v_codes)
         e["merge"].record(main_s)
         for l in range(n_layers):
             p = pools[l]
@@ -354,7 +355,7 @@ def main():
     dec_gbps = dec_bytes / (t_dec * 1e-3) / 1e9
     ver_bytes = n_layers * T * Hkv * VERIFY_BYTES_PER_TOKEN_HEAD
     ver_gbps = ver_bytes / (t_ver * 1e-3) / 1e9
-    h2d_gbps = (sum(h.numel() for h in host_k) * 2) / (t_h2d * 1e-3) / 1e9
+    h2d_gbps = (host_k.numel() + host_v.numel()) / (t_h2d * 1e-3) / 1e9
     ver_us = t_ver * 1e3 / n_layers
     overlap = max(0.0, min(1.0, (t_dec + t_h2d - (ms("dec0", "merge0"))) / min(t_dec, t_h2d)))
 

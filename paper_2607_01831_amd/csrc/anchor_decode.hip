@@ -14,10 +14,12 @@
 // Exactness of the operands:
 //  * a nibble n becomes the bf16 value 128 + n (bit pattern 0x4300 | n), one
 //    v_perm per two values; the 128 offset is removed after the product.
-//  * the K scale is folded into the query: q'_d = 16 q_d s_d per 128-token
-//    group, carried as bf16 hi + bf16 lo (two MFMAs, ~16 significant bits);
-//    zero and the 7.5 bucket centre enter a per-group bias
-//    sum_d q_d (z_d + 7.5 s_d) - 128 sum_d q'_d.
+//  * the K scale is folded into the query: q'_d = 16 c q_d s_d per 128-token
+//    group (c = log2(e) / sqrt(128), so the products come out as softmax
+//    exponents in log2 units), carried as bf16 hi + bf16 lo (two MFMAs, ~16
+//    significant bits); zero, the 7.5 bucket centre and the 128 offset enter
+//    a per-group bias c sum_d q_d (z_d - 2040.5 s_d), the accumulator's
+//    initial value.
 //  * the V scale is folded into the softmax weight: p'_t = p_t s_t (bf16);
 //    the zero/centre term sum_t p_t (z_t + 7.5 s_t) is a per-head scalar and
 //    the 128 offset is measured by one extra MFMA against a constant operand.
@@ -262,8 +264,8 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         u32x4_t hi, lo;
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
-            const float q0 = live ? 16.0f * qv[e] * sv[e] : 0.0f;
-            const float q1 = live ? 16.0f * qv[e + 1] * sv[e + 1] : 0.0f;
+            const float q0 = live ? (16.0f * kscore) * qv[e] * sv[e] : 0.0f;
+            const float q1 = live ? (16.0f * kscore) * qv[e + 1] * sv[e + 1] : 0.0f;
             const uint32_t hp = pack2(q0, q1);
             hi[e / 2] = hp;
             lo[e / 2] = pack2(q0 - bf16_val(hp & 0xffffu), q1 - __uint_as_float(hp & 0xffff0000u));
@@ -332,6 +334,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
 
     u32x4_t bq[8];
     float bk = 0.0f;
+    f32x4_t bk4 = {0.f, 0.f, 0.f, 0.f};
     // Folded query operands and bias of the group of tile j.
     auto load_group_operands = [&](int j) {
         const int gl = w + 4 * (j >> 2);
@@ -341,6 +344,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         bk = col < heads ? (s_bias[0][gl][col] + s_bias[1][gl][col]) +
                                (s_bias[2][gl][col] + s_bias[3][gl][col])
                          : 0.0f;
+        bk4 = f32x4_t{bk, bk, bk, bk};
     };
     // Scores of tile j (log2 units): lane (col, kg) gets token
     // t0 + 16 r + 4 kg + i in x[4 r + i]; tokens past the context get -inf.
@@ -350,7 +354,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         *reinterpret_cast<uint4 *>(vlds + v_wr_addr + 16 * kNibbleRow) = cur.v[1];
         f32x4_t sc[2];
 #pragma unroll
-        for (int r = 0; r < 2; ++r) sc[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int r = 0; r < 2; ++r) sc[r] = bk4;  // the bias enters as the initial accumulator
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
 #pragma unroll
@@ -363,7 +367,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
             }
         }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) x[i] = fmaf(sc[i >> 2][i & 3], kscore, bk);
+        for (int i = 0; i < 8; ++i) x[i] = sc[i >> 2][i & 3];
         const int t0 = tile_t0(j);
         if (t0 + kTile > T) {
             asm volatile("" ::: "memory");  // keep the masking out of full tiles

@@ -224,6 +224,31 @@ class KVPool:
             pool.v_codes = torch.zeros(2 * n, **u8)
         return pool
 
+    @staticmethod
+    def allocate_layers(L: Layout, B: int, layers: int, device="cuda", codes: bool = True):
+        """Pools for `layers` layers whose planes are consecutive slices of one
+        allocation per plane kind, so that a whole cache's residual planes can
+        be transported and merged in one call each.  Returns (pools, whole),
+        whole being a KVPool-like record of the full-length planes (its meta
+        is that of layer 0 and is not used)."""
+        n = L.plane_bytes(64)
+        u8 = dict(dtype=torch.uint8, device=device)
+        big = {name: torch.zeros(layers * n, **u8) for name in ("k_anc", "v_anc", "k_res", "v_res")}
+        if codes:
+            big["k_codes"] = torch.zeros(layers * 2 * n, **u8)
+            big["v_codes"] = torch.zeros(layers * 2 * n, **u8)
+        pools = []
+        for l in range(layers):
+            pool = KVPool(L, B, *(big[name][l * n:(l + 1) * n] for name in ("k_anc", "v_anc", "k_res", "v_res")),
+                          Meta.empty(L, B, device))
+            if codes:
+                pool.k_codes = big["k_codes"][l * 2 * n:(l + 1) * 2 * n]
+                pool.v_codes = big["v_codes"][l * 2 * n:(l + 1) * 2 * n]
+            pools.append(pool)
+        whole = KVPool(L, B, big["k_anc"], big["v_anc"], big["k_res"], big["v_res"], pools[0].meta,
+                       big.get("k_codes"), big.get("v_codes"))
+        return pools, whole
+
     def encode(self, b: int, T: int, block_table, k, v, stream=None) -> None:
         lynx_kv_encode(self.layout, b, T, block_table, k, v, self.k_anc, self.v_anc, self.k_res,
                        self.v_res, self.meta, stream)
