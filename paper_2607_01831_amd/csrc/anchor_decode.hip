@@ -57,7 +57,12 @@ __device__ __forceinline__ uint32_t bf16_bits(float x) {
     return (uint32_t)__builtin_bit_cast(unsigned short, (__bf16)x);
 }
 __device__ __forceinline__ float bf16_val(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
-__device__ __forceinline__ uint32_t pack2(float a, float b) { return bf16_bits(a) | (bf16_bits(b) << 16); }
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// Two floats -> two bf16 (round to nearest even) in one word, a in the low half.
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
 
 // Eight nibbles of one 32-bit word (nibble j = element j) -> eight bf16
 // values 128 + n in MFMA k-order (j = 0, 2, 4, 6, 1, 3, 5, 7).
