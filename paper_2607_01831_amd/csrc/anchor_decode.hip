@@ -109,14 +109,18 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     // groups of this split that hold tokens (uniform across the workgroup)
     const int n_groups = max(0, min(NG, (T - g0 * kKGroup + kKGroup - 1) / kKGroup));
 
-    // Folded query operands of every group of the split, one 16-byte MFMA
-    // operand piece per (group, kk, hi/lo, row group kg, head); a trailing
-    // zero piece feeds the columns past the chunk's heads.
-    constexpr int kBPieces = NG * 8 * 4 * GP;
-    __shared__ u32x4_t s_b[kBPieces + 1];
-    __shared__ float s_bias[kWaves][NG][GP];  // per-wavefront partial biases
-    __shared__ __attribute__((aligned(16))) float s_vs[NG * kKGroup];
-    __shared__ __attribute__((aligned(16))) float s_vz[NG * kKGroup];
+    // The split is walked in rounds of 4 groups, one group per wavefront.
+    // Folded query operands of a round: one 16-byte MFMA operand piece per
+    // (group, kk, hi/lo, row group kg, head), double-buffered across rounds;
+    // a trailing zero piece feeds the columns past the chunk's heads.
+    constexpr int kRounds = NG / 4;
+    constexpr int kBufs = kRounds > 1 ? 2 : 1;
+    constexpr int kRoundPieces = 4 * 8 * 4 * GP;
+    constexpr int kZeroPiece = kBufs * kRoundPieces;
+    __shared__ u32x4_t s_b[kZeroPiece + 1];
+    __shared__ float s_bias[kBufs][kWaves][4][GP];  // per-wavefront partial biases
+    __shared__ __attribute__((aligned(16))) float s_vs[kBufs][4 * kKGroup];
+    __shared__ __attribute__((aligned(16))) float s_vz[kBufs][4 * kKGroup];
     __shared__ __attribute__((aligned(16))) uint8_t s_v[kWaves][kTile * kNibbleRow];
     __shared__ __attribute__((aligned(16))) float s_o[kWaves][GP][kHeadDim];
     __shared__ float s_m[kWaves][GP], s_l[kWaves][GP], s_ob[kWaves][GP];
@@ -149,53 +153,57 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         return ((size_t)blk * Hkv + h) * a.geo.bt + (size_t)(t - bi * a.geo.bt);
     };
 
-    // ---- prologue loads, all issued before the first tile loads so that the
-    // waits for them leave the tiles in flight ----
-    // V metadata of the split's tokens (zero past the context)
-    constexpr int kVmPer = NG * kKGroup / kThreads;
+    // ---- per-round metadata, loaded one round ahead into registers ----
+    const int n_rounds = (n_groups + 3) / 4;
+    // V metadata of a round's tokens (zero past the context)
+    constexpr int kVmPer = 4 * kKGroup / kThreads;
     float vs_r[kVmPer], vz_r[kVmPer];
-#pragma unroll
-    for (int k = 0; k < kVmPer; ++k) {
-        const int t = g0 * kKGroup + tid + k * kThreads;
-        const size_t ti = vmeta + (size_t)min(t, max(T - 1, 0));
-        vs_r[k] = a.meta.v_scale[ti];
-        vz_r[k] = a.meta.v_zero[ti];
-        if (t >= T) vs_r[k] = vz_r[k] = 0.0f;
-    }
     // K scales and query pieces of the fold: piece (gl, kk, dg, hh) covers
-    // dims 32 dg + 8 kk .. + 7 of head hh and group gl.  Indices are clamped
-    // into range; pieces past the heads or groups are zeroed below.
-    constexpr int kFoldPieces = NG * 4 * 4 * GP;
+    // dims 32 dg + 8 kk .. + 7 of head hh and group gl of the round.  Indices
+    // are clamped into range; pieces past the heads or groups are zeroed.
+    constexpr int kFoldPieces = 4 * 4 * 4 * GP;
     constexpr int kFoldPer = kFoldPieces / kThreads;
     static_assert(kFoldPieces % kThreads == 0, "fold pieces must tile the workgroup");
     float4 fs0[kFoldPer], fs1[kFoldPer];
-    uint4 fq[kFoldPer];
+    uint4 fq[kFoldPer];  // the query pieces are the same in every round
 #pragma unroll
     for (int k = 0; k < kFoldPer; ++k) {
         const int pidx = tid + k * kThreads;
         const int hh = min(pidx % GP, heads - 1);
-        const int dg = (pidx / GP) % 4;
-        const int kk = (pidx / (4 * GP)) % 4;
-        const int gl = min(pidx / (16 * GP), n_groups - 1);
-        const int d0 = 32 * dg + 8 * kk;
-        const float *sp = a.meta.k_scale + kmeta + (size_t)(g0 + gl) * kHeadDim + d0;
-        fs0[k] = *reinterpret_cast<const float4 *>(sp);
-        fs1[k] = *reinterpret_cast<const float4 *>(sp + 4);
+        const int d0 = 32 * ((pidx / GP) % 4) + 8 * ((pidx / (4 * GP)) % 4);
         fq[k] = *reinterpret_cast<const uint4 *>(a.q + (q_row0 + hh) * kHeadDim + d0);
     }
-    // bias operands: query of head col, K scale/zero of group col, dims 32 w + 8 kg ..
-    uint4 bqw;
+    // bias operands: query of head col, K scale/zero of group col of the round,
+    // dims 32 w + 8 kg ..
+    const uint4 bqw = *reinterpret_cast<const uint4 *>(
+        a.q + (q_row0 + min(col, heads - 1)) * kHeadDim + 32 * w + 8 * kg);
     float4 bs0, bs1, bz0, bz1;
-    {
-        const int hc = min(col, heads - 1);
-        const int gc = min(col, n_groups - 1);
-        bqw = *reinterpret_cast<const uint4 *>(a.q + (q_row0 + hc) * kHeadDim + 32 * w + 8 * kg);
+    auto load_round_meta = [&](int r) {
+#pragma unroll
+        for (int k = 0; k < kVmPer; ++k) {
+            const int t = (g0 + 4 * r) * kKGroup + tid + k * kThreads;
+            const size_t ti = vmeta + (size_t)min(t, T - 1);
+            vs_r[k] = a.meta.v_scale[ti];
+            vz_r[k] = a.meta.v_zero[ti];
+            if (t >= T) vs_r[k] = vz_r[k] = 0.0f;
+        }
+#pragma unroll
+        for (int k = 0; k < kFoldPer; ++k) {
+            const int pidx = tid + k * kThreads;
+            const int gl = min(4 * r + pidx / (16 * GP), n_groups - 1);
+            const int d0 = 32 * ((pidx / GP) % 4) + 8 * ((pidx / (4 * GP)) % 4);
+            const float *sp = a.meta.k_scale + kmeta + (size_t)(g0 + gl) * kHeadDim + d0;
+            fs0[k] = *reinterpret_cast<const float4 *>(sp);
+            fs1[k] = *reinterpret_cast<const float4 *>(sp + 4);
+        }
+        const int gc = min(4 * r + min(col, 3), n_groups - 1);
         const size_t mo = kmeta + (size_t)(g0 + gc) * kHeadDim + 32 * w + 8 * kg;
         bs0 = *reinterpret_cast<const float4 *>(a.meta.k_scale + mo);
         bs1 = *reinterpret_cast<const float4 *>(a.meta.k_scale + mo + 4);
         bz0 = *reinterpret_cast<const float4 *>(a.meta.k_zero + mo);
         bz1 = *reinterpret_cast<const float4 *>(a.meta.k_zero + mo + 4);
-    }
+    };
+    load_round_meta(0);
 
     // ---- this wavefront's tiles: groups w, w+4, ..; 4 tiles of 32 tokens each ----
     constexpr int kTilesPerWave = NG;  // (NG / 4) groups x 4 tiles
@@ -245,78 +253,83 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     for (int j = 0; j < kPrefetch; ++j)
         if (j < kTilesPerWave) load_tile(j, tiles[j]);
 
-    // ---- prologue (whole workgroup): fold every group's K scale into the
-    // query, per-wavefront bias partials, V metadata into LDS ----
-    // (a) Folded operands, one 16-byte piece (8 dims) at a time: piece
-    // (gl, kk, dg, hh) holds q'_d = 16 q_d s_d of dims 32 dg + 8 kk + pi(e),
-    // as bf16 hi in s_b and bf16 lo 4 GP pieces further.
+    // ---- fold of one round (whole workgroup): the groups' K scales into
+    // the query, per-wavefront bias partials, V metadata into LDS ----
+    auto fold_round = [&](int buf, int r) {
+        // (a) Folded operands, one 16-byte piece (8 dims) at a time: piece
+        // (gl, kk, dg, hh) holds q'_d = 16 c q_d s_d of dims 32 dg + 8 kk +
+        // pi(e), as bf16 hi in s_b and bf16 lo 4 GP pieces further.
 #pragma unroll
-    for (int k = 0; k < kFoldPer; ++k) {
-        const int pidx = tid + k * kThreads;
-        const int hh = pidx % GP;
-        const int dg = (pidx / GP) % 4;
-        const int kk = (pidx / (4 * GP)) % 4;
-        const int gl = pidx / (16 * GP);
-        const bool live = hh < heads && gl < n_groups;
-        const uint4 qw = fq[k];
-        // dims d0 + (0, 2, 4, 6, 1, 3, 5, 7)
-        const float qv[8] = {bf16_val(qw.x & 0xffffu), bf16_val(qw.y & 0xffffu),
-                             bf16_val(qw.z & 0xffffu), bf16_val(qw.w & 0xffffu),
-                             __uint_as_float(qw.x & 0xffff0000u), __uint_as_float(qw.y & 0xffff0000u),
-                             __uint_as_float(qw.z & 0xffff0000u), __uint_as_float(qw.w & 0xffff0000u)};
-        const float4 s0 = fs0[k], s1 = fs1[k];
-        const float sv[8] = {s0.x, s0.z, s1.x, s1.z, s0.y, s0.w, s1.y, s1.w};
-        u32x4_t hi, lo;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-            const float q0 = live ? (16.0f * kscore) * qv[e] * sv[e] : 0.0f;
-            const float q1 = live ? (16.0f * kscore) * qv[e + 1] * sv[e + 1] : 0.0f;
-            const uint32_t hp = pack2(q0, q1);
-            hi[e / 2] = hp;
-            lo[e / 2] = pack2(q0 - bf16_val(hp & 0xffffu), q1 - __uint_as_float(hp & 0xffff0000u));
-        }
-        const int piece = ((gl * 8 + kk * 2) * 4 + dg) * GP + hh;
-        s_b[piece] = hi;
-        s_b[piece + 4 * GP] = lo;
-    }
-    if (tid == 0) s_b[kBPieces] = u32x4_t{0u, 0u, 0u, 0u};
-    // (b) Biases bias[gl][hh] = sum_d q_d (z_d - 2040.5 s_d) as a small matrix
-    // product on the matrix cores: rows = heads, columns = groups, wavefront w
-    // contracting dims 32 w..32 w+31 (zc carried as bf16 hi + lo); the four
-    // wavefront partials are summed when a group's operands are loaded.
-    {
-        u32x4_t qa = {0u, 0u, 0u, 0u};
-        if (col < heads) qa = u32x4_t{bqw.x, bqw.y, bqw.z, bqw.w};
-        u32x4_t zh = {0u, 0u, 0u, 0u}, zl = {0u, 0u, 0u, 0u};
-        if (col < n_groups) {
-            const float zc[8] = {bz0.x - 2040.5f * bs0.x, bz0.y - 2040.5f * bs0.y,
-                                 bz0.z - 2040.5f * bs0.z, bz0.w - 2040.5f * bs0.w,
-                                 bz1.x - 2040.5f * bs1.x, bz1.y - 2040.5f * bs1.y,
-                                 bz1.z - 2040.5f * bs1.z, bz1.w - 2040.5f * bs1.w};
+        for (int k = 0; k < kFoldPer; ++k) {
+            const int pidx = tid + k * kThreads;
+            const int hh = pidx % GP;
+            const int dg = (pidx / GP) % 4;
+            const int kk = (pidx / (4 * GP)) % 4;
+            const int gl = pidx / (16 * GP);
+            const bool live = hh < heads && 4 * r + gl < n_groups;
+            const uint4 qw = fq[k];
+            // dims d0 + (0, 2, 4, 6, 1, 3, 5, 7)
+            const float qv[8] = {bf16_val(qw.x & 0xffffu), bf16_val(qw.y & 0xffffu),
+                                 bf16_val(qw.z & 0xffffu), bf16_val(qw.w & 0xffffu),
+                                 __uint_as_float(qw.x & 0xffff0000u), __uint_as_float(qw.y & 0xffff0000u),
+                                 __uint_as_float(qw.z & 0xffff0000u), __uint_as_float(qw.w & 0xffff0000u)};
+            const float4 s0 = fs0[k], s1 = fs1[k];
+            const float sv[8] = {s0.x, s0.z, s1.x, s1.z, s0.y, s0.w, s1.y, s1.w};
+            u32x4_t hi, lo;
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const uint32_t hp = pack2(zc[e], zc[e + 1]);
-                zh[e / 2] = hp;
-                zl[e / 2] = pack2(zc[e] - bf16_val(hp & 0xffffu), zc[e + 1] - __uint_as_float(hp & 0xffff0000u));
+                const float q0 = live ? (16.0f * kscore) * qv[e] * sv[e] : 0.0f;
+                const float q1 = live ? (16.0f * kscore) * qv[e + 1] * sv[e + 1] : 0.0f;
+                const uint32_t hp = pack2(q0, q1);
+                hi[e / 2] = hp;
+                lo[e / 2] = pack2(q0 - bf16_val(hp & 0xffffu), q1 - __uint_as_float(hp & 0xffff0000u));
+            }
+            const int piece = buf * kRoundPieces + ((gl * 8 + kk * 2) * 4 + dg) * GP + hh;
+            s_b[piece] = hi;
+            s_b[piece + 4 * GP] = lo;
+        }
+        // (b) Biases bias[gl][hh] = c sum_d q_d (z_d - 2040.5 s_d) as a small
+        // matrix product on the matrix cores: rows = heads, columns = the
+        // round's groups, wavefront w contracting dims 32 w..32 w+31 (zc
+        // carried as bf16 hi + lo); the four wavefront partials are summed
+        // when a group's operands are loaded.
+        {
+            u32x4_t qa = {0u, 0u, 0u, 0u};
+            if (col < heads) qa = u32x4_t{bqw.x, bqw.y, bqw.z, bqw.w};
+            u32x4_t zh = {0u, 0u, 0u, 0u}, zl = {0u, 0u, 0u, 0u};
+            if (col < 4 && 4 * r + col < n_groups) {
+                const float zc[8] = {bz0.x - 2040.5f * bs0.x, bz0.y - 2040.5f * bs0.y,
+                                     bz0.z - 2040.5f * bs0.z, bz0.w - 2040.5f * bs0.w,
+                                     bz1.x - 2040.5f * bs1.x, bz1.y - 2040.5f * bs1.y,
+                                     bz1.z - 2040.5f * bs1.z, bz1.w - 2040.5f * bs1.w};
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    const uint32_t hp = pack2(zc[e], zc[e + 1]);
+                    zh[e / 2] = hp;
+                    zl[e / 2] = pack2(zc[e] - bf16_val(hp & 0xffffu), zc[e + 1] - __uint_as_float(hp & 0xffff0000u));
+                }
+            }
+            f32x4_t cb = {0.f, 0.f, 0.f, 0.f};
+            cb = mfma(qa, zh, cb);
+            cb = mfma(qa, zl, cb);
+            // lane (group col, row group kg) holds heads 4 kg + i
+            if (col < 4) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (4 * kg + i < GP) s_bias[buf][w][col][4 * kg + i] = cb[i] * kscore;
             }
         }
-        f32x4_t cb = {0.f, 0.f, 0.f, 0.f};
-        cb = mfma(qa, zh, cb);
-        cb = mfma(qa, zl, cb);
-        // lane (group col, row group kg) holds heads 4 kg + i
-        if (col < NG) {
+        // (c) V metadata
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (4 * kg + i < GP) s_bias[w][col][4 * kg + i] = cb[i] * kscore;
+        for (int k = 0; k < kVmPer; ++k) {
+            s_vs[buf][tid + k * kThreads] = vs_r[k];
+            s_vz[buf][tid + k * kThreads] = vz_r[k];
         }
-    }
-    // (c) V metadata
-#pragma unroll
-    for (int k = 0; k < kVmPer; ++k) {
-        s_vs[tid + k * kThreads] = vs_r[k];
-        s_vz[tid + k * kThreads] = vz_r[k];
-    }
-    __syncthreads();  // folded operands, biases and V metadata are ready
+    };
+    fold_round(0, 0);
+    if (tid == 0) s_b[kZeroPiece] = u32x4_t{0u, 0u, 0u, 0u};
+    if (n_rounds > 1) load_round_meta(1);
+    __syncthreads();  // the first round's operands, biases and V metadata are ready
 
     // ---- per-wave online-softmax state (lane: column col, token group kg) ----
     float m_run = -INFINITY, l_part = 0.0f, ob_part = 0.0f;
@@ -340,14 +353,14 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     u32x4_t bq[8];
     float bk = 0.0f;
     f32x4_t bk4 = {0.f, 0.f, 0.f, 0.f};
-    // Folded query operands and bias of the group of tile j.
-    auto load_group_operands = [&](int j) {
-        const int gl = w + 4 * (j >> 2);
+    // Folded query operands and bias of this wavefront's group of a round.
+    auto load_group_operands = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-            bq[i] = b_piece >= 0 ? s_b[(gl * 8 + i) * 4 * GP + b_piece] : s_b[kBPieces];
-        bk = col < heads ? (s_bias[0][gl][col] + s_bias[1][gl][col]) +
-                               (s_bias[2][gl][col] + s_bias[3][gl][col])
+            bq[i] = b_piece >= 0 ? s_b[buf * kRoundPieces + (w * 8 + i) * 4 * GP + b_piece]
+                                 : s_b[kZeroPiece];
+        bk = col < heads ? (s_bias[buf][0][w][col] + s_bias[buf][1][w][col]) +
+                               (s_bias[buf][2][w][col] + s_bias[buf][3][w][col])
                          : 0.0f;
         bk4 = f32x4_t{bk, bk, bk, bk};
     };
@@ -387,13 +400,12 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         return max_kg(fmax3(fmax3(x[0], x[1], x[2]), fmax3(x[3], x[4], x[5]), fmax2(x[6], x[7])));
     };
     // Softmax weights against reference m_ref, then P V for tile j.
-    auto tile_accumulate = [&](int j, const float (&x)[8]) {
-        const int gl = w + 4 * (j >> 2);
-        const int tl = gl * kKGroup + kTile * (j & 3) + 4 * kg;
-        const float4 vs0 = *reinterpret_cast<const float4 *>(&s_vs[tl]);
-        const float4 vs1 = *reinterpret_cast<const float4 *>(&s_vs[tl + 16]);
-        const float4 vz0 = *reinterpret_cast<const float4 *>(&s_vz[tl]);
-        const float4 vz1 = *reinterpret_cast<const float4 *>(&s_vz[tl + 16]);
+    auto tile_accumulate = [&](int buf, int j, const float (&x)[8]) {
+        const int tl = w * kKGroup + kTile * (j & 3) + 4 * kg;
+        const float4 vs0 = *reinterpret_cast<const float4 *>(&s_vs[buf][tl]);
+        const float4 vs1 = *reinterpret_cast<const float4 *>(&s_vs[buf][tl + 16]);
+        const float4 vz0 = *reinterpret_cast<const float4 *>(&s_vz[buf][tl]);
+        const float4 vz1 = *reinterpret_cast<const float4 *>(&s_vz[buf][tl + 16]);
         const float vsv[8] = {vs0.x, vs0.y, vs0.z, vs0.w, vs1.x, vs1.y, vs1.z, vs1.w};
         const float vzv[8] = {vz0.x, vz0.y, vz0.z, vz0.w, vz1.x, vz1.y, vz1.z, vz1.w};
         float pw[8];
@@ -424,17 +436,32 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     // Fast path: the softmax reference of each head is the maximum of the
     // wavefront's first tile and stays fixed, so the loop carries no rescale.
     // Weights of later, larger scores exceed 1; if any sum leaves the safe
-    // range the wavefront redoes its tiles below with a running maximum.
+    // range the workgroup redoes the split below with a running maximum.
+    // Each round ends with a barrier, after the next round's fold.
 #pragma unroll
-    for (int j = 0; j < kTilesPerWave; ++j) {
-        if (!tile_valid(j)) break;  // wavefront-uniform; later tiles are past the context too
-        if (j + kPrefetch < kTilesPerWave)
-            load_tile(j + kPrefetch, tiles[(j + kPrefetch) % (kPrefetch + 1)]);
-        if ((j & 3) == 0) load_group_operands(j);
-        float x[8];
-        tile_scores(tiles[j % (kPrefetch + 1)], j, x);
-        if (j == 0) m_run = tile_max(x);
-        tile_accumulate(j, x);
+    for (int r = 0; r < kRounds; ++r) {
+        if (r >= n_rounds) break;  // uniform across the workgroup
+        const int buf = kBufs > 1 ? (r & 1) : 0;
+        load_group_operands(buf);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int j = 4 * r + jj;
+            if (j + kPrefetch < kTilesPerWave)
+                load_tile(j + kPrefetch, tiles[(j + kPrefetch) % (kPrefetch + 1)]);
+            if (tile_valid(j)) {  // wavefront-uniform
+                float x[8];
+                tile_scores(tiles[j % (kPrefetch + 1)], j, x);
+                if (j == 0) m_run = tile_max(x);
+                tile_accumulate(buf, j, x);
+            }
+        }
+        if (kRounds > 1) {
+            if (r + 1 < n_rounds) {
+                fold_round(buf ^ 1, r + 1);
+                if (r + 2 < n_rounds) load_round_meta(r + 2);
+            }
+            __syncthreads();  // next round's operands in place; this round's buffer is free
+        }
     }
     bool unsafe = !(l_part < 1e30f) || !(fabsf(ob_part) < 1e30f);
 #pragma unroll
@@ -443,39 +470,46 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         for (int i = 0; i < 4; ++i) unsafe |= !(fabsf(acc[n][i]) < 1e30f);
 #pragma unroll
     for (int i = 0; i < 4; ++i) unsafe |= !(fabsf(acc_off[i]) < 1e30f);
-    if (__any(unsafe)) {
+    if (__syncthreads_or(unsafe)) {
         // Slow path (scores far above the first tile's): running maximum
-        // with rescaling, one tile at a time.
+        // with rescaling, one round and tile at a time.
         m_run = -INFINITY;
         l_part = ob_part = 0.0f;
 #pragma unroll
         for (int n = 0; n < 8; ++n) acc[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         acc_off = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int j = 0; j < kTilesPerWave; ++j) {
-            if (!tile_valid(j)) break;
-            Tile cur;
-            load_tile(j, cur);
-            if ((j & 3) == 0) load_group_operands(j);
-            float x[8];
-            tile_scores(cur, j, x);
-            const float mx = tile_max(x);
-            if (__any(mx > m_run)) {
-                const float m_new = fmaxf(mx, m_run);
-                const float alpha = (m_run == -INFINITY) ? 0.0f : exp2f(m_run - m_new);
-                m_run = m_new;
-                l_part *= alpha;
-                ob_part *= alpha;
-                float af[4];
+        for (int r = 0; r < n_rounds; ++r) {
+            load_round_meta(r);
+            fold_round(0, r);
+            __syncthreads();
+            load_group_operands(0);
+            for (int jj = 0; jj < 4; ++jj) {
+                const int j = 4 * r + jj;
+                if (!tile_valid(j)) continue;
+                Tile cur;
+                load_tile(j, cur);
+                float x[8];
+                tile_scores(cur, j, x);
+                const float mx = tile_max(x);
+                if (__any(mx > m_run)) {
+                    const float m_new = fmaxf(mx, m_run);
+                    const float alpha = (m_run == -INFINITY) ? 0.0f : exp2f(m_run - m_new);
+                    m_run = m_new;
+                    l_part *= alpha;
+                    ob_part *= alpha;
+                    float af[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) af[i] = __shfl(alpha, 4 * kg + i);
+                    for (int i = 0; i < 4; ++i) af[i] = __shfl(alpha, 4 * kg + i);
 #pragma unroll
-                for (int n = 0; n < 8; ++n)
+                    for (int n = 0; n < 8; ++n)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[n][i] *= af[i];
+                        for (int i = 0; i < 4; ++i) acc[n][i] *= af[i];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc_off[i] *= af[i];
+                    for (int i = 0; i < 4; ++i) acc_off[i] *= af[i];
+                }
+                tile_accumulate(0, j, x);
             }
-            tile_accumulate(j, x);
+            __syncthreads();
         }
     }
 
@@ -580,6 +614,8 @@ hipError_t launch_anchor_decode_mfma(const DecodeArgs &args, int chunks, hipStre
         launch_groups<4>(args, grid, stream);
     } else if (args.groups_per_split == 8) {
         launch_groups<8>(args, grid, stream);
+    } else if (args.groups_per_split == 16) {
+        launch_groups<16>(args, grid, stream);
     } else {
         return hipErrorInvalidValue;
     }

@@ -540,10 +540,12 @@ AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_le
     p.rows_chunk = 1;
     while (p.rows_chunk < 8 && p.rows_chunk < p.rows_total) p.rows_chunk *= 2;
     p.n_chunks = (p.rows_total + p.rows_chunk - 1) / p.rows_chunk;
-    // Context tokens per split: 512, doubled (up to 1024) while the launch
-    // still has >= 1024 workgroups, so long contexts write fewer partials.
+    // Context tokens per split: 512, doubled while the launch still has >=
+    // 1024 workgroups, so long contexts write fewer partials and workgroups
+    // live longer: up to 2048 for decode (512 when 16-head chunks leave no
+    // LDS for more groups), up to 1024 for verification.
     p.split_tokens = kWaves * kKGroup;
-    const int max_split = (nq == 1 && G > 8) ? 512 : 1024;  // decode with 16-head chunks: 4 groups
+    const int max_split = nq == 1 ? (G > 8 ? 512 : 2048) : 1024;
     while (p.split_tokens < max_split) {
         const long long next = ((long long)max_seq_len + 2 * p.split_tokens - 1) / (2 * p.split_tokens);
         if (next * g.Hkv * B < 1024) break;
