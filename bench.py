@@ -111,8 +111,8 @@ def _csv(dirname, suffix):
 
 
 def _short(name: str) -> str:
-    for key in ("anchor_decode_kernel", "attn_combine_kernel", "attn_split_kernel", "encode_kernel",
-                "merge_kernel", "copyBuffer"):
+    for key in ("anchor_decode_kernel", "attn_combine_kernel", "attn_split_kernel", "verify_kernel",
+                "encode_kernel", "merge_kernel", "copyBuffer"):
         if key in name:
             if key == "attn_split_kernel":
                 return "attn_split_kernel<codes>" if "(lynx::KvMode)1" in name else "attn_split_kernel<anchor>"
@@ -338,6 +338,19 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    # The same decode calls once more with no residual transport running
+    # (reported beside the step's figure, which overlaps the transport).
+    e0, e1 = ev(), ev()
+    e0.record(main_s)
+    for _ in range(args.steps):
+        for l in range(n_layers):
+            p = pools[l]
+            lynx.lynx_attn_anchor_decode(L, 1, Hq, T, lens, table, p.k_anc, p.v_anc, p.meta,
+                                         Q[l], out, None, ws)
+    e1.record(main_s)
+    torch.cuda.synchronize()
+    t_dec_alone = e0.elapsed_time(e1) / args.steps
+
     def ms(a, b):
         return sum(r[a].elapsed_time(r[b]) for r in recs) / len(recs)
 
@@ -384,6 +397,8 @@ def main():
             "encode_us_per_layer": round(t_enc * 1e3 / n_layers, 2),
             "anchor_decode_GBps": round(dec_gbps, 2),
             "anchor_decode_us_per_layer": round(t_dec * 1e3 / n_layers, 3),
+            "anchor_decode_GBps_without_transport": round(dec_bytes / (t_dec_alone * 1e-3) / 1e9, 2),
+            "anchor_decode_us_per_layer_without_transport": round(t_dec_alone * 1e3 / n_layers, 3),
             "merge_GBps": round(merge_gbps, 2), "merge_frac": round(merge_gbps / HBM_PEAK_GBPS, 4),
             "merge_us_per_layer": round(t_merge * 1e3 / n_layers, 2),
             "verify_us_per_layer": round(ver_us, 2),
