@@ -254,3 +254,62 @@ def test_anchor_decode_ragged_batch_stale_workspace():
     ref, ref_lse = oracle_decode(c, q)
     assert_close(out.float().cpu().numpy(), ref, what="ragged batch, stale workspace")
     np.testing.assert_allclose(lse.cpu().numpy(), ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
+
+
+def _dominant(k, q, t, h, G, boost):
+    """Make token t of kv head h score boost x |q| for the first query head of
+    h's group; q is one sequence's [Hq][128] queries."""
+    qh = q[h * G].float()
+    k[t, h] = (boost * qh / qh.norm()).to(k.dtype)
+
+
+def _decode_check_sampled(c, q, mask, what):
+    out, lse = gpu_anchor_decode(c, q)
+    ref, ref_lse = oracle_decode(c, q, unit_mask=mask)
+    G = q.shape[1] // c.Hkv
+    for b, h in zip(*np.nonzero(mask)):
+        assert_close(out[b, h * G:(h + 1) * G], ref[b, h * G:(h + 1) * G], what=f"{what} b={b} h={h}")
+        np.testing.assert_allclose(lse[b, h * G:(h + 1) * G], ref_lse[b, h * G:(h + 1) * G],
+                                   rtol=LSE_RTOL, atol=LSE_ATOL)
+
+
+@pytest.mark.slow
+def test_anchor_decode_two_round_splits_dominant_token():
+    """Splits of 8 groups (two rounds of the rolling fold): 2 x 32 kv heads x
+    ~20K tokens.  One unit holds a token whose score overflows the first
+    tile's reference (the workgroup redoes the split with a running maximum),
+    one a milder outlier."""
+    Hkv, G, lens = 32, 4, [20000, 19000]
+    q = random_bf16((2, Hkv * G, 128), seed=21)
+    ks, vs = [], []
+    for b, T in enumerate(lens):
+        k, v = random_kv(T, Hkv, seed=900 + b)
+        ks.append(k)
+        vs.append(v)
+    _dominant(ks[1], q[1], 15000, 5, G, 400.0)
+    _dominant(ks[0], q[0], 12000, 3, G, 30.0)
+    c = build_cache(ks, vs, Hkv, merge=False)
+    mask = np.zeros((2, Hkv), np.uint8)
+    mask[1, 5] = mask[0, 3] = mask[0, 17] = mask[1, 30] = 1
+    _decode_check_sampled(c, q, mask, "8-group splits")
+
+
+@pytest.mark.slow
+def test_anchor_decode_sixteen_group_splits_ragged():
+    """Splits of 16 groups (four rounds of the rolling fold) over a ragged
+    batch of 8 x 16 kv heads, including a one-token sequence and lengths that
+    end inside a round; one unit forces the running-maximum path."""
+    Hkv, G = 16, 2
+    lens = [15000, 3000, 14999, 2049, 8000, 15000, 1, 12345]
+    q = random_bf16((len(lens), Hkv * G, 128), seed=22)
+    ks, vs = [], []
+    for b, T in enumerate(lens):
+        k, v = random_kv(T, Hkv, seed=950 + b)
+        ks.append(k)
+        vs.append(v)
+    _dominant(ks[2], q[2], 14000, 7, G, 400.0)
+    c = build_cache(ks, vs, Hkv, merge=False)
+    mask = np.zeros((len(lens), Hkv), np.uint8)
+    for b, h in [(2, 7), (0, 0), (1, 15), (3, 4), (4, 9), (6, 2), (7, 11), (5, 8)]:
+        mask[b, h] = 1
+    _decode_check_sampled(c, q, mask, "16-group splits")
