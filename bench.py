@@ -68,6 +68,8 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="run one plain device copy of 640 MiB before the steps (counter calibration)")
     p.add_argument("--summarize-trace", metavar="DIR")
+    p.add_argument("--trace-split", type=int, default=0,
+                   help="with --summarize-trace: report the first N decode calls apart from the rest")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     return p.parse_args()
 
@@ -135,7 +137,7 @@ def _decode_calls(rows):
     return calls
 
 
-def summarize_trace(dirname):
+def summarize_trace(dirname, split=0):
     rows = _csv(dirname, "kernel_trace.csv")
     by = {}
     for r in rows:
@@ -145,13 +147,18 @@ def summarize_trace(dirname):
     for n, ds in sorted(by.items(), key=lambda kv: -sum(kv[1])):
         print(f"| {n} | {len(ds)} | {sum(ds) / len(ds):.2f} | {min(ds):.2f} | {max(ds):.2f} |")
     calls = _decode_calls(rows)
-    if calls:
-        split = [(int(a["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, _ in calls]
-        comb = [(int(b["End_Timestamp"]) - int(b["Start_Timestamp"])) / 1e3 for _, b in calls]
-        span = [(int(b["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, b in calls]
-        n = len(calls)
-        print(f"\nanchor-decode calls: {n}; per call: anchor_decode_kernel {sum(split) / n:.2f} us + "
-              f"attn_combine_kernel {sum(comb) / n:.2f} us = {(sum(split) + sum(comb)) / n:.2f} us of "
+    parts = [("all", calls)] if not split else [(f"calls 1..{split}", calls[:split]),
+                                                 (f"calls {split + 1}..{len(calls)}", calls[split:])]
+    print()
+    for label, cs in parts:
+        if not cs:
+            continue
+        sk = [(int(a["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, _ in cs]
+        comb = [(int(b["End_Timestamp"]) - int(b["Start_Timestamp"])) / 1e3 for _, b in cs]
+        span = [(int(b["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, b in cs]
+        n = len(cs)
+        print(f"anchor-decode calls ({label}): {n}; per call: anchor_decode_kernel {sum(sk) / n:.2f} us + "
+              f"attn_combine_kernel {sum(comb) / n:.2f} us = {(sum(sk) + sum(comb)) / n:.2f} us of "
               f"kernel time; first start to last end {sum(span) / n:.2f} us")
 
 
@@ -230,7 +237,7 @@ def cpu_baseline(w, layer_inputs, n_layers):
 def main():
     args = parse()
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace)
+        summarize_trace(args.summarize_trace, args.trace_split)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
