@@ -540,15 +540,17 @@ AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_le
     p.rows_chunk = 1;
     while (p.rows_chunk < 8 && p.rows_chunk < p.rows_total) p.rows_chunk *= 2;
     p.n_chunks = (p.rows_total + p.rows_chunk - 1) / p.rows_chunk;
-    // Context tokens per split: 512, doubled while the launch still has >=
-    // 1024 workgroups, so long contexts write fewer partials and workgroups
-    // live longer: up to 2048 for decode (512 when 16-head chunks leave no
-    // LDS for more groups), up to 1024 for verification.
+    // Context tokens per split: 512, doubled while the launch still fills
+    // the chip (>= 1024 decode workgroups, two per CU; >= 512 verification
+    // workgroups, also two per CU), so long contexts write fewer partials
+    // and workgroups live longer: up to 2048 tokens (512 for decode when
+    // 16-head chunks leave no LDS for more groups).
     p.split_tokens = kWaves * kKGroup;
-    const int max_split = nq == 1 ? (G > 8 ? 512 : 2048) : 1024;
+    const int max_split = nq == 1 && G > 8 ? 512 : 2048;
+    const int min_workgroups = nq == 1 ? 1024 : 512;
     while (p.split_tokens < max_split) {
         const long long next = ((long long)max_seq_len + 2 * p.split_tokens - 1) / (2 * p.split_tokens);
-        if (next * g.Hkv * B < 1024) break;
+        if (next * g.Hkv * B < min_workgroups) break;
         p.split_tokens *= 2;
     }
     // at least one split, so that empty sequences still get (zero) outputs

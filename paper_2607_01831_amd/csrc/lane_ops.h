@@ -1,7 +1,7 @@
 // Wavefront-level helpers shared by the matrix-core attention kernels:
-// operand vector types and cross-lane reductions on VALU permute paths (DPP
-// inside a 16-lane row, permlane16/32 swaps across rows), no LDS traffic.
-// Not part of the public ABI.
+// operand vector types, cross-lane reductions on VALU permute paths (DPP
+// inside a 16-lane row, permlane16/32 swaps across rows, no LDS traffic),
+// and global-to-LDS copies.  Not part of the public ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -53,6 +53,52 @@ __device__ __forceinline__ float max_kg(float v) {
     v = fmax2(__int_as_float(r[0]), __int_as_float(r[1]));
     r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
     return fmax2(__int_as_float(r[0]), __int_as_float(r[1]));
+}
+
+// ---- Global-to-LDS copies (global_load_lds), issued as inline assembly ----
+// One instruction moves 16 (or 4) bytes per lane from each lane's global
+// address into LDS at M0 + 16 * lane (4 * lane): a wavefront fills one
+// contiguous 1 KB (256 B) LDS run, and the lanes' global addresses choose
+// which source chunk lands where.  The copies count in vmcnt like loads, in
+// issue order.  They are written as assembly so that the compiler, which
+// cannot tell which LDS bytes they fill, does not drain every copy in flight
+// before each LDS read: a kernel using them waits explicitly with
+// wait_vmcnt<N>() before reading the bytes, keeps its own global loads out
+// of the stretches where copies are in flight (their compiler-placed waits
+// would also drain the copies), and waits for vmcnt(0) before reusing the
+// LDS for anything else or exiting.
+
+// LDS byte address of a __shared__ object (low 32 bits of its flat address).
+__device__ __forceinline__ uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)p; }
+
+// The LDS address (and a base address) must be the same in every lane; they
+// are read from the first lane, since the compiler cannot always prove it.
+__device__ __forceinline__ uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ const void *uniform(const void *p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    return (const void *)(uintptr_t)(((uint64_t)uniform((uint32_t)(v >> 32)) << 32) | uniform((uint32_t)v));
+}
+// 16 bytes per lane from sbase + voff (sbase uniform) to LDS at lds + 16 lane.
+__device__ __forceinline__ void lds_copy16(const void *sbase, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(uniform(sbase)),
+                 "s"(uniform(lds))
+                 : "memory");
+}
+// 16 bytes per lane from the lane's own address.
+__device__ __forceinline__ void lds_copy16(const void *addr, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(addr), "s"(uniform(lds))
+                 : "memory");
+}
+// 4 bytes per lane from the lane's own address to LDS at lds + 4 lane.
+__device__ __forceinline__ void lds_copy4(const void *addr, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(addr), "s"(uniform(lds))
+                 : "memory");
+}
+// Wait until at most N vector-memory operations of this wavefront are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 }  // namespace lynx

@@ -158,6 +158,64 @@ def test_verify(nq, tail):
     assert_close(out, ref, what=f"verify k={nq} tail={tail}")
 
 
+@pytest.mark.parametrize("bt", [16, 8])
+def test_verify_paged_ragged(bt):
+    """Verification over paged pools with ragged lengths: block_tokens 16
+    (16-token runs share a block) and 8 (every token row is looked up on its
+    own), k = 8 drafts with the causal tail, 32 query rows per kv head."""
+    Hkv, G, nq = 2, 4, 8
+    lens = [1000, 37, 513]
+    kv = [random_kv(T, Hkv, seed=800 + bt + i) for i, T in enumerate(lens)]
+    c = build_cache([a for a, _ in kv], [b for _, b in kv], Hkv, bt=bt, seed=bt)
+    q = random_bf16((len(lens), nq, Hkv * G, 128), seed=810 + bt)
+    kn = random_bf16((len(lens), nq, Hkv, 128), seed=811 + bt)
+    vn = random_bf16((len(lens), nq, Hkv, 128), seed=812 + bt)
+    out = gpu_verify(c, q, kn, vn)
+    ref, _ = oracle_verify(c, q, kn, vn)
+    assert_close(out, ref, what=f"paged verify bt={bt}")
+
+
+@pytest.mark.parametrize("boost", [30.0, 400.0])
+def test_verify_dominant_late_token(boost):
+    """One draft row meets a late context token whose score dwarfs the rest:
+    with boost 400 the fixed softmax reference of the first tile overflows and
+    the wavefronts holding that token redo their tiles with a running maximum;
+    boost 30 stays on the fast path."""
+    T, Hkv, G, nq = 3000, 2, 4, 8
+    g = torch.Generator().manual_seed(900 + int(boost))
+    q = torch.randn(1, nq, G * Hkv, 128, generator=g)
+    k = torch.randn(T, Hkv, 128, generator=g)
+    v = torch.randn(T, Hkv, 128, generator=g)
+    for h in range(Hkv):
+        k[2500, h] = boost * q[0, 3, h * G] / q[0, 3, h * G].norm()
+    c = build_cache([k.to(torch.bfloat16)], [v.to(torch.bfloat16)], Hkv)
+    qb = q.to(torch.bfloat16)
+    kn = random_bf16((1, nq, Hkv, 128), seed=901)
+    vn = random_bf16((1, nq, Hkv, 128), seed=902)
+    out = gpu_verify(c, qb, kn, vn)
+    ref, _ = oracle_verify(c, qb, kn, vn)
+    assert_close(out, ref, what=f"verify dominant token x{boost}")
+
+
+@pytest.mark.slow
+def test_verify_eight_group_splits():
+    """64K context x 8 kv heads, k = 8: the plan picks 1024-token splits (8
+    groups, two per wavefront); 2 sampled kv heads against the oracle."""
+    T, Hkv, G, nq = 65536, 8, 4, 8
+    k, v = random_kv(T, Hkv, seed=950)
+    c = build_cache([k], [v], Hkv)
+    q = random_bf16((1, nq, Hkv * G, 128), seed=951)
+    kn = random_bf16((1, nq, Hkv, 128), seed=952)
+    vn = random_bf16((1, nq, Hkv, 128), seed=953)
+    mask = np.zeros((1, Hkv), np.uint8)
+    mask[0, [2, 7]] = 1
+    out = gpu_verify(c, q, kn, vn)
+    ref, _ = oracle_verify(c, q, kn, vn, unit_mask=mask)
+    for h in (2, 7):
+        sl = (0, slice(None), slice(h * G, (h + 1) * G), slice(None))
+        assert_close(out[sl], ref[sl], what=f"64K verify kv head {h}")
+
+
 def test_tiny_config_end_to_end():
     """Tiny workload: 1 layer, 8 q / 4 kv heads, 4096 tokens, 4 K outlier
     channels x10 per kv head; encode, merge, anchor decode, verify k = 1."""
