@@ -17,6 +17,12 @@ One step = the whole hot path over all 32 layers:
      plane kind over all layers                               [main stream]
   5. verification attention of the 8 drafts over the codes    [main stream]
 
+After the timed steps, two stages are timed on their own (reported under
+"stages"): the same decode calls with no transport running, and the
+verification of k = 8 drafts at 128K context (32 q / 8 kv heads, one layer,
+merged codes + causal BF16 tail), the configuration the paper's verification
+latency is quoted for.
+
 Printed: one JSON line.  `value` is the anchor-decode attention throughput in
 GB/s of algorithmic KV bytes (144 bytes per token per kv head) over the timed
 steps, from HIP events on the stream the kernels run on.
@@ -48,7 +54,7 @@ WORKLOAD = "llama3-8b-32k"
 COPY_CALIBRATION_BYTES = 640 << 20
 TRAFFIC_SUMMARY = ROOT / "profiles" / "anchor_decode_llama3-8b-32k_traffic.md"
 # sources whose kernels make up one anchor-decode call
-DECODE_SOURCES = ["anchor_decode.hip", "attention.hip", "lynx_internal.h"]
+DECODE_SOURCES = ["anchor_decode.hip", "attention.hip", "lynx_internal.h", "lane_ops.h"]
 
 # algorithmic bytes per unit
 ENC_BYTES_PER_ELEM = 2.0 + 0.5 + 0.5 + 0.0625   # read BF16, write 2 nibbles, metadata
@@ -70,7 +76,11 @@ def parse():
     p.add_argument("--summarize-trace", metavar="DIR")
     p.add_argument("--trace-split", type=int, default=0,
                    help="with --summarize-trace: report the first N decode calls apart from the rest")
+    p.add_argument("--trace-verify-tail", type=int, default=0,
+                   help="with --summarize-trace: report the last N verify calls apart from the rest")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    p.add_argument("--verify-128k-calls", type=int, default=20,
+                   help="timed verification calls at 128K context (0 skips the stage)")
     return p.parse_args()
 
 
@@ -122,14 +132,15 @@ def _short(name: str) -> str:
     return name.split("(")[0][:60]
 
 
-def _decode_calls(rows):
-    """Pair every anchor_decode_kernel dispatch with the attn_combine_kernel
-    dispatch that follows it: one lynx_attn_anchor_decode call."""
+def _calls(rows, first):
+    """Pair every `first` dispatch (anchor_decode_kernel or verify_kernel)
+    with the attn_combine_kernel dispatch that follows it: one
+    lynx_attn_anchor_decode or lynx_attn_verify call."""
     rows = sorted(rows, key=lambda r: int(r["Dispatch_Id"]))
     calls, pending = [], None
     for r in rows:
         n = _short(r["Kernel_Name"])
-        if n == "anchor_decode_kernel":
+        if n == first:
             pending = r
         elif n == "attn_combine_kernel" and pending is not None:
             calls.append((pending, r))
@@ -137,7 +148,22 @@ def _decode_calls(rows):
     return calls
 
 
-def summarize_trace(dirname, split=0):
+def _decode_calls(rows):
+    return _calls(rows, "anchor_decode_kernel")
+
+
+def _print_calls(what, label, cs):
+    first = "anchor_decode_kernel" if what == "anchor-decode" else "verify_kernel"
+    sk = [(int(a["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, _ in cs]
+    comb = [(int(b["End_Timestamp"]) - int(b["Start_Timestamp"])) / 1e3 for _, b in cs]
+    span = [(int(b["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, b in cs]
+    n = len(cs)
+    print(f"{what} calls ({label}): {n}; per call: {first} {sum(sk) / n:.2f} us + "
+          f"attn_combine_kernel {sum(comb) / n:.2f} us = {(sum(sk) + sum(comb)) / n:.2f} us of "
+          f"kernel time; first start to last end {sum(span) / n:.2f} us")
+
+
+def summarize_trace(dirname, split=0, verify_tail=0):
     rows = _csv(dirname, "kernel_trace.csv")
     by = {}
     for r in rows:
@@ -151,15 +177,14 @@ def summarize_trace(dirname, split=0):
                                                  (f"calls {split + 1}..{len(calls)}", calls[split:])]
     print()
     for label, cs in parts:
-        if not cs:
-            continue
-        sk = [(int(a["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, _ in cs]
-        comb = [(int(b["End_Timestamp"]) - int(b["Start_Timestamp"])) / 1e3 for _, b in cs]
-        span = [(int(b["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, b in cs]
-        n = len(cs)
-        print(f"anchor-decode calls ({label}): {n}; per call: anchor_decode_kernel {sum(sk) / n:.2f} us + "
-              f"attn_combine_kernel {sum(comb) / n:.2f} us = {(sum(sk) + sum(comb)) / n:.2f} us of "
-              f"kernel time; first start to last end {sum(span) / n:.2f} us")
+        if cs:
+            _print_calls("anchor-decode", label, cs)
+    vcalls = _calls(rows, "verify_kernel")
+    if verify_tail and len(vcalls) > verify_tail:
+        _print_calls("verify", f"calls 1..{len(vcalls) - verify_tail}", vcalls[:-verify_tail])
+        _print_calls("verify", f"last {verify_tail}", vcalls[-verify_tail:])
+    elif vcalls:
+        _print_calls("verify", "all", vcalls)
 
 
 def summarize_pmc(fetch_dir, write_dir):
@@ -201,6 +226,57 @@ def summarize_pmc(fetch_dir, write_dir):
 
 # --------------------------------------------------------------- CPU baseline --
 
+def verify_128k(calls, dev):
+    """Verification at 128K context (32 q / 8 kv heads, k = 8 drafts with
+    their causal BF16 tail) over merged codes: two encoded layers, used in
+    turn so that no call finds the previous one's bytes in the 256 MB
+    last-level cache; HIP events around the timed calls."""
+    import torch
+
+    from paper_2607_01831_amd import inputs, lynx
+
+    w3 = inputs.WORKLOADS["llama3-8b-verify-128k"]
+    T3, Hkv, Hq, nq = w3.context, w3.Hkv, w3.Hq, w3.drafts
+    L3 = lynx.contiguous_layout(Hkv, 1, T3)
+    table = torch.zeros(1, 1, dtype=torch.int32, device=dev)
+    lens = torch.tensor([T3], dtype=torch.int32, device=dev)
+    pools, qs, kns, vns = [], [], [], []
+    for layer in range(2):
+        pool = lynx.KVPool.allocate(L3, 1, device=dev)
+        k = inputs.kv(w3, "k", layer=layer, device=dev)
+        v = inputs.kv(w3, "v", layer=layer, device=dev)
+        pool.encode(0, T3, table, k, v)
+        pool.merge()
+        del k, v
+        pools.append(pool)
+        qs.append(inputs.queries(w3, layer=layer, nq=nq, device=dev))
+        kn, vn = inputs.drafts_kv(w3, layer=layer, device=dev)
+        kns.append(kn)
+        vns.append(vn)
+    out = torch.empty(1, nq, Hq, 128, dtype=torch.bfloat16, device=dev)
+    ws = lynx.workspace(L3, 1, Hq, nq, T3)
+
+    def call(i):
+        p = pools[i % 2]
+        lynx.lynx_attn_verify(L3, 1, Hq, nq, T3, lens, table, p.k_codes, p.v_codes, p.meta,
+                              qs[i % 2], kns[i % 2], vns[i % 2], out, ws)
+
+    for i in range(4):
+        call(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(calls):
+        call(i)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / calls
+    gbps = T3 * Hkv * VERIFY_BYTES_PER_TOKEN_HEAD / (us * 1e-6) / 1e9
+    del pools
+    return {"verify_128k_us": round(us, 2), "verify_128k_GBps": round(gbps, 2),
+            "verify_128k_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+
+
 def cpu_baseline(w, layer_inputs, n_layers):
     """The CPU oracle, untuned, timed on this host on a bounded sample: the
     anchor decode of the first n_layers layers (all kv heads)."""
@@ -237,7 +313,7 @@ def cpu_baseline(w, layer_inputs, n_layers):
 def main():
     args = parse()
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.trace_split)
+        summarize_trace(args.summarize_trace, args.trace_split, args.trace_verify_tail)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
@@ -358,6 +434,8 @@ def main():
     torch.cuda.synchronize()
     t_dec_alone = e0.elapsed_time(e1) / args.steps
 
+    ver128 = verify_128k(args.verify_128k_calls, dev) if args.verify_128k_calls > 0 else None
+
     def ms(a, b):
         return sum(r[a].elapsed_time(r[b]) for r in recs) / len(recs)
 
@@ -411,6 +489,7 @@ def main():
             "verify_us_per_layer": round(ver_us, 2),
             "verify_GBps": round(ver_gbps, 2),
             "residual_h2d_GBps": round(h2d_gbps, 2),
+            **(ver128 or {}),
             "decode_hidden_behind_h2d": round(overlap, 3),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
             "setup_s": round(t_setup, 1),
