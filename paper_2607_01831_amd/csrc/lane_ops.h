@@ -100,5 +100,26 @@ __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+// The same for a count the compiler folds to a constant (an unrolled loop's
+// arithmetic); a count above 31 waits for all.
+__device__ __forceinline__ void wait_vmcnt_folded(int n) {
+    switch (n) {
+#define LYNX_WAIT_CASE(N) \
+    case N:               \
+        wait_vmcnt<N>();  \
+        break;
+        LYNX_WAIT_CASE(1) LYNX_WAIT_CASE(2) LYNX_WAIT_CASE(3) LYNX_WAIT_CASE(4) LYNX_WAIT_CASE(5)
+        LYNX_WAIT_CASE(6) LYNX_WAIT_CASE(7) LYNX_WAIT_CASE(8) LYNX_WAIT_CASE(9) LYNX_WAIT_CASE(10)
+        LYNX_WAIT_CASE(11) LYNX_WAIT_CASE(12) LYNX_WAIT_CASE(13) LYNX_WAIT_CASE(14) LYNX_WAIT_CASE(15)
+        LYNX_WAIT_CASE(16) LYNX_WAIT_CASE(17) LYNX_WAIT_CASE(18) LYNX_WAIT_CASE(19) LYNX_WAIT_CASE(20)
+        LYNX_WAIT_CASE(21) LYNX_WAIT_CASE(22) LYNX_WAIT_CASE(23) LYNX_WAIT_CASE(24) LYNX_WAIT_CASE(25)
+        LYNX_WAIT_CASE(26) LYNX_WAIT_CASE(27) LYNX_WAIT_CASE(28) LYNX_WAIT_CASE(29) LYNX_WAIT_CASE(30)
+        LYNX_WAIT_CASE(31)
+#undef LYNX_WAIT_CASE
+    default:
+        wait_vmcnt<0>();
+        break;
+    }
+}
 
 }  // namespace lynx
