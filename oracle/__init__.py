@@ -53,6 +53,9 @@ def _load():
     lib.oracle_verify.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P,
                                   P, P, P, P, P, I]
     lib.oracle_verify.restype = I
+    lib.oracle_anchor_decode_tail.argtypes = [I, I, I, I, I, I, P, P, P, P, P, P, P, P,
+                                              P, I, P, P, P, P, P, I]
+    lib.oracle_anchor_decode_tail.restype = I
     _LIB = lib
     return lib
 
@@ -150,10 +153,13 @@ def dequant(mode: str, L: Layout, b: int, T: int, block_table: np.ndarray,
 
 def anchor_decode(L: Layout, Hq: int, seq_lens: np.ndarray, block_table: np.ndarray,
                   k_anc: np.ndarray, v_anc: np.ndarray, meta: Meta, q_bits: np.ndarray,
-                  unit_mask: np.ndarray | None = None, nthreads: int | None = None):
+                  unit_mask: np.ndarray | None = None, nthreads: int | None = None,
+                  k_tail_bits: np.ndarray | None = None, v_tail_bits: np.ndarray | None = None):
     """One query per sequence (q_bits uint16 [B][Hq][128]) over the Anchor-only
-    cache.  Returns (out fp64 [B][Hq][128], lse fp64 [B][Hq]); units left out
-    by unit_mask ([B][Hkv] flags) come back as NaN."""
+    cache, followed, if given, by the BF16 tokens generated since the context
+    arrived (k_tail_bits, v_tail_bits uint16 [B][n_tail][Hkv][128], all
+    visible to the query).  Returns (out fp64 [B][Hq][128], lse fp64 [B][Hq]);
+    units left out by unit_mask ([B][Hkv] flags) come back as NaN."""
     seq_lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
     B = seq_lens.size
     q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
@@ -162,14 +168,56 @@ def anchor_decode(L: Layout, Hq: int, seq_lens: np.ndarray, block_table: np.ndar
     lse = np.full((B, Hq), np.nan)
     mask = None if unit_mask is None else np.ascontiguousarray(unit_mask, dtype=np.uint8)
     bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
-    rc = _load().oracle_anchor_decode(
-        L.Hkv, L.bt, L.max_blocks, L.max_tokens, B, Hq, _ptr(seq_lens), _ptr(bt_arr),
-        _ptr(k_anc), _ptr(v_anc), _ptr(meta.k_scale), _ptr(meta.k_zero),
-        _ptr(meta.v_scale), _ptr(meta.v_zero), _ptr(q_bits), _ptr(out), _ptr(lse),
-        _ptr(mask), nthreads or default_threads())
+    if k_tail_bits is None:
+        rc = _load().oracle_anchor_decode(
+            L.Hkv, L.bt, L.max_blocks, L.max_tokens, B, Hq, _ptr(seq_lens), _ptr(bt_arr),
+            _ptr(k_anc), _ptr(v_anc), _ptr(meta.k_scale), _ptr(meta.k_zero),
+            _ptr(meta.v_scale), _ptr(meta.v_zero), _ptr(q_bits), _ptr(out), _ptr(lse),
+            _ptr(mask), nthreads or default_threads())
+    else:
+        k_tail_bits = np.ascontiguousarray(k_tail_bits, dtype=np.uint16)
+        v_tail_bits = np.ascontiguousarray(v_tail_bits, dtype=np.uint16)
+        n_tail = k_tail_bits.shape[1]
+        assert k_tail_bits.shape == (B, n_tail, L.Hkv, HEAD_DIM)
+        assert v_tail_bits.shape == k_tail_bits.shape
+        rc = _load().oracle_anchor_decode_tail(
+            L.Hkv, L.bt, L.max_blocks, L.max_tokens, B, Hq, _ptr(seq_lens), _ptr(bt_arr),
+            _ptr(k_anc), _ptr(v_anc), _ptr(meta.k_scale), _ptr(meta.k_zero),
+            _ptr(meta.v_scale), _ptr(meta.v_zero), _ptr(q_bits), n_tail, _ptr(k_tail_bits),
+            _ptr(v_tail_bits), _ptr(out), _ptr(lse), _ptr(mask), nthreads or default_threads())
     if rc != 0:
         raise ValueError(f"oracle_anchor_decode failed ({rc})")
     return out, lse
+
+
+def accept_greedy(target_logits: np.ndarray, draft_tokens: np.ndarray):
+    """Greedy verification of k drafted tokens (Sec. 4.3: keep the longest
+    prefix the target model agrees with, then correct the first divergence).
+
+    target_logits: [B][k+1][V], the target model's scores for the token at
+    each of the k draft positions and the one after them; draft_tokens:
+    int [B][k].  The target's choice at a position is its highest score, the
+    lowest vocabulary index among equal scores.  Returns (accepted int32 [B],
+    next_token int32 [B]): the number of leading drafts equal to the target's
+    choices, and the target's choice at the first position after them (the
+    correction, or the bonus token when all k are kept)."""
+    logits = np.asarray(target_logits)
+    drafts = np.asarray(draft_tokens)
+    B, k1, _ = logits.shape
+    k = k1 - 1
+    assert drafts.shape == (B, k)
+    accepted = np.zeros(B, np.int32)
+    next_token = np.zeros(B, np.int32)
+    for b in range(B):
+        n = 0
+        while n < k:
+            choice = int(np.argmax(logits[b, n]))  # first index of the maximum
+            if choice != int(drafts[b, n]):
+                break
+            n += 1
+        accepted[b] = n
+        next_token[b] = int(np.argmax(logits[b, n]))
+    return accepted, next_token
 
 
 def verify(L: Layout, Hq: int, seq_lens: np.ndarray, block_table: np.ndarray,

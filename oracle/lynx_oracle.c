@@ -24,7 +24,9 @@
  *              equation): decode of one query over the Anchor-only cache
  *              (Sec. 4.2 Anchor phase, Speculative Decoder) and the single
  *              parallel verification pass of k draft queries over the merged
- *              cache, causal among the drafts (Sec. 4.3).
+ *              cache, causal among the drafts (Sec. 4.3); the decode may also
+ *              attend the BF16 tokens generated since the context arrived
+ *              (the speculative decoder's own KV, Sec. 4.2-4.3).
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   - K is grouped per channel over 128 consecutive tokens, V per token over
@@ -49,6 +51,8 @@
  *   - Query head hq reads kv head hq / (Hq / Hkv).
  *   - Verification: draft query i sees the whole context plus draft tokens
  *     0..i, whose K/V are BF16 and never quantized.
+ *   - Decode with a tail: the query sees the whole context plus all n_tail
+ *     BF16 tokens passed with it (the caller passes exactly the visible ones).
  *
  * Precision: the codec runs in fp32 because fp32 arithmetic decides the
  * integer codes and the GPU path must take the same decision; attention runs
@@ -306,6 +310,7 @@ static void attend(const double *q, const double *keys, const double *vals,
 typedef struct {
     int mode; /* 0 anchor decode, 1 verify */
     int Hkv, bt, max_blocks, max_tokens, B, Hq, nq;
+    int n_tail; /* anchor decode: BF16 tail tokens per sequence, all visible */
     const int32_t *seq_lens, *block_table;
     const uint8_t *k_plane, *v_plane;
     const float *k_scale, *k_zero, *v_scale, *v_zero;
@@ -333,15 +338,19 @@ static void attention_unit(const attn_job *J, int u, double *keys, double *vals)
     double qd[HEAD_DIM];
     for (int i = 0; i < J->nq; ++i) {
         int n = T;
-        if (J->mode == 1 && J->k_new) {
-            /* Draft tokens 0..i follow the context, in BF16. */
-            for (int j = 0; j <= i; ++j)
+        if (J->k_new) {
+            /* BF16 tokens follow the context: in verification drafts 0..i
+               (causal among the drafts); in decode all n_tail tokens generated
+               since the context was transferred. */
+            const int n_new = J->mode == 1 ? i + 1 : J->n_tail;
+            const int stride = J->mode == 1 ? J->nq : J->n_tail;
+            for (int j = 0; j < n_new; ++j)
                 for (int d = 0; d < HEAD_DIM; ++d) {
-                    size_t src = ((((size_t)b * J->nq + j) * Hkv) + kvh) * HEAD_DIM + d;
+                    size_t src = ((((size_t)b * stride + j) * Hkv) + kvh) * HEAD_DIM + d;
                     keys[(size_t)(T + j) * HEAD_DIM + d] = bf16_bits_to_float(J->k_new[src]);
                     vals[(size_t)(T + j) * HEAD_DIM + d] = bf16_bits_to_float(J->v_new[src]);
                 }
-            n = T + i + 1;
+            n = T + n_new;
         }
         for (int g = 0; g < G; ++g) {
             int hq = kvh * G + g;
@@ -360,7 +369,7 @@ static void *attention_worker(void *arg)
     int max_T = 0;
     for (int b = 0; b < J->B; ++b)
         if (J->seq_lens[b] > max_T) max_T = J->seq_lens[b];
-    size_t one = (size_t)(max_T + J->nq + 1) * HEAD_DIM;
+    size_t one = (size_t)(max_T + J->nq + J->n_tail + 1) * HEAD_DIM;
     double *keys = (double *)malloc(one * sizeof(double));
     double *vals = (double *)malloc(one * sizeof(double));
     if (!keys || !vals) {
@@ -378,7 +387,7 @@ static void *attention_worker(void *arg)
 static int run_attention(attn_job *base)
 {
     if (base->Hkv < 1 || base->Hq < 1 || base->Hq % base->Hkv != 0 || base->B < 0 ||
-        base->nq < 1)
+        base->nq < 1 || base->n_tail < 0)
         return -1;
     for (int b = 0; b < base->B; ++b)
         if (base->seq_lens[b] < 0 || base->seq_lens[b] > base->max_tokens) return -1;
@@ -430,6 +439,37 @@ int oracle_anchor_decode(int Hkv, int bt, int max_blocks, int max_tokens, int B,
     J.k_plane = k_anc; J.v_plane = v_anc;
     J.k_scale = k_scale; J.k_zero = k_zero; J.v_scale = v_scale; J.v_zero = v_zero;
     J.q = q; J.out = out; J.lse = lse; J.unit_mask = unit_mask;
+    J.nthreads = nthreads;
+    return run_attention(&J);
+}
+
+/*
+ * Anchor-phase decode with the tokens generated since the context arrived:
+ * one query per sequence over the Anchor-only cache followed by n_tail BF16
+ * tokens (k_new, v_new: BF16 bits [B][n_tail][Hkv][128]), all visible to the
+ * query.  n_tail = 0 is the plain anchor decode.
+ */
+int oracle_anchor_decode_tail(int Hkv, int bt, int max_blocks, int max_tokens, int B,
+                              int Hq, const int32_t *seq_lens,
+                              const int32_t *block_table, const uint8_t *k_anc,
+                              const uint8_t *v_anc, const float *k_scale,
+                              const float *k_zero, const float *v_scale,
+                              const float *v_zero, const uint16_t *q, int n_tail,
+                              const uint16_t *k_new, const uint16_t *v_new,
+                              double *out, double *lse, const uint8_t *unit_mask,
+                              int nthreads)
+{
+    if (n_tail < 0 || (n_tail > 0 && (!k_new || !v_new))) return -1;
+    attn_job J;
+    memset(&J, 0, sizeof J);
+    J.mode = 0;
+    J.Hkv = Hkv; J.bt = bt; J.max_blocks = max_blocks; J.max_tokens = max_tokens;
+    J.B = B; J.Hq = Hq; J.nq = 1; J.n_tail = n_tail;
+    J.seq_lens = seq_lens; J.block_table = block_table;
+    J.k_plane = k_anc; J.v_plane = v_anc;
+    J.k_scale = k_scale; J.k_zero = k_zero; J.v_scale = v_scale; J.v_zero = v_zero;
+    J.q = q; J.k_new = n_tail > 0 ? k_new : NULL; J.v_new = n_tail > 0 ? v_new : NULL;
+    J.out = out; J.lse = lse; J.unit_mask = unit_mask;
     J.nthreads = nthreads;
     return run_attention(&J);
 }

@@ -174,3 +174,43 @@ def test_verify_without_drafts_is_decode_over_full_codes():
     out, _ = oracle.verify(L, 2, np.array([77]), table, kc, vc, meta, q)
     np.testing.assert_array_equal(out[0, 0], out[0, 1])
     assert not np.allclose(out[0, 0], out[0, 2])
+
+
+@pytest.mark.parametrize("n_tail,lens", [(1, [50, 0]), (5, [129, 33]), (64, [300, 1])])
+def test_anchor_decode_tail_vs_sdpa(n_tail, lens):
+    """Decode with the tokens generated since the context arrived: the query
+    sees the anchor-only context and every BF16 tail token (an empty context
+    leaves the tail alone)."""
+    rng = np.random.default_rng(600 + n_tail)
+    Hkv, G = 2, 4
+    Hq = Hkv * G
+    L, table, planes, meta, _, _ = make_cache(rng, lens, Hkv)
+    B = len(lens)
+    q = bf16_bits(rng.standard_normal((B, Hq, D)).astype(np.float32))
+    kt = bf16_bits(rng.standard_normal((B, n_tail, Hkv, D)).astype(np.float32))
+    vt = bf16_bits(rng.standard_normal((B, n_tail, Hkv, D)).astype(np.float32))
+    out, lse = oracle.anchor_decode(L, Hq, np.array(lens), table, planes["k_anc"], planes["v_anc"],
+                                    meta, q, nthreads=2, k_tail_bits=kt, v_tail_bits=vt)
+    for b, T in enumerate(lens):
+        kh, vh = oracle.dequant("anchor", L, b, T, table, planes["k_anc"], planes["v_anc"], meta)
+        kk = np.concatenate([kh.transpose(1, 0, 2), bits_to_f64(kt[b]).transpose(1, 0, 2)], axis=1)
+        vv = np.concatenate([vh.transpose(1, 0, 2), bits_to_f64(vt[b]).transpose(1, 0, 2)], axis=1)
+        kk, vv = np.repeat(kk, G, axis=0), np.repeat(vv, G, axis=0)   # [Hq][T + n_tail][D]
+        qq = bits_to_f64(q[b])[:, None, :]
+        ref = sdpa_ref(qq, kk, vv)[:, 0, :]
+        np.testing.assert_allclose(out[b], ref, rtol=1e-10, atol=1e-12)
+        s = np.einsum("hd,htd->ht", qq[:, 0, :], kk) / math.sqrt(D)
+        np.testing.assert_allclose(lse[b], torch.logsumexp(torch.from_numpy(s), dim=1).numpy(),
+                                   rtol=1e-12, atol=1e-12)
+
+
+def test_anchor_decode_empty_tail_is_plain_decode():
+    rng = np.random.default_rng(611)
+    L, table, planes, meta, _, _ = make_cache(rng, [70, 9], 2)
+    q = bf16_bits(rng.standard_normal((2, 4, D)).astype(np.float32))
+    empty = np.zeros((2, 0, 2, D), np.uint16)
+    a, la = oracle.anchor_decode(L, 4, np.array([70, 9]), table, planes["k_anc"], planes["v_anc"], meta, q)
+    b, lb = oracle.anchor_decode(L, 4, np.array([70, 9]), table, planes["k_anc"], planes["v_anc"], meta, q,
+                                 k_tail_bits=empty, v_tail_bits=empty)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(la, lb)

@@ -5,7 +5,8 @@ oracle itself), builds it on the CPU, and runs the CPU pin tests against the
 planted build in a subprocess: they must fail.  Covered mistakes: wrong
 rounding, a dropped term, a wrong constant, a swapped nibble order, a wrong
 group size, a transposed metadata index, a wrong sign, a wrong head mapping,
-a missing causal mask, a swapped merge.
+a missing causal mask, a dropped decode tail or a wrong tail stride, a
+swapped merge.
 """
 import os
 import subprocess
@@ -31,8 +32,12 @@ MUTANTS = {
     "softmax_sign": ("s[t] = exp(s[t] - m);", "s[t] = exp(m - s[t]);"),
     "no_sm_scale": ("s[t] = acc * sm_scale;", "s[t] = acc;"),
     "gqa_strided": ("int hq = kvh * G + g;", "int hq = g * Hkv + kvh;"),
-    "no_causal_mask": [("for (int j = 0; j <= i; ++j)", "for (int j = 0; j < J->nq; ++j)"),
-                       ("n = T + i + 1;", "n = T + J->nq;")],
+    "no_causal_mask": ("const int n_new = J->mode == 1 ? i + 1 : J->n_tail;",
+                       "const int n_new = J->mode == 1 ? J->nq : J->n_tail;"),
+    "decode_tail_dropped": ("const int n_new = J->mode == 1 ? i + 1 : J->n_tail;",
+                            "const int n_new = J->mode == 1 ? i + 1 : 0;"),
+    "decode_tail_stride": ("const int stride = J->mode == 1 ? J->nq : J->n_tail;",
+                           "const int stride = J->nq;"),
     "merge_swapped": ("codes[e] = (uint8_t)(a * 16 + r);", "codes[e] = (uint8_t)(r * 16 + a);"),
     "v_meta_wrong_stride": ("size_t vm = ((size_t)b * Hkv + h) * (size_t)max_tokens + t;\n    double kq",
                             "size_t vm = ((size_t)h * 1 + b) * (size_t)max_tokens + t;\n    double kq"),
