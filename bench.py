@@ -17,11 +17,13 @@ One step = the whole hot path over all 32 layers:
      plane kind over all layers                               [main stream]
   5. verification attention of the 8 drafts over the codes    [main stream]
 
-After the timed steps, two stages are timed on their own (reported under
-"stages"): the same decode calls with no transport running, and the
+After the timed steps, four stages are timed on their own (reported under
+"stages"): the same decode calls with no transport running; the
 verification of k = 8 drafts at 128K context (32 q / 8 kv heads, one layer,
 merged codes + causal BF16 tail), the configuration the paper's verification
-latency is quoted for.
+latency is quoted for; the decode calls once more with the 8 BF16 tokens the
+speculative decoder generated; and greedy acceptance of 8 drafts over a
+128256-entry vocabulary.
 
 Printed: one JSON line.  `value` is the anchor-decode attention throughput in
 GB/s of algorithmic KV bytes (144 bytes per token per kv head) over the timed
@@ -79,6 +81,8 @@ def parse():
     p.add_argument("--trace-verify-tail", type=int, default=0,
                    help="with --summarize-trace: report the last N verify calls apart from the rest")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    p.add_argument("--no-spec-stages", dest="spec_stages", action="store_false",
+                   help="skip the decode-with-tail and draft-acceptance stages")
     p.add_argument("--verify-128k-calls", type=int, default=20,
                    help="timed verification calls at 128K context (0 skips the stage)")
     return p.parse_args()
@@ -436,6 +440,39 @@ def main():
 
     ver128 = verify_128k(args.verify_128k_calls, dev) if args.verify_128k_calls > 0 else None
 
+    # The speculative decoder's own pieces, timed alone: decode over the
+    # anchors plus the 8 BF16 tokens it generated (32 layers), and greedy
+    # acceptance of 8 drafts over a 128256-entry vocabulary.
+    spec = {}
+    if args.spec_stages:
+        e0, e1 = ev(), ev()
+        e0.record(main_s)
+        for _ in range(args.steps):
+            for l in range(n_layers):
+                p = pools[l]
+                lynx.lynx_attn_anchor_decode_tail(L, 1, Hq, T, lens, table, p.k_anc, p.v_anc, p.meta,
+                                                  Q[l], KN[l], VN[l], out, None, ws)
+        e1.record(main_s)
+        torch.cuda.synchronize()
+        spec["anchor_decode_tail8_us_per_layer"] = round(e0.elapsed_time(e1) * 1e3 / (args.steps * n_layers), 3)
+        vocab = 128256
+        g = torch.Generator().manual_seed(7)
+        logits = torch.randn(1, nq + 1, vocab, generator=g).to(dev)
+        drafts = logits[:, :nq].argmax(dim=2).to(torch.int32)
+        acc = torch.empty(1, dtype=torch.int32, device=dev)
+        nxt = torch.empty(1, dtype=torch.int32, device=dev)
+        aws = torch.empty(max(lynx.lynx_spec_accept_workspace_bytes(1, nq, vocab), 16),
+                          dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            lynx.lynx_spec_accept_greedy(logits, drafts, acc, nxt, aws)
+        e0.record(main_s)
+        for _ in range(20):
+            lynx.lynx_spec_accept_greedy(logits, drafts, acc, nxt, aws)
+        e1.record(main_s)
+        torch.cuda.synchronize()
+        spec["accept_greedy_k8_vocab128256_us"] = round(e0.elapsed_time(e1) * 1e3 / 20, 2)
+        spec["accept_greedy_all_kept"] = int(acc.item()) == nq
+
     def ms(a, b):
         return sum(r[a].elapsed_time(r[b]) for r in recs) / len(recs)
 
@@ -490,6 +527,7 @@ def main():
             "verify_GBps": round(ver_gbps, 2),
             "residual_h2d_GBps": round(h2d_gbps, 2),
             **(ver128 or {}),
+            **spec,
             "decode_hidden_behind_h2d": round(overlap, 3),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
             "setup_s": round(t_setup, 1),

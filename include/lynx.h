@@ -182,6 +182,61 @@ int lynx_attn_verify(const lynx_layout *L, int32_t B, int32_t Hq, int32_t k,
                      const void *q_bf16, const void *k_new, const void *v_new, void *out_bf16,
                      void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * lynx_attn_anchor_decode_tail -- lynx_attn_anchor_decode for a speculative
+ * decoder that has already generated tokens of its own (Sec. 4.2-4.3): the
+ * query attends the Anchor-only context and, after it, the n_tail tokens
+ * generated since the context arrived, whose K/V are BF16 (computed locally,
+ * never quantized), all of them visible to the query (the caller passes
+ * exactly the visible ones).  Arguments as lynx_attn_anchor_decode, plus:
+ *
+ *   n_tail       generated tokens per sequence, 0 <= n_tail <= 64 (0 is the
+ *                plain anchor decode)
+ *   k_tail, v_tail  BF16 [B][n_tail][Hkv][128] (device), or NULL when
+ *                n_tail == 0
+ *   workspace    >= lynx_attn_workspace_bytes(L, B, Hq, 1, max_seq_len)
+ * A sequence with no context attends its tail alone.
+ */
+int lynx_attn_anchor_decode_tail(const lynx_layout *L, int32_t B, int32_t Hq,
+                                 int32_t max_seq_len, const int32_t *seq_lens,
+                                 const int32_t *block_table, const uint8_t *k_anc,
+                                 const uint8_t *v_anc, const lynx_meta *meta, const void *q_bf16,
+                                 int32_t n_tail, const void *k_tail, const void *v_tail,
+                                 void *out_bf16, float *lse, void *workspace,
+                                 size_t workspace_bytes, void *stream);
+
+/*
+ * lynx_spec_accept_workspace_bytes -- device workspace of
+ * lynx_spec_accept_greedy for B sequences, k drafts and a vocabulary of
+ * `vocab` entries.  Returns 0 on invalid arguments.
+ */
+size_t lynx_spec_accept_workspace_bytes(int32_t B, int32_t k, int32_t vocab);
+
+/*
+ * lynx_spec_accept_greedy -- greedy acceptance of the drafts after the
+ * verification pass (Sec. 4.3: keep the longest prefix of the drafts the
+ * target model agrees with, correct the first divergence).  The target's
+ * choice at a position is its highest score, the lowest vocabulary index
+ * among equal scores.
+ *
+ *   B, k, vocab    sequences (<= 65535), drafts per sequence (1..64) and
+ *                  vocabulary size
+ *   target_logits  fp32 [B][k+1][vocab] (device): the target's scores for
+ *                  the token at each draft position and at the one after the
+ *                  last; scores must be finite (a NaN never wins)
+ *   draft_tokens   int32 [B][k] (device)
+ *   accepted       int32 [B] (device, written): number of leading drafts
+ *                  equal to the target's choices (0..k)
+ *   next_token     int32 [B] (device, written): the target's choice at
+ *                  position `accepted` (the correction, or the bonus token
+ *                  when all k are kept)
+ *   workspace      >= lynx_spec_accept_workspace_bytes(B, k, vocab)
+ */
+int lynx_spec_accept_greedy(int32_t B, int32_t k, int32_t vocab, const float *target_logits,
+                            const int32_t *draft_tokens, int32_t *accepted,
+                            int32_t *next_token, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
 /* Static, human-readable text for a lynx_status value. */
 const char *lynx_strerror(int status);
 

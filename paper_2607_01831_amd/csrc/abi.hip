@@ -139,7 +139,36 @@ int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t
         return LYNX_EWORKSPACE;
     hipError_t e = lynx::launch_attention(
         lynx::KvMode::kAnchor, g, p, B, Hq, 1, max_seq_len, seq_lens, block_table, k_anc, v_anc,
-        mp, static_cast<const uint16_t *>(q_bf16), nullptr, nullptr,
+        mp, static_cast<const uint16_t *>(q_bf16), nullptr, nullptr, 0,
+        static_cast<uint16_t *>(out_bf16), lse, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_attn_anchor_decode_tail(const lynx_layout *L, int32_t B, int32_t Hq,
+                                 int32_t max_seq_len, const int32_t *seq_lens,
+                                 const int32_t *block_table, const uint8_t *k_anc,
+                                 const uint8_t *v_anc, const lynx_meta *meta, const void *q_bf16,
+                                 int32_t n_tail, const void *k_tail, const void *v_tail,
+                                 void *out_bf16, float *lse, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_attention_common(L, B, Hq, max_seq_len, seq_lens, block_table, k_anc, v_anc,
+                                    meta, q_bf16, out_bf16, &g, &mp);
+    if (rc != LYNX_OK) return rc;
+    if (n_tail < 0 || n_tail > 64) return LYNX_EINVAL;
+    if (n_tail > 0 && (!k_tail || !v_tail || !aligned16(k_tail) || !aligned16(v_tail)))
+        return LYNX_EINVAL;
+    if (B == 0) return LYNX_OK;
+    if (lse && !aligned16(lse)) return LYNX_EINVAL;
+    const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, 1, max_seq_len, false);
+    if (!workspace || !aligned16(workspace) || workspace_bytes < p.workspace_bytes())
+        return LYNX_EWORKSPACE;
+    hipError_t e = lynx::launch_attention(
+        lynx::KvMode::kAnchor, g, p, B, Hq, 1, max_seq_len, seq_lens, block_table, k_anc, v_anc,
+        mp, static_cast<const uint16_t *>(q_bf16),
+        n_tail > 0 ? static_cast<const uint16_t *>(k_tail) : nullptr,
+        n_tail > 0 ? static_cast<const uint16_t *>(v_tail) : nullptr, n_tail,
         static_cast<uint16_t *>(out_bf16), lse, workspace, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
@@ -165,8 +194,31 @@ int lynx_attn_verify(const lynx_layout *L, int32_t B, int32_t Hq, int32_t k,
     hipError_t e = lynx::launch_attention(
         lynx::KvMode::kCodes, g, p, B, Hq, k, max_seq_len, seq_lens, block_table, k_codes, v_codes,
         mp, static_cast<const uint16_t *>(q_bf16), static_cast<const uint16_t *>(k_new),
-        static_cast<const uint16_t *>(v_new), static_cast<uint16_t *>(out_bf16), nullptr,
+        static_cast<const uint16_t *>(v_new), k, static_cast<uint16_t *>(out_bf16), nullptr,
         workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+size_t lynx_spec_accept_workspace_bytes(int32_t B, int32_t k, int32_t vocab) {
+    if (B < 0 || B > 65535 || k < 1 || k > 64 || vocab < 1) return 0;
+    return (size_t)B * (size_t)(k + 1) * (size_t)lynx::spec_accept_chunks(vocab) *
+           (sizeof(float) + sizeof(int32_t));
+}
+
+int lynx_spec_accept_greedy(int32_t B, int32_t k, int32_t vocab, const float *target_logits,
+                            const int32_t *draft_tokens, int32_t *accepted,
+                            int32_t *next_token, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+    if (B < 0 || B > 65535 || k < 1 || k > 64 || vocab < 1) return LYNX_EINVAL;
+    if (B == 0) return LYNX_OK;
+    const void *ptrs[] = {target_logits, draft_tokens, accepted, next_token};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    const size_t need = lynx_spec_accept_workspace_bytes(B, k, vocab);
+    if (!workspace || !aligned16(workspace) || workspace_bytes < need) return LYNX_EWORKSPACE;
+    hipError_t e = lynx::launch_spec_accept_greedy(B, k, vocab, target_logits, draft_tokens,
+                                                   accepted, next_token, workspace,
+                                                   static_cast<hipStream_t>(stream));
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
 

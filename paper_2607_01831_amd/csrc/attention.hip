@@ -38,7 +38,9 @@ struct AttnArgs {
     int B, Hq, nq, G, max_seq_len;
     int rows_total, n_ctx_splits, n_splits, split_tokens;
     int split_base;  // split index of blockIdx.x == 0
-    int tail_in_combine;  // the combine kernel attends the BF16 draft tail itself
+    int tail_in_combine;  // the combine kernel attends the BF16 tail itself
+    int tail_count;       // tokens of the tail every query sees; -1: query i sees i + 1 (drafts)
+    int tail_stride;      // tail tokens stored per sequence in k_new / v_new
     const int32_t *seq_lens;
     const int32_t *block_table;
     const uint8_t *k_plane;
@@ -382,11 +384,12 @@ __global__ __launch_bounds__(kAttnThreads) void attn_split_kernel(AttnArgs a) {
 constexpr int kCombineThreads = 256;
 
 // One workgroup per (row, kv head, sequence): merge the partials of all
-// splits, normalise, round to BF16, write lse.  Thread (split group sg,
-// float4 column d4) folds every 8th split into a running (max, sum, output),
-// loading 16 splits' partial outputs and (max, sum) pairs together so that
-// each step costs one round trip to memory; the 8 running triples meet in
-// LDS.
+// splits and the BF16 tail tokens, normalise, round to BF16, write lse.
+// Thread (split group sg, float4 column d4) folds every 8th split into a
+// running (max, sum, output), loading 16 splits' partial outputs and (max,
+// sum) pairs together so that each step costs one round trip to memory;
+// then every 8th tail token the same way, as a partial of weight 1.  The 8
+// running triples meet in LDS.
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a, uint16_t *out,
                                                                        float *lse) {
     const int gr = blockIdx.x;
@@ -396,33 +399,44 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     const int Hkv = a.geo.Hkv;
     const size_t base = (((size_t)b * Hkv + h) * a.rows_total + gr) * a.n_splits;
     // splits with partials: every split, or the context ones when this kernel
-    // attends the draft tail itself
+    // attends the tail itself
     const int n = a.tail_in_combine ? a.n_ctx_splits : a.n_splits;
     constexpr int kGroups = kCombineThreads / (kHeadDim / 4);  // 8 split groups
     constexpr int kBatch = 16;
     __shared__ float4 s_acc[kGroups][kHeadDim / 4];
     __shared__ float s_m[kGroups][kHeadDim / 4], s_l[kGroups][kHeadDim / 4];
-    __shared__ float s_ts[64];  // draft-tail scores (log2 units)
+    __shared__ float s_ts[64];  // tail scores (log2 units)
 
-    // query row gr <-> (draft qi, head qg); with a tail, draft qi also sees
-    // the BF16 K/V of drafts 0..qi (causal among the drafts)
+    // query row gr <-> (query qi, head qg); with a tail, query qi also sees
+    // the BF16 tokens of the tail: drafts 0..qi in verification (causal among
+    // the drafts), all tail_count generated tokens in decode
     const int qi = gr / a.G;
     const int qg = gr % a.G;
     const size_t qrow = ((size_t)b * a.nq + qi) * a.Hq + (size_t)h * a.G + qg;
-    const int n_tail = a.tail_in_combine ? qi + 1 : 0;
+    const int n_tail = a.tail_in_combine ? (a.tail_count < 0 ? qi + 1 : a.tail_count) : 0;
     if (n_tail > 0) {
-        const int lane = tid & 63, wv = tid >> 6;
-        const uint32_t qw = reinterpret_cast<const uint32_t *>(a.q + qrow * kHeadDim)[lane];
-        const float q0 = bf16_lo(qw), q1 = bf16_hi(qw);
+        // tail scores, 16 tokens per pass: thread (token tid / 16, dims
+        // 8 (tid % 16) .. + 7), summed over the 16 lanes of a token
+        const int piece = tid & 15;
+        float qv[8];
+        unpack8_bf16(*reinterpret_cast<const uint4 *>(a.q + qrow * kHeadDim + 8 * piece), qv);
         const float sm = kLog2e * rsqrtf((float)kHeadDim);
-        for (int j = wv; j < n_tail; j += kCombineThreads / 64) {
-            const uint32_t kw = reinterpret_cast<const uint32_t *>(
-                a.k_new + (((size_t)b * a.nq + j) * Hkv + h) * kHeadDim)[lane];
-            float d = fmaf(q0, bf16_lo(kw), q1 * bf16_hi(kw));
+        for (int j0 = 0; j0 < n_tail; j0 += 16) {
+            const int j = j0 + (tid >> 4);
+            float d = 0.0f;
+            if (j < n_tail) {
+                float kv[8];
+                unpack8_bf16(*reinterpret_cast<const uint4 *>(
+                                 a.k_new + (((size_t)b * a.tail_stride + j) * Hkv + h) * kHeadDim + 8 * piece),
+                             kv);
 #pragma unroll
-            for (int s = 1; s < 64; s <<= 1) d += __shfl_xor(d, s);
-            if (lane == 0) s_ts[j] = d * sm;
+                for (int e = 0; e < 8; ++e) d = fmaf(qv[e], kv[e], d);
+            }
+#pragma unroll
+            for (int off = 8; off > 0; off >>= 1) d += __shfl_xor(d, off);
+            if (piece == 0 && j < n_tail) s_ts[j] = d * sm;
         }
+        __syncthreads();
     }
 
     const int d4 = tid % (kHeadDim / 4);
@@ -431,19 +445,12 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     float m_t = -INFINITY, l_t = 0.0f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     bool nan = false;
-    for (int s0 = sg; s0 < n; s0 += kGroups * kBatch) {
-        float4 v[kBatch];
-        float2 ml[kBatch];
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int s = min(s0 + kGroups * u, n - 1);
-            v[u] = o4[(size_t)s * (kHeadDim / 4)];
-            ml[u] = a.ws_ml[base + s];
-        }
+    // fold a batch of partials (max ml.x, sum ml.y, output v) into the running triple
+    auto fold = [&](const float4 (&v)[kBatch], float2 (&ml)[kBatch], const bool (&live)[kBatch]) {
         float mb = m_t;
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            if (s0 + kGroups * u >= n) ml[u] = make_float2(-INFINITY, 0.0f);
+            if (!live[u]) ml[u] = make_float2(-INFINITY, 0.0f);
             mb = fmaxf(mb, ml[u].x);
         }
         const float sc = m_t == -INFINITY ? 0.0f : exp2f(m_t - mb);
@@ -465,37 +472,47 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
             acc.w = fmaf(x.w, e, acc.w);
         }
         m_t = mb;
+    };
+    for (int s0 = sg; s0 < n; s0 += kGroups * kBatch) {
+        float4 v[kBatch];
+        float2 ml[kBatch];
+        bool live[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int s = min(s0 + kGroups * u, n - 1);
+            v[u] = o4[(size_t)s * (kHeadDim / 4)];
+            ml[u] = a.ws_ml[base + s];
+            live[u] = s0 + kGroups * u < n;
+        }
+        fold(v, ml, live);
+    }
+    // the tail tokens: partials (score, 1, value)
+    for (int j0 = sg; j0 < n_tail; j0 += kGroups * kBatch) {
+        float4 v[kBatch];
+        float2 ml[kBatch];
+        bool live[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int j = min(j0 + kGroups * u, n_tail - 1);
+            const uint2 vw = *reinterpret_cast<const uint2 *>(
+                a.v_new + (((size_t)b * a.tail_stride + j) * Hkv + h) * kHeadDim + 4 * d4);
+            v[u] = make_float4(bf16_lo(vw.x), bf16_hi(vw.x), bf16_lo(vw.y), bf16_hi(vw.y));
+            ml[u] = make_float2(s_ts[j], 1.0f);
+            live[u] = j0 + kGroups * u < n_tail;
+        }
+        fold(v, ml, live);
     }
     s_acc[sg][d4] = acc;
     s_m[sg][d4] = m_t;
     s_l[sg][d4] = nan ? NAN : l_t;
     __syncthreads();
     if (sg == 0) {
-        // the draft tail as one more partial: (tm, tl, to) over dims 4 d4 ..
-        float tm = -INFINITY, tl = 0.0f;
-        float4 to = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int j = 0; j < n_tail; ++j) tm = fmaxf(tm, s_ts[j]);
-        for (int j = 0; j < n_tail; ++j) {
-            const float p = exp2f(s_ts[j] - tm);
-            const uint2 vw = *reinterpret_cast<const uint2 *>(
-                a.v_new + (((size_t)b * a.nq + j) * Hkv + h) * kHeadDim + 4 * d4);
-            tl += p;
-            to.x = fmaf(p, bf16_lo(vw.x), to.x);
-            to.y = fmaf(p, bf16_hi(vw.x), to.y);
-            to.z = fmaf(p, bf16_lo(vw.y), to.z);
-            to.w = fmaf(p, bf16_hi(vw.y), to.w);
-        }
-        float M = tm;
+        float M = -INFINITY;
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) M = fmaxf(M, s_m[g][d4]);
         float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
         float L = 0.0f;
         bool any_nan = false;
-        if (n_tail > 0) {
-            const float f = exp2f(tm - M);
-            O = make_float4(to.x * f, to.y * f, to.z * f, to.w * f);
-            L = tl * f;
-        }
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
             const float f = s_m[g][d4] == -INFINITY ? 0.0f : exp2f(s_m[g][d4] - M);
@@ -566,7 +583,8 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
                             int nq, int max_seq_len, const int32_t *seq_lens,
                             const int32_t *block_table, const uint8_t *k_plane,
                             const uint8_t *v_plane, MetaPtrs meta, const uint16_t *q,
-                            const uint16_t *k_new, const uint16_t *v_new, uint16_t *out,
+                            const uint16_t *k_new, const uint16_t *v_new, int tail_count,
+                            uint16_t *out,
                             float *lse, void *workspace, hipStream_t stream) {
     if (B == 0 || plan.n_splits == 0) return hipSuccess;
     AttnArgs a;
@@ -581,7 +599,12 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
     a.n_splits = plan.n_splits;
     a.split_tokens = plan.split_tokens;
     a.split_base = 0;
-    a.tail_in_combine = (mode == KvMode::kCodes && k_new != nullptr) ? 1 : 0;
+    // the matrix-core paths leave the BF16 tail to the combine kernel:
+    // causal drafts in verification, tail_count generated tokens in decode
+    const bool mfma_path = mode == KvMode::kCodes || nq == 1;
+    a.tail_in_combine = (mfma_path && k_new != nullptr) ? 1 : 0;
+    a.tail_count = mode == KvMode::kCodes ? -1 : tail_count;
+    a.tail_stride = mode == KvMode::kCodes ? nq : tail_count;
     a.seq_lens = seq_lens;
     a.block_table = block_table;
     a.k_plane = k_plane;
@@ -592,7 +615,7 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
     a.v_new = v_new;
     a.ws_o = reinterpret_cast<float *>(workspace);
     a.ws_ml = reinterpret_cast<float2 *>(reinterpret_cast<char *>(workspace) + plan.o_bytes);
-    if (mode == KvMode::kAnchor && nq == 1 && k_new == nullptr) {
+    if (mode == KvMode::kAnchor && nq == 1) {
         // matrix-core decode over the anchor nibbles
         DecodeArgs d;
         d.geo = g;

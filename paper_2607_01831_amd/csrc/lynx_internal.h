@@ -71,7 +71,7 @@ struct DecodeArgs {
 hipError_t launch_anchor_decode_mfma(const DecodeArgs &args, int chunks, hipStream_t stream);
 
 // Arguments of the matrix-core verification kernel (verify.hip): context
-// splits only; the BF16 draft tail is the last split, computed elsewhere.
+// splits only; the combine kernel attends the BF16 draft tail.
 struct VerifyArgs {
     Geometry geo;
     int B, Hq, G, nq, max_seq_len;
@@ -93,11 +93,21 @@ hipError_t launch_verify_mfma(const VerifyArgs &args, int split_groups, hipStrea
 
 AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_len, bool tail);
 
+// k_new / v_new: the BF16 tail, or nullptr.  Verification (kCodes): k drafts
+// per sequence, causal among the drafts.  Decode (kAnchor, nq == 1):
+// tail_count generated tokens per sequence, all visible to the query.
 hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan, int B, int Hq,
                             int nq, int max_seq_len, const int32_t *seq_lens,
                             const int32_t *block_table, const uint8_t *k_plane,
                             const uint8_t *v_plane, MetaPtrs meta, const uint16_t *q,
-                            const uint16_t *k_new, const uint16_t *v_new, uint16_t *out,
-                            float *lse, void *workspace, hipStream_t stream);
+                            const uint16_t *k_new, const uint16_t *v_new, int tail_count,
+                            uint16_t *out, float *lse, void *workspace, hipStream_t stream);
+
+// ---- greedy acceptance of drafts (spec.hip) -----------------------------------
+// Workspace: B * (k + 1) * spec_accept_chunks(vocab) (score, index) pairs.
+int spec_accept_chunks(int vocab);
+hipError_t launch_spec_accept_greedy(int B, int k, int vocab, const float *logits,
+                                     const int32_t *drafts, int32_t *accepted,
+                                     int32_t *next_token, void *workspace, hipStream_t stream);
 
 }  // namespace lynx

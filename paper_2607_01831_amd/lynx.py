@@ -61,6 +61,10 @@ def load():
                                     ctypes.c_int),
         "lynx_attn_verify": ([LP, I32, I32, I32, I32, P, P, P, P, MP, P, P, P, P, P, SZ, P],
                              ctypes.c_int),
+        "lynx_attn_anchor_decode_tail": ([LP, I32, I32, I32, P, P, P, P, MP, P, I32, P, P, P, P, P,
+                                          SZ, P], ctypes.c_int),
+        "lynx_spec_accept_workspace_bytes": ([I32, I32, I32], SZ),
+        "lynx_spec_accept_greedy": ([I32, I32, I32, P, P, P, P, P, SZ, P], ctypes.c_int),
         "lynx_strerror": ([ctypes.c_int], ctypes.c_char_p),
     }
     for name, (args, res) in sigs.items():
@@ -182,6 +186,40 @@ def lynx_attn_anchor_decode(L: Layout, B: int, Hq: int, max_seq_len: int, seq_le
         ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table), _ptr(k_anc),
         _ptr(v_anc), ctypes.byref(met), _ptr(q), _ptr(out), _ptr(lse), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def lynx_attn_anchor_decode_tail(L: Layout, B: int, Hq: int, max_seq_len: int, seq_lens,
+                                 block_table, k_anc, v_anc, meta: Meta, q, k_tail, v_tail, out,
+                                 lse=None, workspace_buf=None, stream=None) -> None:
+    """Anchor decode that also attends the BF16 tail k_tail / v_tail
+    ([B][n_tail][Hkv][128], or None for n_tail = 0)."""
+    lay, met = L.c(), meta.c()
+    ws = workspace_buf
+    n_tail = 0 if k_tail is None else int(k_tail.shape[1])
+    _check("lynx_attn_anchor_decode_tail", load().lynx_attn_anchor_decode_tail(
+        ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table), _ptr(k_anc),
+        _ptr(v_anc), ctypes.byref(met), _ptr(q), n_tail, _ptr(k_tail), _ptr(v_tail), _ptr(out),
+        _ptr(lse), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def lynx_spec_accept_workspace_bytes(B: int, k: int, vocab: int) -> int:
+    return int(load().lynx_spec_accept_workspace_bytes(B, k, vocab))
+
+
+def lynx_spec_accept_greedy(target_logits, draft_tokens, accepted, next_token,
+                            workspace_buf=None, stream=None) -> None:
+    """target_logits fp32 [B][k+1][V], draft_tokens int32 [B][k]; writes
+    accepted and next_token (int32 [B]).  workspace_buf: None allocates
+    lynx_spec_accept_workspace_bytes() bytes with torch."""
+    B, k1, V = (int(x) for x in target_logits.shape)
+    ws = workspace_buf
+    if ws is None:
+        n = lynx_spec_accept_workspace_bytes(B, k1 - 1, V)
+        ws = torch.empty(max(n, 16), dtype=torch.uint8, device=target_logits.device)
+    _check("lynx_spec_accept_greedy", load().lynx_spec_accept_greedy(
+        B, k1 - 1, V, _ptr(target_logits), _ptr(draft_tokens), _ptr(accepted), _ptr(next_token),
+        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def lynx_attn_verify(L: Layout, B: int, Hq: int, k: int, max_seq_len: int, seq_lens,

@@ -116,3 +116,33 @@ def test_validation_rejects_before_launch(lib):
     assert lib.lynx_attn_anchor_decode(ctypes.byref(lay), 0, 32, 64, None, None, None, None,
                                        ctypes.byref(meta), None, None, None, None, 0,
                                        None) == E.LYNX_OK
+
+
+def test_tail_and_acceptance_validation(lib):
+    """The decode-with-tail and greedy-acceptance entry points reject bad
+    arguments before launching anything (no pointer below is dereferenced)."""
+    from paper_2607_01831_amd import lynx
+    E = lynx
+    L = _layout()
+    lay = L.c()
+    meta = lynx.lynx_meta(16, 32, 48, 64)
+    base = (16, 16, 16, 16, ctypes.byref(meta), 16)
+    # n_tail out of range; a tail count without its tensors; half a tail
+    assert lib.lynx_attn_anchor_decode_tail(ctypes.byref(lay), 1, 32, 64, *base, 65, 16, 16, 16,
+                                            None, 16, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_attn_anchor_decode_tail(ctypes.byref(lay), 1, 32, 64, *base, 3, None, None, 16,
+                                            None, 16, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_attn_anchor_decode_tail(ctypes.byref(lay), 1, 32, 64, *base, 3, 16, None, 16,
+                                            None, 16, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_attn_anchor_decode_tail(ctypes.byref(lay), 1, 32, 64, *base, 3, 16, 16, 16,
+                                            None, None, 0, None) == E.LYNX_EWORKSPACE
+    # acceptance: workspace size, bad k / vocab, misaligned logits, short workspace
+    n = lynx.lynx_spec_accept_workspace_bytes(4, 8, 128256)
+    assert n == 4 * 9 * ((128256 + 4095) // 4096) * 8
+    assert lynx.lynx_spec_accept_workspace_bytes(4, 0, 100) == 0
+    assert lynx.lynx_spec_accept_workspace_bytes(4, 65, 100) == 0
+    assert lynx.lynx_spec_accept_workspace_bytes(4, 8, 0) == 0
+    assert lib.lynx_spec_accept_greedy(2, 0, 100, 16, 16, 16, 16, 16, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_spec_accept_greedy(2, 4, 100, 20, 16, 16, 16, 16, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_spec_accept_greedy(2, 4, 100, 16, 16, 16, 16, 16, 8, None) == E.LYNX_EWORKSPACE
+    assert lib.lynx_spec_accept_greedy(0, 4, 100, None, None, None, None, None, 0, None) == E.LYNX_OK

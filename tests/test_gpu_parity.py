@@ -371,3 +371,81 @@ def test_anchor_decode_sixteen_group_splits_ragged():
     for b, h in [(2, 7), (0, 0), (1, 15), (3, 4), (4, 9), (6, 2), (7, 11), (5, 8)]:
         mask[b, h] = 1
     _decode_check_sampled(c, q, mask, "16-group splits")
+
+
+def gpu_anchor_decode_tail(c, q, kt, vt):
+    B, Hq = c.B, q.shape[1]
+    out = torch.empty(B, Hq, 128, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(B, Hq, dtype=torch.float32, device="cuda")
+    max_len = max(c.lens)
+    ws = lynx.workspace(c.L, B, Hq, 1, max_len)
+    note(f"anchor_decode_tail B={B} Hq={Hq} n_tail={0 if kt is None else kt.shape[1]} lens={c.lens[:4]}")
+    lynx.lynx_attn_anchor_decode_tail(c.L, B, Hq, max_len, c.lens_dev(), c.table_dev(), c.pool.k_anc,
+                                      c.pool.v_anc, c.pool.meta, q.cuda(),
+                                      None if kt is None else kt.cuda(),
+                                      None if vt is None else vt.cuda(), out, lse, ws)
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy(), lse.cpu().numpy()
+
+
+@pytest.mark.parametrize("n_tail,lens,bt", [(1, [300, 0], None), (8, [1500, 37, 4000], None),
+                                            (64, [129, 700], 16), (5, [900, 0, 61], 8)])
+def test_anchor_decode_tail(n_tail, lens, bt):
+    """Anchor decode that also attends the BF16 tokens generated since the
+    context arrived (all n_tail visible); an empty context attends the tail
+    alone."""
+    Hkv, G = 2, 4
+    kv = [random_kv(T, Hkv, seed=1000 + 7 * n_tail + i) for i, T in enumerate(lens)]
+    c = build_cache([a for a, _ in kv], [b for _, b in kv], Hkv, bt=bt, seed=n_tail, merge=False)
+    B = len(lens)
+    q = random_bf16((B, Hkv * G, 128), seed=1100 + n_tail)
+    kt = random_bf16((B, n_tail, Hkv, 128), seed=1101 + n_tail)
+    vt = random_bf16((B, n_tail, Hkv, 128), seed=1102 + n_tail)
+    out, lse = gpu_anchor_decode_tail(c, q, kt, vt)
+    ref, ref_lse = oracle.anchor_decode(c.OL, Hkv * G, np.array(c.lens), c.table.numpy(),
+                                        c.planes["k_anc"], c.planes["v_anc"], c.meta, bits(q),
+                                        k_tail_bits=bits(kt), v_tail_bits=bits(vt))
+    assert_close(out, ref, what=f"decode with {n_tail}-token tail")
+    np.testing.assert_allclose(lse, ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
+
+
+def test_anchor_decode_empty_tail_matches_plain_decode():
+    Hkv, G = 2, 4
+    kv = [random_kv(T, Hkv, seed=1200 + T) for T in (333, 1024)]
+    c = build_cache([a for a, _ in kv], [b for _, b in kv], Hkv, merge=False)
+    q = random_bf16((2, Hkv * G, 128), seed=1201)
+    a, la = gpu_anchor_decode(c, q)
+    b, lb = gpu_anchor_decode_tail(c, q, None, None)
+    assert np.array_equal(a, b) and np.array_equal(la, lb)
+
+
+@pytest.mark.parametrize("B,k,V", [(4, 8, 128256), (3, 4, 1001), (37, 1, 12295), (2, 64, 4096)])
+def test_spec_accept_greedy(B, k, V):
+    """Greedy acceptance, bit-exact against the oracle: random scores with the
+    drafts copying the target's choices up to a random point, some positions
+    holding a tie between two indices (the lower one wins)."""
+    g = torch.Generator().manual_seed(B * 1000 + k + V)
+    logits = torch.randn(B, k + 1, V, generator=g)
+    choice = logits.argmax(dim=2)
+    # plant ties: a second index with the same top score, below or above the first
+    for b in range(B):
+        for i in range(k + 1):
+            if (b + i) % 3 == 0:
+                other = int(torch.randint(0, V, (1,), generator=g))
+                logits[b, i, other] = logits[b, i, choice[b, i]]
+    lg = logits.numpy()
+    choice_np = lg.argmax(axis=2)  # first index of the maximum
+    drafts = choice_np[:, :k].astype(np.int32).copy()
+    cut = torch.randint(0, k + 1, (B,), generator=g).numpy()
+    for b in range(B):
+        if cut[b] < k:
+            drafts[b, cut[b]] = (drafts[b, cut[b]] + 1) % V
+    acc = torch.empty(B, dtype=torch.int32, device="cuda")
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    note(f"spec_accept_greedy B={B} k={k} V={V}")
+    lynx.lynx_spec_accept_greedy(torch.from_numpy(lg).cuda(), torch.from_numpy(drafts).cuda(), acc, nxt)
+    torch.cuda.synchronize()
+    ref_acc, ref_nxt = oracle.accept_greedy(lg, drafts)
+    assert np.array_equal(acc.cpu().numpy(), ref_acc)
+    assert np.array_equal(nxt.cpu().numpy(), ref_nxt)
+    assert np.array_equal(ref_acc, cut)
