@@ -387,9 +387,11 @@ constexpr int kCombineThreads = 256;
 // splits and the BF16 tail tokens, normalise, round to BF16, write lse.
 // Thread (split group sg, float4 column d4) folds every 8th split into a
 // running (max, sum, output), loading 16 splits' partial outputs and (max,
-// sum) pairs together so that each step costs one round trip to memory;
-// then every 8th tail token the same way, as a partial of weight 1.  The 8
-// running triples meet in LDS.
+// sum) pairs together, then every 8th tail token the same way, as a partial
+// of weight 1.  The 8 running triples meet in LDS.  Every load the kernel
+// needs first (the first 16 splits' partials, the tail's values, and the
+// query and tail keys for the tail scores) is issued before any of them is
+// used, so the kernel waits for memory once.
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a, uint16_t *out,
                                                                        float *lse) {
     const int gr = blockIdx.x;
@@ -403,9 +405,11 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     const int n = a.tail_in_combine ? a.n_ctx_splits : a.n_splits;
     constexpr int kGroups = kCombineThreads / (kHeadDim / 4);  // 8 split groups
     constexpr int kBatch = 16;
+    constexpr int kTailMax = 64;                   // tail tokens attended at most
+    constexpr int kTailPer = kTailMax / kGroups;   // per split group
     __shared__ float4 s_acc[kGroups][kHeadDim / 4];
     __shared__ float s_m[kGroups][kHeadDim / 4], s_l[kGroups][kHeadDim / 4];
-    __shared__ float s_ts[64];  // tail scores (log2 units)
+    __shared__ float s_ts[kTailMax];  // tail scores (log2 units)
 
     // query row gr <-> (query qi, head qg); with a tail, query qi also sees
     // the BF16 tokens of the tail: drafts 0..qi in verification (causal among
@@ -414,6 +418,34 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     const int qg = gr % a.G;
     const size_t qrow = ((size_t)b * a.nq + qi) * a.Hq + (size_t)h * a.G + qg;
     const int n_tail = a.tail_in_combine ? (a.tail_count < 0 ? qi + 1 : a.tail_count) : 0;
+
+    const int d4 = tid % (kHeadDim / 4);
+    const int sg = tid / (kHeadDim / 4);
+    const float4 *o4 = reinterpret_cast<const float4 *>(a.ws_o) + base * (kHeadDim / 4) + d4;
+    // a batch of partials: splits s0, s0 + 8, ... (clamped to the last split)
+    float4 v[kBatch];
+    float2 ml[kBatch];
+    bool live[kBatch];
+    auto load_batch = [&](int s0) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int s = min(s0 + kGroups * u, n - 1);
+            v[u] = o4[(size_t)s * (kHeadDim / 4)];
+            ml[u] = a.ws_ml[base + s];
+            live[u] = s0 + kGroups * u < n;
+        }
+    };
+    load_batch(sg);
+    // this thread's tail values: tokens sg, sg + 8, ... (dims 4 d4 .. + 3)
+    uint2 tvw[kTailPer];
+    if (n_tail > 0) {
+#pragma unroll
+        for (int u = 0; u < kTailPer; ++u) {
+            const int j = min(sg + kGroups * u, n_tail - 1);
+            tvw[u] = *reinterpret_cast<const uint2 *>(
+                a.v_new + (((size_t)b * a.tail_stride + j) * Hkv + h) * kHeadDim + 4 * d4);
+        }
+    }
     if (n_tail > 0) {
         // tail scores, 16 tokens per pass: thread (token tid / 16, dims
         // 8 (tid % 16) .. + 7), summed over the 16 lanes of a token
@@ -421,17 +453,21 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
         float qv[8];
         unpack8_bf16(*reinterpret_cast<const uint4 *>(a.q + qrow * kHeadDim + 8 * piece), qv);
         const float sm = kLog2e * rsqrtf((float)kHeadDim);
-        for (int j0 = 0; j0 < n_tail; j0 += 16) {
-            const int j = j0 + (tid >> 4);
-            float d = 0.0f;
-            if (j < n_tail) {
-                float kv[8];
-                unpack8_bf16(*reinterpret_cast<const uint4 *>(
-                                 a.k_new + (((size_t)b * a.tail_stride + j) * Hkv + h) * kHeadDim + 8 * piece),
-                             kv);
+        uint4 kw[kTailMax / 16];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) d = fmaf(qv[e], kv[e], d);
-            }
+        for (int p = 0; p < kTailMax / 16; ++p) {
+            const int j = min(16 * p + (tid >> 4), n_tail - 1);
+            kw[p] = *reinterpret_cast<const uint4 *>(
+                a.k_new + (((size_t)b * a.tail_stride + j) * Hkv + h) * kHeadDim + 8 * piece);
+        }
+#pragma unroll
+        for (int p = 0; p < kTailMax / 16; ++p) {
+            const int j = 16 * p + (tid >> 4);
+            float kv[8];
+            unpack8_bf16(kw[p], kv);
+            float d = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) d = fmaf(qv[e], kv[e], d);
 #pragma unroll
             for (int off = 8; off > 0; off >>= 1) d += __shfl_xor(d, off);
             if (piece == 0 && j < n_tail) s_ts[j] = d * sm;
@@ -439,19 +475,17 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
         __syncthreads();
     }
 
-    const int d4 = tid % (kHeadDim / 4);
-    const int sg = tid / (kHeadDim / 4);
-    const float4 *o4 = reinterpret_cast<const float4 *>(a.ws_o) + base * (kHeadDim / 4) + d4;
     float m_t = -INFINITY, l_t = 0.0f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     bool nan = false;
-    // fold a batch of partials (max ml.x, sum ml.y, output v) into the running triple
-    auto fold = [&](const float4 (&v)[kBatch], float2 (&ml)[kBatch], const bool (&live)[kBatch]) {
+    // fold N partials (max mlv.x, sum mlv.y, output vv) into the running triple
+    auto fold = [&](const auto &vv, auto &mlv, const auto &lv) {
+        constexpr int N = sizeof(lv) / sizeof(lv[0]);
         float mb = m_t;
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            if (!live[u]) ml[u] = make_float2(-INFINITY, 0.0f);
-            mb = fmaxf(mb, ml[u].x);
+        for (int u = 0; u < N; ++u) {
+            if (!lv[u]) mlv[u] = make_float2(-INFINITY, 0.0f);
+            mb = fmaxf(mb, mlv[u].x);
         }
         const float sc = m_t == -INFINITY ? 0.0f : exp2f(m_t - mb);
         acc.x *= sc;
@@ -460,12 +494,12 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
         acc.w *= sc;
         l_t *= sc;
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const float e = ml[u].x == -INFINITY ? 0.0f : exp2f(ml[u].x - mb);
-            nan |= isnan(ml[u].y);
-            l_t = fmaf(ml[u].y, e, l_t);
+        for (int u = 0; u < N; ++u) {
+            const float e = mlv[u].x == -INFINITY ? 0.0f : exp2f(mlv[u].x - mb);
+            nan |= isnan(mlv[u].y);
+            l_t = fmaf(mlv[u].y, e, l_t);
             // a split with weight 0 may hold no partial output at all
-            const float4 x = e != 0.0f ? v[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 x = e != 0.0f ? vv[u] : make_float4(0.f, 0.f, 0.f, 0.f);
             acc.x = fmaf(x.x, e, acc.x);
             acc.y = fmaf(x.y, e, acc.y);
             acc.z = fmaf(x.z, e, acc.z);
@@ -474,33 +508,22 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
         m_t = mb;
     };
     for (int s0 = sg; s0 < n; s0 += kGroups * kBatch) {
-        float4 v[kBatch];
-        float2 ml[kBatch];
-        bool live[kBatch];
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int s = min(s0 + kGroups * u, n - 1);
-            v[u] = o4[(size_t)s * (kHeadDim / 4)];
-            ml[u] = a.ws_ml[base + s];
-            live[u] = s0 + kGroups * u < n;
-        }
+        if (s0 != sg) load_batch(s0);
         fold(v, ml, live);
     }
     // the tail tokens: partials (score, 1, value)
-    for (int j0 = sg; j0 < n_tail; j0 += kGroups * kBatch) {
-        float4 v[kBatch];
-        float2 ml[kBatch];
-        bool live[kBatch];
+    if (n_tail > 0) {
+        float4 tv[kTailPer];
+        float2 tml[kTailPer];
+        bool tlive[kTailPer];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int j = min(j0 + kGroups * u, n_tail - 1);
-            const uint2 vw = *reinterpret_cast<const uint2 *>(
-                a.v_new + (((size_t)b * a.tail_stride + j) * Hkv + h) * kHeadDim + 4 * d4);
-            v[u] = make_float4(bf16_lo(vw.x), bf16_hi(vw.x), bf16_lo(vw.y), bf16_hi(vw.y));
-            ml[u] = make_float2(s_ts[j], 1.0f);
-            live[u] = j0 + kGroups * u < n_tail;
+        for (int u = 0; u < kTailPer; ++u) {
+            const int j = sg + kGroups * u;
+            tlive[u] = j < n_tail;
+            tv[u] = make_float4(bf16_lo(tvw[u].x), bf16_hi(tvw[u].x), bf16_lo(tvw[u].y), bf16_hi(tvw[u].y));
+            tml[u] = make_float2(tlive[u] ? s_ts[j] : -INFINITY, 1.0f);
         }
-        fold(v, ml, live);
+        fold(tv, tml, tlive);
     }
     s_acc[sg][d4] = acc;
     s_m[sg][d4] = m_t;
