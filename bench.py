@@ -17,13 +17,16 @@ One step = the whole hot path over all 32 layers:
      plane kind over all layers                               [main stream]
   5. verification attention of the 8 drafts over the codes    [main stream]
 
-After the timed steps, four stages are timed on their own (reported under
+After the timed steps, six stages are timed on their own (reported under
 "stages"): the same decode calls with no transport running; the
 verification of k = 8 drafts at 128K context (32 q / 8 kv heads, one layer,
 merged codes + causal BF16 tail), the configuration the paper's verification
 latency is quoted for; the decode calls once more with the 8 BF16 tokens the
-speculative decoder generated; and greedy acceptance of 8 drafts over a
-128256-entry vocabulary.
+speculative decoder generated; greedy acceptance of 8 drafts over a
+128256-entry vocabulary; the batched paged decode of 16 sequences of 16K-64K
+tokens in 16-token blocks; and the 70B-shaped overlap run (4 x 128K tokens,
+64 q / 8 kv heads: 16 decode steps against the residual H2D, then merge and
+verification of 4 drafts, with the overlap fraction and end-to-end time).
 
 Printed: one JSON line.  `value` is the anchor-decode attention throughput in
 GB/s of algorithmic KV bytes (144 bytes per token per kv head) over the timed
@@ -83,6 +86,10 @@ def parse():
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     p.add_argument("--no-spec-stages", dest="spec_stages", action="store_false",
                    help="skip the decode-with-tail and draft-acceptance stages")
+    p.add_argument("--paged-calls", type=int, default=20,
+                   help="timed paged batch-decode calls (paged-b16-16k-64k; 0 skips the stage)")
+    p.add_argument("--no-overlap-70b", dest="overlap_70b", action="store_false",
+                   help="skip the 70B-shaped overlap run (70b-overlap-b4-128k)")
     p.add_argument("--verify-128k-calls", type=int, default=20,
                    help="timed verification calls at 128K context (0 skips the stage)")
     return p.parse_args()
@@ -281,6 +288,168 @@ def verify_128k(calls, dev):
             "verify_128k_frac": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
+def paged_decode_stage(calls, dev):
+    """Batched paged anchor decode (paged-b16-16k-64k): 16 sequences with
+    lengths uniform on [16384, 65536] in 16-token blocks under a random block
+    table over one pool, 32 q / 8 kv heads, one query token per sequence.  The
+    pool's anchor planes (about 755 MB) exceed the 256 MB last-level cache, so
+    every call reads them from HBM; HIP events around the timed calls."""
+    import torch
+
+    from paper_2607_01831_amd import inputs, lynx
+
+    w = inputs.WORKLOADS["paged-b16-16k-64k"]
+    lens = inputs.seq_lengths(w)
+    table, n_blocks = inputs.paged_block_table(lens, w.block_tokens,
+                                               inputs.seed_of(w.wid, inputs.T_BLOCKS))
+    L = lynx.Layout(num_kv_heads=w.Hkv, block_tokens=w.block_tokens,
+                    max_blocks_per_seq=table.shape[1], num_blocks=n_blocks, max_tokens=w.context)
+    pool = lynx.KVPool.allocate(L, w.batch, device=dev, codes=False)
+    tdev, ldev = table.to(dev), lens.to(dev)
+    for b in range(w.batch):
+        T = int(lens[b])
+        k = inputs.kv(w, "k", seq=b, T=T, device=dev)
+        v = inputs.kv(w, "v", seq=b, T=T, device=dev)
+        pool.encode(b, T, tdev, k, v)
+        del k, v
+    q = inputs.queries(w, device=dev)
+    out = torch.empty(w.batch, w.Hq, 128, dtype=torch.bfloat16, device=dev)
+    max_len = int(lens.max())
+    ws = lynx.workspace(L, w.batch, w.Hq, 1, max_len, device=dev)
+
+    def call():
+        lynx.lynx_attn_anchor_decode(L, w.batch, w.Hq, max_len, ldev, tdev, pool.k_anc, pool.v_anc,
+                                     pool.meta, q, out, None, ws)
+
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(calls):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / calls
+    nbytes = int(lens.sum()) * w.Hkv * DECODE_BYTES_PER_TOKEN_HEAD
+    gbps = nbytes / (us * 1e-6) / 1e9
+    del pool
+    return {"paged_b16_decode_us": round(us, 2), "paged_b16_decode_MB": round(nbytes / 1e6, 1),
+            "paged_b16_decode_GBps": round(gbps, 2),
+            "paged_b16_decode_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+
+
+def overlap_70b_stage(dev):
+    """The 70B-shaped overlap run (70b-overlap-b4-128k): 4 sequences x 131072
+    tokens, 64 q / 8 kv heads.  Timed with HIP events, each part alone and
+    then overlapped: 16 anchor-decode steps (a fresh query per step); the
+    H2D of the residual planes (512 MiB) from pinned host memory on a side
+    stream; both at once; then merge of both planes and verification of
+    k = 4 drafts with their causal BF16 tail.  overlap = (t_dec + t_h2d -
+    t_both) / min(t_dec, t_h2d) (1 = the shorter one fully hidden);
+    end_to_end = t_both + merge + verify."""
+    import torch
+
+    from paper_2607_01831_amd import inputs, lynx
+
+    w = inputs.WORKLOADS["70b-overlap-b4-128k"]
+    B, T, Hkv, Hq, nq, steps = w.batch, w.context, w.Hkv, w.Hq, w.drafts, w.decode_steps
+    L = lynx.contiguous_layout(Hkv, B, T)
+    pool = lynx.KVPool.allocate(L, B, device=dev)
+    table = inputs.contiguous_block_table(B).to(dev)
+    lens = torch.full((B,), T, dtype=torch.int32, device=dev)
+    for b in range(B):
+        k = inputs.kv(w, "k", seq=b, device=dev)
+        v = inputs.kv(w, "v", seq=b, device=dev)
+        pool.encode(b, T, table, k, v)
+        del k, v
+    host_k = pool.k_res.cpu().pin_memory()
+    host_v = pool.v_res.cpu().pin_memory()
+    recv_k, recv_v = torch.empty_like(pool.k_res), torch.empty_like(pool.v_res)
+    qs = [inputs.queries(w, step=s, device=dev) for s in range(steps)]
+    qv = inputs.queries(w, step=steps, nq=nq, device=dev)
+    kn, vn = inputs.drafts_kv(w, device=dev)
+    out = torch.empty(B, Hq, 128, dtype=torch.bfloat16, device=dev)
+    outv = torch.empty(B, nq, Hq, 128, dtype=torch.bfloat16, device=dev)
+    nws = max(lynx.lynx_attn_workspace_bytes(L, B, Hq, 1, T), lynx.lynx_attn_workspace_bytes(L, B, Hq, nq, T))
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    main_s, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def decode_steps():
+        for s in range(steps):
+            lynx.lynx_attn_anchor_decode(L, B, Hq, T, lens, table, pool.k_anc, pool.v_anc, pool.meta,
+                                         qs[s], out, None, ws)
+
+    def transport(after):
+        side.wait_event(after)
+        with torch.cuda.stream(side):
+            recv_k.copy_(host_k, non_blocking=True)
+            recv_v.copy_(host_v, non_blocking=True)
+            done = ev()
+            done.record(side)
+        return done
+
+    def merge_verify():
+        lynx.lynx_kv_merge(pool.k_anc, recv_k, pool.k_codes)
+        lynx.lynx_kv_merge(pool.v_anc, recv_v, pool.v_codes)
+        m = ev()
+        m.record(main_s)
+        lynx.lynx_attn_verify(L, B, Hq, nq, T, lens, table, pool.k_codes, pool.v_codes, pool.meta,
+                              qv, kn, vn, outv, ws)
+        return m
+
+    decode_steps()
+    merge_verify()
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(3):
+        # decode alone
+        a0, a1 = ev(), ev()
+        a0.record(main_s); decode_steps(); a1.record(main_s)
+        torch.cuda.synchronize()
+        # transport alone
+        h0 = ev(); h0.record(main_s)
+        h1 = transport(h0)
+        torch.cuda.synchronize()
+        # both, then merge + verify
+        b0 = ev(); b0.record(main_s)
+        hb = transport(b0)
+        decode_steps()
+        main_s.wait_event(hb)
+        b1 = ev(); b1.record(main_s)
+        m1 = merge_verify()
+        v1 = ev(); v1.record(main_s)
+        torch.cuda.synchronize()
+        r = {"t_dec": a0.elapsed_time(a1), "t_h2d": h0.elapsed_time(h1), "t_both": b0.elapsed_time(b1),
+             "merge": b1.elapsed_time(m1), "verify": m1.elapsed_time(v1), "e2e": b0.elapsed_time(v1)}
+        if best is None or r["e2e"] < best["e2e"]:
+            best = r
+    t_dec, t_h2d, t_both = best["t_dec"], best["t_h2d"], best["t_both"]
+    dec_bytes = B * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
+    res_bytes = host_k.numel() + host_v.numel()
+    merge_bytes = 2 * B * T * Hkv * 128 * MERGE_BYTES_PER_ELEM
+    ver_bytes = B * T * Hkv * VERIFY_BYTES_PER_TOKEN_HEAD
+    us_step = t_dec * 1e3 / steps
+    r = {
+        "decode_us_per_step": round(us_step, 2),
+        "decode_GBps": round(dec_bytes / (us_step * 1e-6) / 1e9, 2),
+        "decode_frac": round(dec_bytes / (us_step * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+        "decode_16_steps_us": round(t_dec * 1e3, 1),
+        "h2d_us": round(t_h2d * 1e3, 1),
+        "h2d_GBps": round(res_bytes / (t_h2d * 1e-3) / 1e9, 2),
+        "both_us": round(t_both * 1e3, 1),
+        "overlap": round(max(0.0, min(1.0, (t_dec + t_h2d - t_both) / min(t_dec, t_h2d))), 3),
+        "merge_us": round(best["merge"] * 1e3, 1),
+        "merge_GBps": round(merge_bytes / (best["merge"] * 1e-3) / 1e9, 2),
+        "verify_k4_us": round(best["verify"] * 1e3, 1),
+        "verify_k4_GBps": round(ver_bytes / (best["verify"] * 1e-3) / 1e9, 2),
+        "end_to_end_us": round(best["e2e"] * 1e3, 1),
+    }
+    del pool, host_k, host_v
+    return {"overlap_70b_b4_128k": r}
+
+
 def cpu_baseline(w, layer_inputs, n_layers):
     """The CPU oracle, untuned, timed on this host on a bounded sample: the
     anchor decode of the first n_layers layers (all kv heads)."""
@@ -439,6 +608,8 @@ def main():
     t_dec_alone = e0.elapsed_time(e1) / args.steps
 
     ver128 = verify_128k(args.verify_128k_calls, dev) if args.verify_128k_calls > 0 else None
+    paged = paged_decode_stage(args.paged_calls, dev) if args.paged_calls > 0 else None
+    ovl = overlap_70b_stage(dev) if args.overlap_70b else None
 
     # The speculative decoder's own pieces, timed alone: decode over the
     # anchors plus the 8 BF16 tokens it generated (32 layers), and greedy
@@ -527,6 +698,8 @@ def main():
             "verify_GBps": round(ver_gbps, 2),
             "residual_h2d_GBps": round(h2d_gbps, 2),
             **(ver128 or {}),
+            **(paged or {}),
+            **(ovl or {}),
             **spec,
             "decode_hidden_behind_h2d": round(overlap, 3),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),

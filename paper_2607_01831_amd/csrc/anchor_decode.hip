@@ -105,9 +105,14 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     constexpr int kMaxGroups = NG / kWaves;  // groups per wavefront
     static_assert(NG % kWaves == 0, "groups must split evenly over the wavefronts");
     const int Hkv = a.geo.Hkv;
-    const int split = blockIdx.x;
-    const int h = blockIdx.y % Hkv;
-    const int chunk = blockIdx.y / Hkv;
+    // Grid (split, kv head x chunk, sequence) for the contiguous layout.  A
+    // paged block holds the rows of every kv head for its tokens side by side,
+    // so paged layouts make the kv head the fastest grid index: workgroups
+    // reading the same blocks run together and share DRAM pages.
+    const int split = LAYOUT == 0 ? blockIdx.x : blockIdx.y;
+    const int hc = LAYOUT == 0 ? blockIdx.y : blockIdx.x;
+    const int h = hc % Hkv;
+    const int chunk = hc / Hkv;
     const int b = blockIdx.z;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -575,7 +580,10 @@ void launch_groups(const DecodeArgs &args, dim3 grid, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_anchor_decode_mfma(const DecodeArgs &args, int chunks, hipStream_t stream) {
-    dim3 grid(args.n_splits, args.geo.Hkv * chunks, args.B);
+    // kv head fastest for paged layouts (the kernel reads the grid the same way)
+    if (args.geo.max_blocks != 1 && args.n_splits > 65535) return hipErrorInvalidValue;
+    const unsigned hc = (unsigned)(args.geo.Hkv * chunks);
+    const dim3 grid = args.geo.max_blocks == 1 ? dim3(args.n_splits, hc, args.B) : dim3(hc, args.n_splits, args.B);
     if (args.groups_per_split == 4) {
         launch_groups<4>(args, grid, stream);
     } else if (args.groups_per_split == 8) {

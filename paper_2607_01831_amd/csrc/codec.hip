@@ -130,8 +130,8 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     const uint16_t *__restrict__ k, const uint16_t *__restrict__ v, uint8_t *__restrict__ k_anc,
     uint8_t *__restrict__ v_anc, uint8_t *__restrict__ k_res, uint8_t *__restrict__ v_res,
     MetaPtrs meta) {
-    const int g = blockIdx.x;
-    const int h = blockIdx.y;
+    const int g = blockIdx.y;
+    const int h = blockIdx.x;
     const int tid = threadIdx.x;
     const int m = tid & 15;
     const int tr = tid >> 4;
@@ -331,7 +331,7 @@ hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_t
                          const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
                          uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream) {
     if (T <= 0) return hipSuccess;
-    dim3 grid((T + kKGroup - 1) / kKGroup, g.Hkv);
+    dim3 grid(g.Hkv, (T + kKGroup - 1) / kKGroup);
     int bt_shift = -1;
     for (int sh = 0; sh < 31; ++sh)
         if ((1 << sh) == g.bt) bt_shift = sh;

@@ -125,9 +125,14 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
     constexpr int kMaxGroups = SG / NQ;    // groups per wavefront
     static_assert(SG % NQ == 0, "groups must split evenly over the wavefronts");
     const int Hkv = a.geo.Hkv;
-    const int split = blockIdx.x;
-    const int h = blockIdx.y % Hkv;
-    const int chunk = blockIdx.y / Hkv;
+    // Grid (split, kv head x chunk, sequence) for the contiguous layout.  A
+    // paged block holds the rows of every kv head for its tokens side by side,
+    // so paged layouts make the kv head the fastest grid index: workgroups
+    // reading the same blocks run together and share DRAM pages.
+    const int split = LAYOUT == 0 ? blockIdx.x : blockIdx.y;
+    const int hc = LAYOUT == 0 ? blockIdx.y : blockIdx.x;
+    const int h = hc % Hkv;
+    const int chunk = hc / Hkv;
     const int b = blockIdx.z;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -646,7 +651,10 @@ hipError_t launch_verify_mfma(const VerifyArgs &args, int split_groups, hipStrea
     if (args.rows_total < 1) return hipErrorInvalidValue;
     const int rt = args.rows_total <= 16 ? 1 : 2;
     const int chunks = (args.rows_total + 16 * rt - 1) / (16 * rt);
-    dim3 grid(args.n_ctx_splits, args.geo.Hkv * chunks, args.B);
+    // kv head fastest for paged layouts (the kernel reads the grid the same way)
+    if (args.geo.max_blocks != 1 && args.n_ctx_splits > 65535) return hipErrorInvalidValue;
+    const unsigned hc = (unsigned)(args.geo.Hkv * chunks);
+    const dim3 grid = args.geo.max_blocks == 1 ? dim3(args.n_ctx_splits, hc, args.B) : dim3(hc, args.n_ctx_splits, args.B);
     if (rt == 1)
         launch_layout<1>(args, split_groups, grid, stream);
     else
