@@ -182,6 +182,24 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     // copies per tile: 2 K + 2 V + 1 V metadata, + 1 K metadata (into the
     // wavefront's K-metadata buffer) for a group's first tile
 
+    // LAYOUT 1: the block of every 16-token run the wavefront attends (lane
+    // 8 u + r: run r of its group u), looked up once before any copy is in
+    // flight; a full tile's copies then take their blocks by readlane
+    // instead of waiting on a block-table load each.  Lanes past the
+    // wavefront's groups read a clamped, unused entry.
+    int run_blk = 0;
+    if (LAYOUT == 1) {
+        const int u = lane >> 3;
+        if (u < kMaxGroups) {
+            const int tr = (g0 + w + kWaves * u) * kKGroup + 16 * (lane & 7);
+            const int bi = a.bt_shift >= 0 ? (tr >> a.bt_shift) : tr / a.geo.bt;
+            run_blk = bt_row[min(bi, a.geo.max_blocks - 1)];
+        }
+        // the compiler places its wait for the load before this use: ahead of
+        // every copy, whose waits it does not see
+        asm volatile("" : "+v"(run_blk));
+    }
+
     // Tile j of this wavefront into ring slot j % kDepth.
     auto issue_tile = [&](int j) {
         const int t0 = __builtin_amdgcn_readfirstlane(tile_t0(j));
@@ -196,7 +214,8 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
                 } else {
                     const int tr = t0 + 16 * i;
                     const int bi = a.bt_shift >= 0 ? (tr >> a.bt_shift) : tr / a.geo.bt;
-                    int blk = bt_row[bi];
+                    // run 2 (j % 4) + i of the wavefront's group j / 4
+                    int blk = __builtin_amdgcn_readlane(run_blk, 8 * (j >> 2) + 2 * (j & 3) + i);
                     if (blk < 0 || blk >= a.geo.num_blocks) {
                         bad = true;
                         blk = 0;
