@@ -213,9 +213,23 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
         // clamp keeps 2^-Ev, and so the weights p 2^-Ev, finite
         Ev = max(Ev, -100);
     }
-    // every plain load has been consumed (Ev depends on all of them): nothing
-    // of the compiler's own is in flight once the copies start
-    asm volatile("" ::"v"(Ev) : "memory");
+    // LAYOUT 1: the block of every 16-token run the wavefront attends (lane
+    // 8 u + r: run r of its group u), looked up here so that a full tile's
+    // copies take their blocks by readlane instead of waiting on a
+    // block-table load each.  Lanes past the wavefront's groups read a
+    // clamped, unused entry.
+    int run_blk = 0;
+    if (LAYOUT == 1) {
+        const int u = lane >> 3;
+        if (u < kMaxGroups) {
+            const int tr = (g0 + gq + NQ * u) * kKGroup + 16 * (lane & 7);
+            const int bi = a.bt_shift >= 0 ? (tr >> a.bt_shift) : tr / a.geo.bt;
+            run_blk = bt_row[min(bi, a.geo.max_blocks - 1)];
+        }
+    }
+    // every plain load has been consumed (Ev and run_blk depend on all of
+    // them): nothing of the compiler's own is in flight once the copies start
+    asm volatile("" ::"v"(Ev), "v"(run_blk) : "memory");
     wait_vmcnt<0>();
 
     // ---- copies into the ring ----
@@ -243,7 +257,8 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
                 } else {
                     const int tr = t0 + 16 * run;
                     const int bi = a.bt_shift >= 0 ? (tr >> a.bt_shift) : tr / a.geo.bt;
-                    int blk = bt_row[bi];
+                    // run 2 (j % 4) + run of the wavefront's group j / 4
+                    int blk = __builtin_amdgcn_readlane(run_blk, 8 * (j >> 2) + 2 * (j & 3) + run);
                     if (blk < 0 || blk >= a.geo.num_blocks) {
                         bad = true;
                         blk = 0;
