@@ -8,6 +8,9 @@ its Python binding) never imports, links or runs it, and this package imports
 nothing from the product.
 
 Arrays are numpy.  BF16 tensors travel as their raw uint16 bit patterns.
+The serializer / deserializer of Sec. 4.2 and Sec. 5 (transmission buffers of
+one KV object, and their scatter into the pages) is byte layout written here
+in numpy over the C encode and merge.
 """
 from __future__ import annotations
 
@@ -266,3 +269,114 @@ def encode_batch(L: Layout, seq_lens, block_table, k_list, v_list, n_blocks: int
     for b in range(B):
         encode(L, b, int(seq_lens[b]), block_table, k_list[b], v_list[b], planes, meta)
     return planes, meta
+
+
+# --------------------------------------------------------------------------
+# Serializer / deserializer (Sec. 4.2 Prioritized Transmission; Sec. 5
+# Compression Kernel).  The serializer quantizes one KV object and writes the
+# packed Anchor stream followed immediately by the shared scalars into one
+# contiguous transmission buffer, and the Residual stream into another; the
+# deserializer scatters a received Anchor buffer into the KV pages (Anchor
+# phase) and later combines a received Residual buffer with the Anchors in
+# the pages into the full 8-bit codes (Residual phase).
+#
+# Object: tokens [t0, t0 + n) of one sequence (one layer), all kv heads, with
+# t0 a multiple of the 128-token K group so that its K groups are the
+# sequence's.  Byte layout of the buffers (each section follows the previous
+# one with no padding):
+#   anchor:   K anchor rows [Hkv][n][64], V anchor rows [Hkv][n][64],
+#             K scales, K zeros  fp32 [Hkv][ceil(n/128)][128],
+#             V scales, V zeros  fp32 [Hkv][n]
+#   residual: K residual rows [Hkv][n][64], V residual rows [Hkv][n][64]
+# --------------------------------------------------------------------------
+
+def serialized_sections(Hkv: int, n: int) -> dict:
+    """Byte (offset, size) of every section of an object's buffers, and the
+    two totals ('anchor_bytes', 'residual_bytes')."""
+    g = -(-n // K_GROUP)
+    rows = Hkv * n * 64
+    kmeta = Hkv * g * HEAD_DIM * 4
+    vmeta = Hkv * n * 4
+    sizes = [("k_anc", rows), ("v_anc", rows), ("k_scale", kmeta), ("k_zero", kmeta),
+             ("v_scale", vmeta), ("v_zero", vmeta)]
+    out, off = {}, 0
+    for name, size in sizes:
+        out[name] = (off, size)
+        off += size
+    out["anchor_bytes"] = off
+    out["k_res"] = (0, rows)
+    out["v_res"] = (rows, rows)
+    out["residual_bytes"] = 2 * rows
+    return out
+
+
+def serialize(Hkv: int, n: int, k_bits: np.ndarray, v_bits: np.ndarray):
+    """Quantize an object (k_bits, v_bits: uint16 [n][Hkv][128], the tokens
+    t0..t0+n-1 of a sequence) into its (anchor, residual) transmission
+    buffers (uint8).  The object is encoded as a sequence of its own in a
+    one-block cache, whose planes [Hkv][n][64] and metadata rows are exactly
+    the sections of the buffers."""
+    OL = Layout(Hkv=Hkv, bt=n, max_blocks=1, max_tokens=n)
+    nbytes = plane_bytes(OL, 1, 64)
+    planes = {name: np.zeros(nbytes, np.uint8) for name in ("k_anc", "v_anc", "k_res", "v_res")}
+    meta = Meta.empty(OL, 1)
+    encode(OL, 0, n, np.zeros((1, 1), np.int32), k_bits, v_bits, planes, meta)
+    sec = serialized_sections(Hkv, n)
+    anc = np.concatenate([planes["k_anc"], planes["v_anc"],
+                          meta.k_scale.reshape(-1).view(np.uint8), meta.k_zero.reshape(-1).view(np.uint8),
+                          meta.v_scale.reshape(-1).view(np.uint8), meta.v_zero.reshape(-1).view(np.uint8)])
+    res = np.concatenate([planes["k_res"], planes["v_res"]])
+    assert anc.size == sec["anchor_bytes"] and res.size == sec["residual_bytes"]
+    return anc, res
+
+
+def token_rows(L: Layout, block_table: np.ndarray, b: int, t0: int, n: int) -> np.ndarray:
+    """Row index [Hkv][n] of (b, h, t0 + i) in the planes: the plane
+    addressing ((block_table[b][t / bt] * Hkv + h) * bt + t % bt)."""
+    t = t0 + np.arange(n)
+    blk = np.asarray(block_table, dtype=np.int64)[b, t // L.bt]
+    h = np.arange(L.Hkv)[:, None]
+    return (blk[None, :] * L.Hkv + h) * L.bt + (t % L.bt)[None, :]
+
+
+def deserialize_anchor(L: Layout, b: int, t0: int, n: int, block_table: np.ndarray,
+                       anc_buf: np.ndarray, planes: dict, meta: Meta) -> None:
+    """Anchor phase: scatter an object's anchor buffer into the anchor planes
+    (planes['k_anc'|'v_anc'], flat uint8) and metadata row b of sequence b."""
+    assert t0 % K_GROUP == 0 and t0 + n <= L.max_tokens
+    sec = serialized_sections(L.Hkv, n)
+    buf = np.asarray(anc_buf, dtype=np.uint8)
+    assert buf.size == sec["anchor_bytes"]
+    cols = np.arange(64)
+    dst = (token_rows(L, block_table, b, t0, n) * 64)[:, :, None] + cols
+    for name in ("k_anc", "v_anc"):
+        off, size = sec[name]
+        planes[name][dst] = buf[off:off + size].reshape(L.Hkv, n, 64)
+    g = -(-n // K_GROUP)
+    g0 = t0 // K_GROUP
+    for name, arr in (("k_scale", meta.k_scale), ("k_zero", meta.k_zero)):
+        off, size = sec[name]
+        arr[b, :, g0:g0 + g, :] = buf[off:off + size].view(np.float32).reshape(L.Hkv, g, HEAD_DIM)
+    for name, arr in (("v_scale", meta.v_scale), ("v_zero", meta.v_zero)):
+        off, size = sec[name]
+        arr[b, :, t0:t0 + n] = buf[off:off + size].view(np.float32).reshape(L.Hkv, n)
+
+
+def deserialize_residual(L: Layout, b: int, t0: int, n: int, block_table: np.ndarray,
+                         res_buf: np.ndarray, planes: dict, codes: dict) -> None:
+    """Residual phase: combine an object's residual buffer with its anchor
+    rows already in the pages (planes['k_anc'|'v_anc']) into the code planes
+    (codes['k_codes'|'v_codes'], flat uint8, 128-byte rows) by the merge
+    definition."""
+    assert t0 % K_GROUP == 0 and t0 + n <= L.max_tokens
+    sec = serialized_sections(L.Hkv, n)
+    buf = np.asarray(res_buf, dtype=np.uint8)
+    assert buf.size == sec["residual_bytes"]
+    rows = token_rows(L, block_table, b, t0, n)
+    src = (rows * 64)[:, :, None] + np.arange(64)
+    dst = (rows * 128)[:, :, None] + np.arange(128)
+    for anc_name, res_name, code_name in (("k_anc", "k_res", "k_codes"), ("v_anc", "v_res", "v_codes")):
+        off, size = sec[res_name]
+        anc = planes[anc_name][src].reshape(-1)
+        res = buf[off:off + size]
+        codes[code_name][dst] = merge(anc, res).reshape(L.Hkv, n, 128)
