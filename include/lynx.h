@@ -237,6 +237,76 @@ int lynx_spec_accept_greedy(int32_t B, int32_t k, int32_t vocab, const float *ta
                             int32_t *next_token, void *workspace, size_t workspace_bytes,
                             void *stream);
 
+/*
+ * Serializer / deserializer (Sec. 4.2 Prioritized Transmission; Sec. 5
+ * Compression Kernel).  A KV object is tokens [t0, t0 + n) of one sequence
+ * (one layer), all kv heads, with t0 a multiple of 128 so that its K groups
+ * are the sequence's.  Its two contiguous transmission buffers, each section
+ * directly after the previous one:
+ *   anchor buffer:   K anchor rows [Hkv][n][64] bytes, V anchor rows
+ *                    [Hkv][n][64], then the shared scalars: K scales and K
+ *                    zeros fp32 [Hkv][ceil(n/128)][128], V scales and V zeros
+ *                    fp32 [Hkv][n]  (Hkv * (136 n + 1024 ceil(n/128)) bytes)
+ *   residual buffer: K residual rows [Hkv][n][64], V residual rows
+ *                    [Hkv][n][64]  (128 Hkv n bytes)
+ * Rows and scalars are those lynx_kv_encode gives the same tokens of the
+ * sequence, so serialize + deserialize_anchor reproduces its planes and
+ * metadata, and deserialize_residual its merged codes.
+ */
+
+/* Byte sizes of an object's anchor and residual buffers (host call; no
+ * launch).  Returns LYNX_EINVAL for num_kv_heads < 1, n_tokens < 1 or a NULL
+ * output pointer. */
+int lynx_serialized_bytes(int32_t num_kv_heads, int32_t n_tokens, size_t *anchor_bytes,
+                          size_t *residual_bytes);
+
+/*
+ * lynx_kv_serialize -- the prefill side: quantize one object straight into
+ * its transmission buffers (the anchor stream followed by its scalars; the
+ * residual stream in the other buffer).
+ *   k_bf16, v_bf16  BF16 [n][Hkv][128] (device, read): the object's tokens,
+ *                   i.e. a sequence's K, V advanced by t0 token rows
+ *   anchor_buf, residual_buf  lynx_serialized_bytes() bytes each (device,
+ *                   written, 16-byte aligned, not overlapping)
+ * Launches one kernel.
+ */
+int lynx_kv_serialize(int32_t num_kv_heads, int32_t n_tokens, const void *k_bf16,
+                      const void *v_bf16, void *anchor_buf, void *residual_buf, void *stream);
+
+/*
+ * lynx_kv_deserialize_anchor -- the decode side's Anchor phase: scatter a
+ * received anchor buffer into the anchor planes of the pool (rows of tokens
+ * t0 .. t0 + n - 1 of sequence b, through block_table row b) and into
+ * metadata row b.
+ *   L, block_table, k_anc, v_anc, meta  as for lynx_kv_encode
+ *   t0           first token; a multiple of 128; t0 + n_tokens must not
+ *                exceed min(max_tokens, max_blocks_per_seq * bt)
+ *   anchor_buf   the object's anchor buffer (device, read, 16-byte aligned)
+ * Rows whose block id is outside [0, num_blocks) are skipped.  Launches one
+ * kernel.
+ */
+int lynx_kv_deserialize_anchor(const lynx_layout *L, int32_t b, int32_t t0, int32_t n_tokens,
+                               const int32_t *block_table, const void *anchor_buf,
+                               uint8_t *k_anc, uint8_t *v_anc, const lynx_meta *meta,
+                               void *stream);
+
+/*
+ * lynx_kv_deserialize_residual -- the decode side's Residual phase for one
+ * object: its received residual buffer and its anchor rows already in the
+ * pool (a prior lynx_kv_deserialize_anchor on the same stream, or an encode)
+ * merge into the code planes of the pool (128-byte rows, same block ids):
+ * the lynx_kv_merge rule per byte.
+ *   residual_buf  the object's residual buffer (device, read, 16-byte aligned)
+ *   k_anc, v_anc  anchor planes (device, read); k_codes, v_codes code planes
+ *                 (device, written)
+ * Same t0 / n_tokens rules and skipped rows as the anchor phase.  Launches
+ * one kernel.
+ */
+int lynx_kv_deserialize_residual(const lynx_layout *L, int32_t b, int32_t t0, int32_t n_tokens,
+                                 const int32_t *block_table, const void *residual_buf,
+                                 const uint8_t *k_anc, const uint8_t *v_anc, uint8_t *k_codes,
+                                 uint8_t *v_codes, void *stream);
+
 /* Static, human-readable text for a lynx_status value. */
 const char *lynx_strerror(int status);
 

@@ -223,3 +223,83 @@ int lynx_spec_accept_greedy(int32_t B, int32_t k, int32_t vocab, const float *ta
 }
 
 }  // extern "C"
+
+namespace {
+// Checks shared by the two deserializer phases.
+int check_object(const lynx_layout *L, int32_t b, int32_t t0, int32_t n, const int32_t *block_table,
+                 Geometry *g) {
+    int rc = check_layout(L, g);
+    if (rc != LYNX_OK) return rc;
+    if (b < 0 || t0 < 0 || n < 1 || t0 % lynx::kKGroup != 0) return LYNX_EINVAL;
+    if ((long long)t0 + n > layout_capacity(*g)) return LYNX_EINVAL;
+    if (!block_table || !aligned16(block_table)) return LYNX_EINVAL;
+    return LYNX_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int lynx_serialized_bytes(int32_t num_kv_heads, int32_t n_tokens, size_t *anchor_bytes,
+                          size_t *residual_bytes) {
+    if (num_kv_heads < 1 || n_tokens < 1 || !anchor_bytes || !residual_bytes) return LYNX_EINVAL;
+    const size_t H = (size_t)num_kv_heads, n = (size_t)n_tokens;
+    const size_t g = (n + lynx::kKGroup - 1) / lynx::kKGroup;
+    *anchor_bytes = H * (2 * n * lynx::kNibbleRow + 2 * g * lynx::kHeadDim * 4 + 2 * n * 4);
+    *residual_bytes = H * 2 * n * lynx::kNibbleRow;
+    return LYNX_OK;
+}
+
+int lynx_kv_serialize(int32_t num_kv_heads, int32_t n_tokens, const void *k_bf16,
+                      const void *v_bf16, void *anchor_buf, void *residual_buf, void *stream) {
+    size_t na, nr;
+    if (lynx_serialized_bytes(num_kv_heads, n_tokens, &na, &nr) != LYNX_OK) return LYNX_EINVAL;
+    const void *ptrs[] = {k_bf16, v_bf16, anchor_buf, residual_buf};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(anchor_buf), a1 = a0 + na;
+    const uintptr_t r0 = reinterpret_cast<uintptr_t>(residual_buf), r1 = r0 + nr;
+    if (a0 < r1 && r0 < a1) return LYNX_EINVAL;
+    hipError_t e = lynx::launch_serialize(num_kv_heads, n_tokens,
+                                          static_cast<const uint16_t *>(k_bf16),
+                                          static_cast<const uint16_t *>(v_bf16),
+                                          static_cast<uint8_t *>(anchor_buf),
+                                          static_cast<uint8_t *>(residual_buf),
+                                          static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_kv_deserialize_anchor(const lynx_layout *L, int32_t b, int32_t t0, int32_t n_tokens,
+                               const int32_t *block_table, const void *anchor_buf,
+                               uint8_t *k_anc, uint8_t *v_anc, const lynx_meta *meta,
+                               void *stream) {
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_object(L, b, t0, n_tokens, block_table, &g);
+    if (rc != LYNX_OK) return rc;
+    if ((rc = check_meta(meta, &mp)) != LYNX_OK) return rc;
+    const void *ptrs[] = {anchor_buf, k_anc, v_anc};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    hipError_t e = lynx::launch_deserialize_anchor(g, b, t0, n_tokens, block_table,
+                                                   static_cast<const uint8_t *>(anchor_buf), k_anc,
+                                                   v_anc, mp, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_kv_deserialize_residual(const lynx_layout *L, int32_t b, int32_t t0, int32_t n_tokens,
+                                 const int32_t *block_table, const void *residual_buf,
+                                 const uint8_t *k_anc, const uint8_t *v_anc, uint8_t *k_codes,
+                                 uint8_t *v_codes, void *stream) {
+    Geometry g;
+    int rc = check_object(L, b, t0, n_tokens, block_table, &g);
+    if (rc != LYNX_OK) return rc;
+    const void *ptrs[] = {residual_buf, k_anc, v_anc, k_codes, v_codes};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    hipError_t e = lynx::launch_deserialize_residual(
+        g, b, t0, n_tokens, block_table, static_cast<const uint8_t *>(residual_buf), k_anc, v_anc,
+        k_codes, v_codes, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+}  // extern "C"

@@ -1,5 +1,6 @@
-// Split-stream KV codec kernels for gfx950: encode (quantize, split, pack)
-// and merge (anchor + residual -> 8-bit codes).
+// Split-stream KV codec kernels for gfx950: encode (quantize, split, pack),
+// merge (anchor + residual -> 8-bit codes), and the deserializer's scatter of
+// transmission buffers into the pages (Sec. 4.2 Anchor and Residual phases).
 //
 // Encode follows the grouped linear quantization of Sec. 2.3 (zero = group
 // minimum, scale = range / 255) and the split-stream construction of Alg. 1
@@ -123,7 +124,8 @@ __device__ __forceinline__ void quantize_split8(const float *x, const float *zer
 // Thread (tr = tid / 16, m = tid % 16) owns dims 8m..8m+7 of the window's
 // tokens tr, tr+16, ..., tr+112: every 16-byte load is part of a fully used
 // 256-byte token row, and a token's 16 owners are the 16 lanes of one DPP
-// row.  LAYOUT 0: one block per sequence; 1: paged.
+// row.  LAYOUT 0: one block per sequence; 1: paged; 2: a transmission-buffer
+// object (planes [Hkv][T][64], no block table).
 template <int LAYOUT>
 __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
@@ -159,7 +161,10 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
     auto plane_row = [&](int t, bool &ok) -> size_t {
         int blk, tb;
-        if (LAYOUT == 0) {
+        if (LAYOUT == 2) {
+            blk = 0;
+            tb = t;
+        } else if (LAYOUT == 0) {
             blk = bt_row[0];
             tb = t;
         } else {
@@ -325,6 +330,114 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     }
 }
 
+constexpr int kCopyThreads = 256;
+
+// Row index of (sequence b, kv head h, token t) in a plane pool, or -1 when
+// the block table names no valid block (such rows are skipped, as encode
+// skips them).
+__device__ __forceinline__ long long pool_row(const Geometry &g, const int32_t *bt_row, int bt_shift,
+                                              int h, int t) {
+    const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / g.bt;
+    const int blk = bt_row[bi];
+    if (blk < 0 || blk >= g.num_blocks) return -1;
+    return ((long long)blk * g.Hkv + h) * g.bt + (t - bi * g.bt);
+}
+
+// Anchor phase of the deserializer: the anchor buffer of the object (tokens
+// t0 .. t0 + n - 1 of sequence b) is scattered into the pages.  Part
+// blockIdx.y: 0 = K and V anchor rows (16 bytes per thread), 1 = K scales
+// and zeros (float4 per thread), 2 = V scales and zeros (one float each).
+__global__ __launch_bounds__(kCopyThreads) void deserialize_anchor_kernel(
+    Geometry g, int b, int t0, int n, int bt_shift, const int32_t *__restrict__ block_table,
+    const uint8_t *__restrict__ buf, uint8_t *__restrict__ k_anc, uint8_t *__restrict__ v_anc,
+    MetaPtrs meta) {
+    const int32_t *bt_row = block_table + (size_t)b * g.max_blocks;
+    const size_t rows = (size_t)g.Hkv * n;
+    const size_t rows_bytes = rows * kNibbleRow;
+    const int ng = (n + kKGroup - 1) / kKGroup;
+    const size_t kmeta = (size_t)g.Hkv * ng * kHeadDim;  // floats per K metadata section
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (blockIdx.y == 0) {
+        for (size_t e = i0; e < 2 * rows * 4; e += stride) {
+            const size_t which = e / (rows * 4);  // 0: K, 1: V
+            const size_t r = (e / 4) % rows;
+            const int q = (int)(e & 3);
+            const int h = (int)(r / n), i = (int)(r % n);
+            const long long pr = pool_row(g, bt_row, bt_shift, h, t0 + i);
+            if (pr < 0) continue;
+            const uint4 x = *reinterpret_cast<const uint4 *>(buf + which * rows_bytes + r * kNibbleRow + 16 * q);
+            uint8_t *plane = which == 0 ? k_anc : v_anc;
+            *reinterpret_cast<uint4 *>(plane + (size_t)pr * kNibbleRow + 16 * q) = x;
+        }
+    } else if (blockIdx.y == 1) {
+        const float *src = reinterpret_cast<const float *>(buf + 2 * rows_bytes);
+        for (size_t e = i0; e < 2 * kmeta / 4; e += stride) {
+            const size_t which = e / (kmeta / 4);  // 0: scales, 1: zeros
+            const size_t f = 4 * (e % (kmeta / 4));
+            const int h = (int)(f / ((size_t)ng * kHeadDim));
+            const size_t rem = f % ((size_t)ng * kHeadDim);
+            const float4 x = *reinterpret_cast<const float4 *>(src + which * kmeta + f);
+            float *dst = which == 0 ? meta.k_scale : meta.k_zero;
+            const size_t gi = (((size_t)b * g.Hkv + h) * g.n_groups + t0 / kKGroup) * kHeadDim + rem;
+            *reinterpret_cast<float4 *>(dst + gi) = x;
+        }
+    } else {
+        const float *src = reinterpret_cast<const float *>(buf + 2 * rows_bytes) + 2 * kmeta;
+        for (size_t e = i0; e < 2 * rows; e += stride) {
+            const size_t which = e / rows;  // 0: scales, 1: zeros
+            const size_t r = e % rows;
+            const int h = (int)(r / n), i = (int)(r % n);
+            float *dst = which == 0 ? meta.v_scale : meta.v_zero;
+            dst[((size_t)b * g.Hkv + h) * g.max_tokens + t0 + i] = src[which * rows + r];
+        }
+    }
+}
+
+// Residual phase of the deserializer: the residual buffer of the object and
+// its anchor rows already in the pages merge into the code rows of the
+// pages (16 anchor + 16 residual bytes -> 32 code bytes per thread).
+__global__ __launch_bounds__(kCopyThreads) void deserialize_residual_kernel(
+    Geometry g, int b, int t0, int n, int bt_shift, const int32_t *__restrict__ block_table,
+    const uint8_t *__restrict__ buf, const uint8_t *__restrict__ k_anc,
+    const uint8_t *__restrict__ v_anc, uint8_t *__restrict__ k_codes, uint8_t *__restrict__ v_codes) {
+    const int32_t *bt_row = block_table + (size_t)b * g.max_blocks;
+    const size_t rows = (size_t)g.Hkv * n;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * rows * 4; e += stride) {
+        const size_t which = e / (rows * 4);
+        const size_t r = (e / 4) % rows;
+        const int q = (int)(e & 3);
+        const int h = (int)(r / n), i = (int)(r % n);
+        const long long pr = pool_row(g, bt_row, bt_shift, h, t0 + i);
+        if (pr < 0) continue;
+        const uint4 a = *reinterpret_cast<const uint4 *>((which == 0 ? k_anc : v_anc) +
+                                                         (size_t)pr * kNibbleRow + 16 * q);
+        const uint4 x = *reinterpret_cast<const uint4 *>(buf + which * rows * kNibbleRow +
+                                                         r * kNibbleRow + 16 * q);
+        const uint2 c0 = merge4(a.x, x.x);
+        const uint2 c1 = merge4(a.y, x.y);
+        const uint2 c2 = merge4(a.z, x.z);
+        const uint2 c3 = merge4(a.w, x.w);
+        uint4 *dst = reinterpret_cast<uint4 *>((which == 0 ? k_codes : v_codes) +
+                                               (size_t)pr * kCodeRow + 32 * q);
+        dst[0] = make_uint4(c0.x, c0.y, c1.x, c1.y);
+        dst[1] = make_uint4(c2.x, c2.y, c3.x, c3.y);
+    }
+}
+
+int bt_shift_of(int bt) {
+    for (int sh = 0; sh < 31; ++sh)
+        if ((1 << sh) == bt) return sh;
+    return -1;
+}
+
+unsigned copy_blocks(size_t work) {
+    size_t blocks = (work + kCopyThreads - 1) / kCopyThreads;
+    if (blocks > 256 * 32) blocks = 256 * 32;
+    return (unsigned)(blocks == 0 ? 1 : blocks);
+}
+
 }  // namespace
 
 hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_table,
@@ -356,6 +469,52 @@ hipError_t launch_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, 
     hipLaunchKernelGGL(merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, stream,
                        reinterpret_cast<const uint4 *>(anc), reinterpret_cast<const uint4 *>(res),
                        reinterpret_cast<uint4 *>(codes), n16, anc, res, codes, n_packed);
+    return hipGetLastError();
+}
+
+hipError_t launch_serialize(int Hkv, int n, const uint16_t *k, const uint16_t *v,
+                            uint8_t *anc_buf, uint8_t *res_buf, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    // the object as a one-block cache of its own: its planes and metadata
+    // rows are the sections of the two buffers
+    Geometry g;
+    g.Hkv = Hkv;
+    g.bt = n;
+    g.max_blocks = 1;
+    g.num_blocks = 1;
+    g.max_tokens = n;
+    g.n_groups = (n + kKGroup - 1) / kKGroup;
+    const size_t rows_bytes = (size_t)Hkv * n * kNibbleRow;
+    const size_t kmeta = (size_t)Hkv * g.n_groups * kHeadDim;
+    float *m = reinterpret_cast<float *>(anc_buf + 2 * rows_bytes);
+    MetaPtrs meta{m, m + kmeta, m + 2 * kmeta, m + 2 * kmeta + (size_t)Hkv * n};
+    dim3 grid(Hkv, g.n_groups);
+    hipLaunchKernelGGL(encode_kernel<2>, grid, dim3(kEncodeThreads), 0, stream, g, 0, n, -1,
+                       static_cast<const int32_t *>(nullptr), k, v, anc_buf, anc_buf + rows_bytes,
+                       res_buf, res_buf + rows_bytes, meta);
+    return hipGetLastError();
+}
+
+hipError_t launch_deserialize_anchor(const Geometry &g, int b, int t0, int n,
+                                     const int32_t *block_table, const uint8_t *buf,
+                                     uint8_t *k_anc, uint8_t *v_anc, MetaPtrs meta,
+                                     hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    const size_t work = (size_t)2 * g.Hkv * n * 4;  // the largest part
+    hipLaunchKernelGGL(deserialize_anchor_kernel, dim3(copy_blocks(work), 3), dim3(kCopyThreads), 0,
+                       stream, g, b, t0, n, bt_shift_of(g.bt), block_table, buf, k_anc, v_anc, meta);
+    return hipGetLastError();
+}
+
+hipError_t launch_deserialize_residual(const Geometry &g, int b, int t0, int n,
+                                       const int32_t *block_table, const uint8_t *buf,
+                                       const uint8_t *k_anc, const uint8_t *v_anc,
+                                       uint8_t *k_codes, uint8_t *v_codes, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    const size_t work = (size_t)2 * g.Hkv * n * 4;
+    hipLaunchKernelGGL(deserialize_residual_kernel, dim3(copy_blocks(work)), dim3(kCopyThreads), 0,
+                       stream, g, b, t0, n, bt_shift_of(g.bt), block_table, buf, k_anc, v_anc,
+                       k_codes, v_codes);
     return hipGetLastError();
 }
 

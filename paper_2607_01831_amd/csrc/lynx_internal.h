@@ -35,6 +35,21 @@ hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_t
 hipError_t launch_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t n_packed,
                         hipStream_t stream);
 
+// ---- serializer / deserializer (codec.hip) -----------------------------------
+// Object: tokens t0 .. t0 + n - 1 of one sequence, all kv heads.  Anchor
+// buffer: K, V anchor rows [Hkv][n][64], K scales, K zeros [Hkv][ceil(n/128)][128],
+// V scales, V zeros [Hkv][n]; residual buffer: K, V residual rows.
+hipError_t launch_serialize(int Hkv, int n, const uint16_t *k, const uint16_t *v,
+                            uint8_t *anc_buf, uint8_t *res_buf, hipStream_t stream);
+hipError_t launch_deserialize_anchor(const Geometry &g, int b, int t0, int n,
+                                     const int32_t *block_table, const uint8_t *buf,
+                                     uint8_t *k_anc, uint8_t *v_anc, MetaPtrs meta,
+                                     hipStream_t stream);
+hipError_t launch_deserialize_residual(const Geometry &g, int b, int t0, int n,
+                                       const int32_t *block_table, const uint8_t *buf,
+                                       const uint8_t *k_anc, const uint8_t *v_anc,
+                                       uint8_t *k_codes, uint8_t *v_codes, hipStream_t stream);
+
 // ---- attention (attention.hip) ----------------------------------------------
 enum class KvMode : int { kAnchor = 0, kCodes = 1 };
 

@@ -65,6 +65,10 @@ def load():
                                           SZ, P], ctypes.c_int),
         "lynx_spec_accept_workspace_bytes": ([I32, I32, I32], SZ),
         "lynx_spec_accept_greedy": ([I32, I32, I32, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "lynx_serialized_bytes": ([I32, I32, ctypes.POINTER(SZ), ctypes.POINTER(SZ)], ctypes.c_int),
+        "lynx_kv_serialize": ([I32, I32, P, P, P, P, P], ctypes.c_int),
+        "lynx_kv_deserialize_anchor": ([LP, I32, I32, I32, P, P, P, P, MP, P], ctypes.c_int),
+        "lynx_kv_deserialize_residual": ([LP, I32, I32, I32, P, P, P, P, P, P, P], ctypes.c_int),
         "lynx_strerror": ([ctypes.c_int], ctypes.c_char_p),
     }
     for name, (args, res) in sigs.items():
@@ -237,6 +241,40 @@ def lynx_attn_verify(L: Layout, B: int, Hq: int, k: int, max_seq_len: int, seq_l
 # ----------------------------------------------------------------------------
 # Allocation helpers (torch device memory only)
 # ----------------------------------------------------------------------------
+
+def lynx_serialized_bytes(num_kv_heads: int, n_tokens: int) -> tuple[int, int]:
+    """(anchor_bytes, residual_bytes) of an object of n_tokens tokens."""
+    a, r = ctypes.c_size_t(), ctypes.c_size_t()
+    _check("lynx_serialized_bytes", load().lynx_serialized_bytes(num_kv_heads, n_tokens,
+                                                                 ctypes.byref(a), ctypes.byref(r)))
+    return int(a.value), int(r.value)
+
+
+def lynx_kv_serialize(num_kv_heads: int, n_tokens: int, k, v, anchor_buf, residual_buf,
+                      stream=None) -> None:
+    """k, v: BF16 [n_tokens][Hkv][128] (an object's tokens); the buffers are
+    uint8 device tensors of lynx_serialized_bytes() bytes."""
+    _check("lynx_kv_serialize", load().lynx_kv_serialize(
+        num_kv_heads, n_tokens, _ptr(k), _ptr(v), _ptr(anchor_buf), _ptr(residual_buf),
+        _stream(stream)))
+
+
+def lynx_kv_deserialize_anchor(L: Layout, b: int, t0: int, n_tokens: int, block_table, anchor_buf,
+                               k_anc, v_anc, meta: Meta, stream=None) -> None:
+    lay, met = L.c(), meta.c()
+    _check("lynx_kv_deserialize_anchor", load().lynx_kv_deserialize_anchor(
+        ctypes.byref(lay), b, t0, n_tokens, _ptr(block_table), _ptr(anchor_buf), _ptr(k_anc),
+        _ptr(v_anc), ctypes.byref(met), _stream(stream)))
+
+
+def lynx_kv_deserialize_residual(L: Layout, b: int, t0: int, n_tokens: int, block_table,
+                                 residual_buf, k_anc, v_anc, k_codes, v_codes,
+                                 stream=None) -> None:
+    lay = L.c()
+    _check("lynx_kv_deserialize_residual", load().lynx_kv_deserialize_residual(
+        ctypes.byref(lay), b, t0, n_tokens, _ptr(block_table), _ptr(residual_buf), _ptr(k_anc),
+        _ptr(v_anc), _ptr(k_codes), _ptr(v_codes), _stream(stream)))
+
 
 @dataclass
 class KVPool:

@@ -146,3 +146,35 @@ def test_tail_and_acceptance_validation(lib):
     assert lib.lynx_spec_accept_greedy(2, 4, 100, 20, 16, 16, 16, 16, 1 << 20, None) == E.LYNX_EINVAL
     assert lib.lynx_spec_accept_greedy(2, 4, 100, 16, 16, 16, 16, 16, 8, None) == E.LYNX_EWORKSPACE
     assert lib.lynx_spec_accept_greedy(0, 4, 100, None, None, None, None, None, 0, None) == E.LYNX_OK
+
+
+def test_serdes_sizes_and_validation(lib):
+    """Object buffer sizes, and the serializer / deserializer reject bad
+    arguments before launching anything (no pointer below is dereferenced)."""
+    from paper_2607_01831_amd import lynx
+    E = lynx
+    # one kv head, 130 tokens: 2 x 130 x 64 row bytes + 2 x 2 x 128 x 4 K-scalar
+    # bytes + 2 x 130 x 4 V-scalar bytes; residual 2 x 130 x 64
+    assert lynx.lynx_serialized_bytes(1, 130) == (19728, 16640)
+    assert lynx.lynx_serialized_bytes(8, 32768) == (144 * 32768 * 8, 128 * 32768 * 8)
+    a, r = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.lynx_serialized_bytes(0, 10, ctypes.byref(a), ctypes.byref(r)) == E.LYNX_EINVAL
+    assert lib.lynx_serialized_bytes(2, 0, ctypes.byref(a), ctypes.byref(r)) == E.LYNX_EINVAL
+    # serialize: bad count, NULL / misaligned pointers, overlapping buffers
+    assert lib.lynx_kv_serialize(0, 4, 16, 16, 16, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_serialize(2, 4, None, 16, 16, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_serialize(2, 4, 16, 16, 24, 1 << 20, None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_serialize(2, 4, 16, 16, 1 << 20, (1 << 20) + 64, None) == E.LYNX_EINVAL
+    # deserialize: t0 not a multiple of 128, past the capacity, n < 1
+    L = _layout(max_blocks_per_seq=16, num_blocks=64, max_tokens=256)
+    lay = L.c()
+    meta = lynx.lynx_meta(16, 32, 48, 64)
+    args = (16, 16, 16, 16, ctypes.byref(meta), None)
+    assert lib.lynx_kv_deserialize_anchor(ctypes.byref(lay), 0, 64, 10, *args) == E.LYNX_EINVAL
+    assert lib.lynx_kv_deserialize_anchor(ctypes.byref(lay), 0, 128, 129, *args) == E.LYNX_EINVAL
+    assert lib.lynx_kv_deserialize_anchor(ctypes.byref(lay), 0, 0, 0, *args) == E.LYNX_EINVAL
+    assert lib.lynx_kv_deserialize_anchor(ctypes.byref(lay), -1, 0, 4, *args) == E.LYNX_EINVAL
+    assert lib.lynx_kv_deserialize_residual(ctypes.byref(lay), 0, 64, 10, 16, 16, 16, 16, 16, 16,
+                                            None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_deserialize_residual(ctypes.byref(lay), 0, 0, 4, 16, None, 16, 16, 16, 16,
+                                            None) == E.LYNX_EINVAL
