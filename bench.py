@@ -88,6 +88,8 @@ def parse():
                    help="skip the decode-with-tail and draft-acceptance stages")
     p.add_argument("--paged-calls", type=int, default=20,
                    help="timed paged batch-decode calls (paged-b16-16k-64k; 0 skips the stage)")
+    p.add_argument("--no-serdes", dest="serdes", action="store_false",
+                   help="skip the serializer / deserializer pipeline stage")
     p.add_argument("--no-overlap-70b", dest="overlap_70b", action="store_false",
                    help="skip the 70B-shaped overlap run (70b-overlap-b4-128k)")
     p.add_argument("--verify-128k-calls", type=int, default=20,
@@ -450,6 +452,166 @@ def overlap_70b_stage(dev):
     return {"overlap_70b_b4_128k": r}
 
 
+def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
+    """The prioritized transmission of Sec. 4.2 over the workload's layers, one
+    KV object per layer, on one GPU standing in for both instances:
+
+      sender compute   lynx_kv_serialize of layer l into one of three anchor
+                       buffers (reused once layer l - 3's anchor has left) and
+                       its own residual buffer
+      sender NIC       D2H of every anchor buffer, in layer order, through a
+                       ring of four pinned host slots (the wire); the residual
+                       buffers follow once every anchor has arrived (strict
+                       priority)
+      receiver NIC     H2D of each buffer into one of two receive buffers
+      receiver compute lynx_kv_deserialize_anchor of every layer (the Anchor
+                       phase: decoding could start when it ends), then
+                       lynx_kv_deserialize_residual (the Residual phase)
+
+    Three streams at the default priority: every kernel on the main stream
+    (the receiver's kernel for transfer m - 2 issued after the sender's for
+    m, so neither waits behind the other), the sends on the side stream, the
+    receives on a third.  The send and receive of this loopback share one PCIe link, which
+    carries both directions at once (≈56 GB/s each).  HIP events give the
+    times, relative to the first serialize; the same pipeline without its
+    kernels gives the wire alone.  The received pool is checked against the
+    direct encode + merge of the same layers."""
+    import torch
+
+    from paper_2607_01831_amd import lynx
+
+    na, nr = lynx.lynx_serialized_bytes(Hkv, T)
+    L = lynx.contiguous_layout(Hkv, 1, T)
+    table = torch.zeros(1, 1, dtype=torch.int32, device=dev)
+    u8 = dict(dtype=torch.uint8, device=dev)
+    n_tx, n_wire = 3, 4
+    tx_anc = [torch.empty(na, **u8) for _ in range(n_tx)]
+    tx_res = [torch.empty(nr, **u8) for _ in range(n_layers)]
+    rx = {"a": [torch.empty(na, **u8) for _ in range(2)], "r": [torch.empty(nr, **u8) for _ in range(2)]}
+    # the wire: a ring of pinned host slots, as a NIC's registered buffers
+    ring = [torch.empty(max(na, nr), dtype=torch.uint8).pin_memory() for _ in range(n_wire)]
+    recv, _ = lynx.KVPool.allocate_layers(L, 1, n_layers, device=dev)
+    main_s, s_send, s_recv = torch.cuda.current_stream(), side, torch.cuda.Stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def run(kernels=True):
+        # transfers in wire order: every anchor, then every residual; every
+        # event is recorded (enqueued) before any stream waits on it
+        N = n_layers
+        xfers = [("a", l) for l in range(N)] + [("r", l) for l in range(N)]
+        M = len(xfers)
+        ser = [ev() for _ in range(N)]
+        sent, got, des = ([ev() for _ in range(M)] for _ in range(3))
+        t0 = ev()
+        t0.record(main_s)
+
+        def deserialize(m):
+            kind, l = xfers[m]
+            main_s.wait_event(got[m])
+            if kernels:
+                p = recv[l]
+                if kind == "a":
+                    lynx.lynx_kv_deserialize_anchor(L, 0, 0, T, table, rx["a"][l % 2], p.k_anc, p.v_anc, p.meta)
+                else:
+                    lynx.lynx_kv_deserialize_residual(L, 0, 0, T, table, rx["r"][l % 2], p.k_anc, p.v_anc,
+                                                      p.k_codes, p.v_codes)
+            des[m].record(main_s)
+
+        for m, (kind, l) in enumerate(xfers):
+            nbytes = na if kind == "a" else nr
+            if kind == "a":                          # sender compute
+                if l >= n_tx:
+                    main_s.wait_event(sent[l - n_tx])    # its send buffer has left
+                if kernels:
+                    lynx.lynx_kv_serialize(Hkv, T, K[l], V[l], tx_anc[l % n_tx], tx_res[l])
+                ser[l].record(main_s)
+                s_send.wait_event(ser[l])
+            elif l == 0:
+                s_send.wait_event(got[N - 1])            # residuals once every anchor is in
+            if m >= n_wire:
+                s_send.wait_event(got[m - n_wire])       # its wire slot has been read
+            with torch.cuda.stream(s_send):              # sender NIC
+                src = tx_anc[l % n_tx] if kind == "a" else tx_res[l]
+                ring[m % n_wire][:nbytes].copy_(src, non_blocking=True)
+                sent[m].record(s_send)
+            if m >= 2:                                   # receiver compute, two transfers behind
+                deserialize(m - 2)
+            s_recv.wait_event(sent[m])
+            if m >= 2 and xfers[m - 2][0] == kind:
+                s_recv.wait_event(des[m - 2])            # its receive buffer is free
+            with torch.cuda.stream(s_recv):              # receiver NIC
+                rx[kind][l % 2].copy_(ring[m % n_wire][:nbytes], non_blocking=True)
+                got[m].record(s_recv)
+        deserialize(M - 2)
+        deserialize(M - 1)
+        torch.cuda.synchronize()
+        ms = lambda e: t0.elapsed_time(e)
+        return {"serialized": ms(ser[-1]), "anchors_sent": ms(sent[N - 1]), "anchor_ready": ms(des[N - 1]),
+                "residuals_sent": ms(sent[-1]), "full_ready": ms(des[-1])}
+
+    run()
+    best = wire = None
+    for _ in range(3):
+        r = run()
+        if best is None or r["full_ready"] < best["full_ready"]:
+            best = r
+        r = run(kernels=False)
+        if wire is None or r["full_ready"] < wire["full_ready"]:
+            wire = r
+    run()
+    # each kernel alone
+    def alone(fn):
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record()
+        fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+    t_ser = alone(lambda: [lynx.lynx_kv_serialize(Hkv, T, K[l], V[l], tx_anc[l % n_tx], tx_res[l])
+                           for l in range(n_layers)])
+    t_da = alone(lambda: [lynx.lynx_kv_deserialize_anchor(L, 0, 0, T, table, rx["a"][l % 2], recv[l].k_anc,
+                                                          recv[l].v_anc, recv[l].meta) for l in range(n_layers)])
+    run()  # the loop above scattered the last receive buffers into every layer
+    t_dr = alone(lambda: [lynx.lynx_kv_deserialize_residual(L, 0, 0, T, table, rx["r"][l % 2], recv[l].k_anc,
+                                                            recv[l].v_anc, recv[l].k_codes, recv[l].v_codes)
+                          for l in range(n_layers)])
+    run()
+    elems = T * Hkv * 128 * 2
+    us_l = lambda t: t * 1e3 / n_layers
+    r = {
+        "objects": n_layers,
+        "anchor_MB_per_object": round(na / 1e6, 2),
+        "residual_MB_per_object": round(nr / 1e6, 2),
+        "serialize_us_per_object": round(us_l(t_ser), 2),
+        "serialize_GBps": round(elems * ENC_BYTES_PER_ELEM * n_layers / (t_ser * 1e-3) / 1e9, 1),
+        "deserialize_anchor_us_per_object": round(us_l(t_da), 2),
+        "deserialize_anchor_GBps": round(2 * na * n_layers / (t_da * 1e-3) / 1e9, 1),
+        "deserialize_residual_us_per_object": round(us_l(t_dr), 2),
+        "deserialize_residual_GBps": round(T * Hkv * 512 * n_layers / (t_dr * 1e-3) / 1e9, 1),
+        "pipelined_ms": {k: round(v, 3) for k, v in best.items()},
+        "wire_only_ms": {k: round(v, 3) for k, v in wire.items()},
+        "wire_GBps_per_direction": round((na + nr) * n_layers / (wire["full_ready"] * 1e-3) / 1e9, 2),
+        "anchor_ready_over_full": round(best["anchor_ready"] / best["full_ready"], 3),
+        # share of the serialize + anchor-phase kernel time hidden behind the wire
+        "compute_hidden": round(max(0.0, min(1.0, 1.0 - (best["anchor_ready"] - wire["anchor_ready"])
+                                             / max(t_ser + t_da, 1e-9))), 3),
+    }
+    # the receiver's pool equals the direct encode + merge of the same layers
+    direct = lynx.KVPool.allocate(L, 1, device=dev)
+    ok = True
+    for l in (0, n_layers // 2, n_layers - 1):
+        direct.encode(0, T, table, K[l], V[l])
+        direct.merge()
+        for name in ("k_anc", "v_anc", "k_codes", "v_codes"):
+            ok &= bool(torch.equal(getattr(recv[l], name), getattr(direct, name)))
+        for name in ("k_scale", "k_zero", "v_scale", "v_zero"):
+            ok &= bool(torch.equal(getattr(recv[l].meta, name), getattr(direct.meta, name)))
+    r["received_equals_encode"] = ok
+    del tx_anc, tx_res, rx, ring, recv, direct
+    return {"serdes_pipeline": r}
+
+
 def cpu_baseline(w, layer_inputs, n_layers):
     """The CPU oracle, untuned, timed on this host on a bounded sample: the
     anchor decode of the first n_layers layers (all kv heads)."""
@@ -610,6 +772,7 @@ def main():
     ver128 = verify_128k(args.verify_128k_calls, dev) if args.verify_128k_calls > 0 else None
     paged = paged_decode_stage(args.paged_calls, dev) if args.paged_calls > 0 else None
     ovl = overlap_70b_stage(dev) if args.overlap_70b else None
+    serdes = serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side) if args.serdes else None
 
     # The speculative decoder's own pieces, timed alone: decode over the
     # anchors plus the 8 BF16 tokens it generated (32 layers), and greedy
@@ -700,6 +863,7 @@ def main():
             **(ver128 or {}),
             **(paged or {}),
             **(ovl or {}),
+            **(serdes or {}),
             **spec,
             "decode_hidden_behind_h2d": round(overlap, 3),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
