@@ -59,6 +59,16 @@ def _load():
     lib.oracle_anchor_decode_tail.argtypes = [I, I, I, I, I, I, P, P, P, P, P, P, P, P,
                                               P, I, P, P, P, P, P, I]
     lib.oracle_anchor_decode_tail.restype = I
+    F = ctypes.c_float
+    IP = ctypes.POINTER(ctypes.c_int)
+    lib.oracle_hsplit.argtypes = [I, I, IP, IP]
+    lib.oracle_hsplit.restype = None
+    lib.oracle_htables.argtypes = [F, P, P]
+    lib.oracle_htables.restype = None
+    lib.oracle_hencode.argtypes = [I, I, I, I, I, I, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_hencode.restype = I
+    lib.oracle_hdequant.argtypes = [I, I, I, I, I, I, I, P, P, P, F, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_hdequant.restype = I
     _LIB = lib
     return lib
 
@@ -380,3 +390,86 @@ def deserialize_residual(L: Layout, b: int, t0: int, n: int, block_table: np.nda
         anc = planes[anc_name][src].reshape(-1)
         res = buf[off:off + size]
         codes[code_name][dst] = merge(anc, res).reshape(L.Hkv, n, 128)
+
+
+# --------------------------------------------------------------------------
+# Hierarchical non-linear codec (Alg. 1, Sec. 4.1): pages of 256 tokens and
+# chunks of 32 per channel, alpha-law transform to 7 bits and a sign, split
+# into a signed 4-bit anchor and a signed 4-bit correction.  The readings of
+# the garbled parts of the listing are stated in lynx_oracle.c.
+# --------------------------------------------------------------------------
+
+H_PAGE = 256
+H_CHUNK = 32
+
+
+@dataclass
+class HMeta:
+    """fp32 metadata of the hierarchical codec for K and V of a batch."""
+    k_gmin: np.ndarray    # [B][Hkv][ceil(max_tokens/256)][128]
+    k_gscale: np.ndarray
+    k_mu: np.ndarray      # [B][Hkv][ceil(max_tokens/32)][128]
+    k_sigma: np.ndarray
+    v_gmin: np.ndarray
+    v_gscale: np.ndarray
+    v_mu: np.ndarray
+    v_sigma: np.ndarray
+
+    @staticmethod
+    def empty(L: Layout, B: int) -> "HMeta":
+        pg = (B, L.Hkv, -(-L.max_tokens // H_PAGE), HEAD_DIM)
+        ch = (B, L.Hkv, -(-L.max_tokens // H_CHUNK), HEAD_DIM)
+        z = lambda shape: np.zeros(shape, np.float32)
+        return HMeta(z(pg), z(pg), z(ch), z(ch), z(pg), z(pg), z(ch), z(ch))
+
+    def ptrs(self):
+        return [_ptr(a) for a in (self.k_gmin, self.k_gscale, self.k_mu, self.k_sigma,
+                                  self.v_gmin, self.v_gscale, self.v_mu, self.v_sigma)]
+
+
+def hsplit(I: int, S: int):
+    """Stage 4 of Alg. 1 for one code: (anchor, residual) nibble values."""
+    a, r = ctypes.c_int(), ctypes.c_int()
+    _load().oracle_hsplit(int(I), int(S), ctypes.byref(a), ctypes.byref(r))
+    return a.value, r.value
+
+
+def htables(alpha: float):
+    """(decision thresholds [127], reconstruction levels [128]) for alpha."""
+    theta = np.zeros(127, np.float32)
+    level = np.zeros(128, np.float32)
+    _load().oracle_htables(alpha, _ptr(theta), _ptr(level))
+    return theta, level
+
+
+def hencode(L: Layout, b: int, T: int, block_table: np.ndarray, k_bits: np.ndarray,
+            v_bits: np.ndarray, alpha: float, planes: dict, hmeta: HMeta) -> None:
+    """Hierarchical encode of sequence b (k_bits, v_bits: uint16 [T][Hkv][128])
+    into planes['k_anc'|'v_anc'|'k_res'|'v_res'] and hmeta row b."""
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    k_bits = np.ascontiguousarray(k_bits, dtype=np.uint16)
+    v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
+    assert k_bits.shape == (T, L.Hkv, HEAD_DIM) and v_bits.shape == k_bits.shape
+    rc = _load().oracle_hencode(L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T, _ptr(bt_arr),
+                                _ptr(k_bits), _ptr(v_bits), alpha, _ptr(planes["k_anc"]),
+                                _ptr(planes["v_anc"]), _ptr(planes["k_res"]), _ptr(planes["v_res"]),
+                                *hmeta.ptrs())
+    if rc != 0:
+        raise ValueError(f"oracle_hencode rejected its arguments ({rc})")
+
+
+def hdequant(mode: str, L: Layout, b: int, T: int, block_table: np.ndarray,
+             k_plane: np.ndarray, v_plane: np.ndarray, alpha: float, hmeta: HMeta):
+    """Reconstructed K, V of sequence b as BF16 bits (uint16 [T][Hkv][128]):
+    mode 'anchor' from the anchor nibble planes, 'full' from the merged code
+    planes."""
+    m = {"anchor": 0, "full": 1}[mode]
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    k_out = np.zeros((T, L.Hkv, HEAD_DIM), np.uint16)
+    v_out = np.zeros_like(k_out)
+    rc = _load().oracle_hdequant(m, L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T, _ptr(bt_arr),
+                                 _ptr(k_plane), _ptr(v_plane), alpha, *hmeta.ptrs(), _ptr(k_out),
+                                 _ptr(v_out))
+    if rc != 0:
+        raise ValueError(f"oracle_hdequant rejected its arguments ({rc})")
+    return k_out, v_out

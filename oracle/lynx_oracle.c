@@ -502,3 +502,222 @@ int oracle_verify(int Hkv, int bt, int max_blocks, int max_tokens, int B, int Hq
     J.nthreads = nthreads;
     return run_attention(&J);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Hierarchical non-linear quantization (Alg. 1, Sec. 4.1)                   */
+/* ------------------------------------------------------------------------ */
+/*
+ * Per channel of one kv head (K and V alike), over pages of 256 tokens and
+ * chunks of 32 tokens (the configuration of Sec. 6.1), in the order of the
+ * four stages of Alg. 1:
+ *   1. page normalization: gmin = min x and gscale = max x - gmin over the
+ *      page's tokens; X = (x - gmin) * (1 / gscale), so X lies in [0, 1];
+ *   2. chunk isolation: mu = the mean of X over the chunk's tokens (an fp32
+ *      sum in token order divided by the count), Xc = X - mu,
+ *      sigma = max |Xc|, Xf = Xc * (1 / sigma), so |Xf| <= 1;
+ *   3. non-linear transform: I = Round(127 ln(1 + a |Xf|) / ln(1 + a)), the
+ *      sign S of Xc;
+ *   4. split: V = (I + 7) >> 4 (the anchor magnitude, rounded half down),
+ *      Q_res = 16 V - I (the correction), Q_anc = V for S >= 0 and -V - 1 for
+ *      S < 0, both kept as 4-bit two's complement nibbles.
+ * Readings where the listing is garbled or at odds with the 4-bit streams:
+ *   - the sign is that of the centred value Xc (the listing's X_view is
+ *     non-negative after stage 1);
+ *   - no epsilon: a page (chunk) whose range (sigma) has no finite positive
+ *     reciprocal normalizes to 0;
+ *   - Round(Y) is decided as the number of decision thresholds theta_k
+ *     (k = 0..126) with theta_k <= |Xf|, theta_k being the fp32 value of
+ *     expm1(((k + 0.5) / 127) * log1p(a)) / a in IEEE double: the point
+ *     where the transform equals k + 1/2;
+ *   - V reaches 8 for I >= 121, which 4 bits cannot hold with a sign: V is
+ *     clamped to 7 and Q_res to [-8, 7], so codes above 120 come back as 120;
+ *   - reconstruction maps I' = 16 V - Q_res (anchor only: I' = 16 V) to the
+ *     level expm1((I' / 127) * log1p(a)) / a (fp32 of the double value),
+ *     then x = ((+-level * sigma) + mu) * gscale + gmin, each step an fp32
+ *     operation, rounded to BF16 to nearest even.
+ */
+#define H_PAGE 256
+#define H_CHUNK 32
+
+static void h_tables(float alpha, float *theta, float *level)
+{
+    const double la = log1p((double)alpha);
+    for (int k = 0; k < 127; ++k)
+        theta[k] = (float)(expm1(((k + 0.5) / 127.0) * la) / (double)alpha);
+    for (int i = 0; i < 128; ++i)
+        level[i] = (float)(expm1((i / 127.0) * la) / (double)alpha);
+}
+
+/* The reciprocal of a range, or 0 when it is not a finite positive value. */
+static float range_recip(float r)
+{
+    float v = 1.0f / r;
+    return (r > 0.0f && v <= FLT_MAX) ? v : 0.0f;
+}
+
+/* Stage 4: the anchor and residual nibble values of (I, S). */
+void oracle_hsplit(int I, int S, int *q_anc, int *q_res)
+{
+    int V = (I + 7) >> 4;
+    if (V > 7) V = 7;
+    int r = 16 * V - I;
+    if (r < -8) r = -8;
+    if (r > 7) r = 7;
+    *q_anc = S < 0 ? -V - 1 : V;
+    *q_res = r;
+}
+
+/* Exposes the decision thresholds (127) and reconstruction levels (128). */
+void oracle_htables(float alpha, float *theta, float *level)
+{
+    h_tables(alpha, theta, level);
+}
+
+static int sext4(int nib) { return nib >= 8 ? nib - 16 : nib; }
+
+static uint16_t float_to_bf16_rne(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+/*
+ * k, v: BF16 bits [T][Hkv][128] of sequence b.  Writes its rows of the
+ * anchor and residual nibble planes and its metadata rows: gmin, gscale
+ * [B][Hkv][ceil(max_tokens/256)][128], mu, sigma
+ * [B][Hkv][ceil(max_tokens/32)][128], for K and V.  Returns 0, or -1.
+ */
+int oracle_hencode(int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
+                   const int32_t *block_table, const uint16_t *k, const uint16_t *v, float alpha,
+                   uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
+                   float *k_gmin, float *k_gscale, float *k_mu, float *k_sigma,
+                   float *v_gmin, float *v_gscale, float *v_mu, float *v_sigma)
+{
+    if (Hkv < 1 || bt < 1 || T < 0 || T > max_tokens || !(alpha > 0.0f)) return -1;
+    float theta[127], level[128];
+    h_tables(alpha, theta, level);
+    const int n_pages = (max_tokens + H_PAGE - 1) / H_PAGE;
+    const int n_chunks = (max_tokens + H_CHUNK - 1) / H_CHUNK;
+    const int32_t *bt_row = block_table + (size_t)b * max_blocks;
+    for (int which = 0; which < 2; ++which) {
+        const uint16_t *src = which == 0 ? k : v;
+        uint8_t *anc = which == 0 ? k_anc : v_anc;
+        uint8_t *res = which == 0 ? k_res : v_res;
+        float *gmin_a = which == 0 ? k_gmin : v_gmin, *gsc_a = which == 0 ? k_gscale : v_gscale;
+        float *mu_a = which == 0 ? k_mu : v_mu, *sig_a = which == 0 ? k_sigma : v_sigma;
+        for (int h = 0; h < Hkv; ++h)
+            for (int p = 0; p * H_PAGE < T; ++p) {
+                const int t0 = p * H_PAGE;
+                const int n = T - t0 < H_PAGE ? T - t0 : H_PAGE;
+                for (int d = 0; d < HEAD_DIM; ++d) {
+                    float x[H_PAGE] = {0.0f}, X[H_PAGE];
+                    for (int i = 0; i < n; ++i)
+                        x[i] = bf16_bits_to_float(src[((size_t)(t0 + i) * Hkv + h) * HEAD_DIM + d]);
+                    /* stage 1 */
+                    float lo = x[0], hi = x[0];
+                    for (int i = 1; i < n; ++i) {
+                        if (x[i] < lo) lo = x[i];
+                        if (x[i] > hi) hi = x[i];
+                    }
+                    if (lo == 0.0f) lo = 0.0f;
+                    if (hi == 0.0f) hi = 0.0f;
+                    const float gscale = hi - lo;
+                    const float ig = range_recip(gscale);
+                    for (int i = 0; i < n; ++i) X[i] = (x[i] - lo) * ig;
+                    const size_t pm = (((size_t)b * Hkv + h) * n_pages + p) * HEAD_DIM + d;
+                    gmin_a[pm] = lo;
+                    gsc_a[pm] = gscale;
+                    /* stages 2-4, chunk by chunk */
+                    for (int c = 0; c * H_CHUNK < n; ++c) {
+                        const int i0 = c * H_CHUNK;
+                        const int cnt = n - i0 < H_CHUNK ? n - i0 : H_CHUNK;
+                        float sum = 0.0f;
+                        for (int i = i0; i < i0 + cnt; ++i) sum += X[i];
+                        const float mu = sum / (float)cnt;
+                        float sigma = 0.0f;
+                        for (int i = i0; i < i0 + cnt; ++i) {
+                            const float a = fabsf(X[i] - mu);
+                            if (a > sigma) sigma = a;
+                        }
+                        const float is = range_recip(sigma);
+                        const size_t cm = (((size_t)b * Hkv + h) * n_chunks + (size_t)t0 / H_CHUNK + c) * HEAD_DIM + d;
+                        mu_a[cm] = mu;
+                        sig_a[cm] = sigma;
+                        for (int i = i0; i < i0 + cnt; ++i) {
+                            const float xc = X[i] - mu;
+                            float xf = fabsf(xc * is);
+                            if (xf > 1.0f) xf = 1.0f;
+                            int I = 0;
+                            while (I < 127 && theta[I] <= xf) ++I;
+                            const int S = xc > 0.0f ? 1 : (xc < 0.0f ? -1 : 0);
+                            int qa, qr;
+                            oracle_hsplit(I, S, &qa, &qr);
+                            const int t = t0 + i;
+                            if (bt_row[t / bt] < 0) return -1;
+                            const size_t row = plane_row_offset(bt_row, Hkv, bt, h, t, NIBBLE_ROW);
+                            put_nibble(anc + row, d, qa & 0xF);
+                            put_nibble(res + row, d, qr & 0xF);
+                        }
+                    }
+                }
+            }
+    }
+    return 0;
+}
+
+/*
+ * Reconstruction of sequence b's K and V as BF16 bits [T][Hkv][128]:
+ * mode 0 from the anchor nibble planes alone (I' = 16 V), mode 1 from the
+ * merged code planes (byte of element e: anchor nibble << 4 | residual
+ * nibble; I' = 16 V - Q_res).  Returns 0, or -1.
+ */
+int oracle_hdequant(int mode, int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
+                    const int32_t *block_table, const uint8_t *k_plane, const uint8_t *v_plane,
+                    float alpha, const float *k_gmin, const float *k_gscale, const float *k_mu,
+                    const float *k_sigma, const float *v_gmin, const float *v_gscale,
+                    const float *v_mu, const float *v_sigma, uint16_t *k_out, uint16_t *v_out)
+{
+    if ((mode != 0 && mode != 1) || Hkv < 1 || T < 0 || T > max_tokens || !(alpha > 0.0f)) return -1;
+    float theta[127], level[128];
+    h_tables(alpha, theta, level);
+    const int n_pages = (max_tokens + H_PAGE - 1) / H_PAGE;
+    const int n_chunks = (max_tokens + H_CHUNK - 1) / H_CHUNK;
+    const int32_t *bt_row = block_table + (size_t)b * max_blocks;
+    for (int which = 0; which < 2; ++which) {
+        const uint8_t *plane = which == 0 ? k_plane : v_plane;
+        const float *gmin_a = which == 0 ? k_gmin : v_gmin, *gsc_a = which == 0 ? k_gscale : v_gscale;
+        const float *mu_a = which == 0 ? k_mu : v_mu, *sig_a = which == 0 ? k_sigma : v_sigma;
+        uint16_t *out = which == 0 ? k_out : v_out;
+        for (int t = 0; t < T; ++t)
+            for (int h = 0; h < Hkv; ++h) {
+                if (bt_row[t / bt] < 0) return -1;
+                const uint8_t *row = plane + plane_row_offset(bt_row, Hkv, bt, h, t,
+                                                              mode == 0 ? NIBBLE_ROW : CODE_ROW);
+                for (int d = 0; d < HEAD_DIM; ++d) {
+                    int qa, Ip;
+                    if (mode == 0) {
+                        qa = sext4(get_nibble(row, d));
+                    } else {
+                        qa = sext4(row[d] >> 4);
+                    }
+                    const int V = qa >= 0 ? qa : -qa - 1;
+                    Ip = 16 * V;
+                    if (mode == 1) Ip -= sext4(row[d] & 0xF);
+                    if (Ip < 0) Ip = 0;
+                    if (Ip > 127) Ip = 127;
+                    const float m = qa >= 0 ? level[Ip] : -level[Ip];
+                    const size_t pm = (((size_t)b * Hkv + h) * n_pages + t / H_PAGE) * HEAD_DIM + d;
+                    const size_t cm = (((size_t)b * Hkv + h) * n_chunks + t / H_CHUNK) * HEAD_DIM + d;
+                    const float xc = m * sig_a[cm];
+                    const float X = xc + mu_a[cm];
+                    const float y = X * gsc_a[pm];
+                    const float x = y + gmin_a[pm];
+                    out[((size_t)t * Hkv + h) * HEAD_DIM + d] = float_to_bf16_rne(x);
+                }
+            }
+    }
+    return 0;
+}

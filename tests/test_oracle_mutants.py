@@ -62,3 +62,29 @@ def test_pins_catch_mutant(name, tmp_path):
                         "tests/test_oracle_codec.py", "tests/test_oracle_attention.py"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+# Mistakes planted in the hierarchical codec (Alg. 1), caught by its own pins.
+HIER_MUTANTS = {
+    "sign_of_normalized_value": ("const int S = xc > 0.0f ? 1 : (xc < 0.0f ? -1 : 0);",
+                                 "const int S = 1;"),
+    "mean_not_restored": ("const float X = xc + mu_a[cm];", "const float X = xc;"),
+    "chunk_64": ("#define H_CHUNK 32", "#define H_CHUNK 64"),
+    "no_rounding_bias": ("int V = (I + 7) >> 4;", "int V = I >> 4;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(HIER_MUTANTS))
+def test_hier_pins_catch_mutant(name, tmp_path):
+    find, repl = HIER_MUTANTS[name]
+    assert SRC.count(find) == 1, f"mutation anchor for {name} not unique/present"
+    src = tmp_path / "mutant.c"
+    src.write_text(SRC.replace(find, repl))
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-shared", "-fPIC",
+                    "-pthread", str(src), "-o", str(lib), "-lm"], check=True)
+    env = dict(os.environ, LYNX_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        "tests/test_oracle_hier.py"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
