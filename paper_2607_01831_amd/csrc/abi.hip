@@ -24,6 +24,8 @@ int check_layout(const lynx_layout *L, Geometry *g) {
     g->num_blocks = L->num_blocks;
     g->max_tokens = L->max_tokens;
     g->n_groups = (L->max_tokens + lynx::kKGroup - 1) / lynx::kKGroup;
+    g->n_pages = (L->max_tokens + 255) / 256;
+    g->n_chunks = (L->max_tokens + 31) / 32;
     return LYNX_OK;
 }
 
@@ -299,6 +301,69 @@ int lynx_kv_deserialize_residual(const lynx_layout *L, int32_t b, int32_t t0, in
     hipError_t e = lynx::launch_deserialize_residual(
         g, b, t0, n_tokens, block_table, static_cast<const uint8_t *>(residual_buf), k_anc, v_anc,
         k_codes, v_codes, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+}  // extern "C"
+
+namespace {
+int check_hmeta(const lynx_hmeta *m, lynx::HMetaPtrs *hp) {
+    if (!m) return LYNX_EINVAL;
+    float *ptrs[] = {m->k_gmin, m->k_gscale, m->k_mu, m->k_sigma,
+                     m->v_gmin, m->v_gscale, m->v_mu, m->v_sigma};
+    for (float *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    *hp = lynx::HMetaPtrs{m->k_gmin, m->k_gscale, m->k_mu, m->k_sigma,
+                          m->v_gmin, m->v_gscale, m->v_mu, m->v_sigma};
+    return LYNX_OK;
+}
+bool alpha_ok(float a) { return a > 0.0f && a <= 1e30f; }
+}  // namespace
+
+extern "C" {
+
+int lynx_hkv_encode(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
+                    const void *k_bf16, const void *v_bf16, float alpha, uint8_t *k_anc,
+                    uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res, const lynx_hmeta *meta,
+                    void *stream) {
+    Geometry g;
+    lynx::HMetaPtrs hp;
+    int rc = check_layout(L, &g);
+    if (rc != LYNX_OK) return rc;
+    if ((rc = check_hmeta(meta, &hp)) != LYNX_OK) return rc;
+    if (!alpha_ok(alpha) || b < 0 || T < 0 || T > layout_capacity(g)) return LYNX_EINVAL;
+    if (T == 0) return LYNX_OK;
+    const void *ptrs[] = {block_table, k_bf16, v_bf16, k_anc, v_anc, k_res, v_res};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    lynx::HTables tab;
+    lynx::make_htables(alpha, &tab);
+    hipError_t e = lynx::launch_hencode(g, b, T, block_table, static_cast<const uint16_t *>(k_bf16),
+                                        static_cast<const uint16_t *>(v_bf16), k_anc, v_anc, k_res,
+                                        v_res, hp, tab, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_hkv_dequant(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
+                     int32_t full, const uint8_t *k_plane, const uint8_t *v_plane, float alpha,
+                     const lynx_hmeta *meta, void *k_out_bf16, void *v_out_bf16, void *stream) {
+    Geometry g;
+    lynx::HMetaPtrs hp;
+    int rc = check_layout(L, &g);
+    if (rc != LYNX_OK) return rc;
+    if ((rc = check_hmeta(meta, &hp)) != LYNX_OK) return rc;
+    if (!alpha_ok(alpha) || (full != 0 && full != 1) || b < 0 || T < 0 || T > layout_capacity(g))
+        return LYNX_EINVAL;
+    if (T == 0) return LYNX_OK;
+    const void *ptrs[] = {block_table, k_plane, v_plane, k_out_bf16, v_out_bf16};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    lynx::HTables tab;
+    lynx::make_htables(alpha, &tab);
+    hipError_t e = lynx::launch_hdequant(full == 1, g, b, T, block_table, k_plane, v_plane, hp, tab,
+                                         static_cast<uint16_t *>(k_out_bf16),
+                                         static_cast<uint16_t *>(v_out_bf16),
+                                         static_cast<hipStream_t>(stream));
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
 

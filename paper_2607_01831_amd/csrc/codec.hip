@@ -484,6 +484,8 @@ hipError_t launch_serialize(int Hkv, int n, const uint16_t *k, const uint16_t *v
     g.num_blocks = 1;
     g.max_tokens = n;
     g.n_groups = (n + kKGroup - 1) / kKGroup;
+    g.n_pages = (n + 255) / 256;
+    g.n_chunks = (n + 31) / 32;
     const size_t rows_bytes = (size_t)Hkv * n * kNibbleRow;
     const size_t kmeta = (size_t)Hkv * g.n_groups * kHeadDim;
     float *m = reinterpret_cast<float *>(anc_buf + 2 * rows_bytes);

@@ -1,0 +1,361 @@
+// The hierarchical non-linear codec of Alg. 1 (Sec. 4.1) for gfx950:
+// encode (page normalization, chunk isolation, alpha-law transform, biased
+// split into a signed 4-bit anchor and a signed 4-bit correction) and the
+// deserializer's dequantization of the anchor alone or of the merged codes
+// into BF16 pages (Sec. 4.2 Anchor and Residual phases).
+//
+// Per channel of a kv head (K and V alike), pages of 256 tokens, chunks of
+// 32 (Sec. 6.1):
+//   1. gmin = min x, gscale = max x - gmin over the page; X = (x - gmin) *
+//      (1 / gscale);
+//   2. mu = the chunk's mean of X (fp32 sum in token order / count),
+//      Xc = X - mu, sigma = max |Xc|, Xf = Xc * (1 / sigma);
+//   3. I = Round(127 ln(1 + a|Xf|) / ln(1 + a)): the number of decision
+//      thresholds theta_k <= |Xf| (a binary search over the sorted table);
+//      S = sign(Xc);
+//   4. V = min((I + 7) >> 4, 7), Q_res = clamp(16 V - I, -8, 7),
+//      Q_anc = V, or -V - 1 for S < 0.
+// A range whose reciprocal is not finite and positive normalizes to 0.  Every
+// fp32 product that an add follows is rounded on its own (mul_rn), so no
+// fused multiply-add changes a result.
+#include "lynx_internal.h"
+
+#include <float.h>
+#include <math.h>
+
+namespace lynx {
+namespace {
+
+constexpr int kPage = 256;
+constexpr int kChunk = 32;
+constexpr int kHThreads = 256;
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+// An fp32 product rounded on its own.  HIP contracts a product into a
+// following add (an FMA, one rounding fewer) even across statements; the
+// empty asm hands the rounded product over, so the sum that follows is a
+// separate IEEE add, as the definition has it.
+__device__ __forceinline__ float mul_rn(float a, float b) {
+    float p = a * b;
+    asm volatile("" : "+v"(p));
+    return p;
+}
+
+__device__ __forceinline__ float range_recip(float r) {
+    const float v = 1.0f / r;  // IEEE division (correctly rounded)
+    return (r > 0.0f && v <= FLT_MAX) ? v : 0.0f;
+}
+
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (u >> 16) | 0x40u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Stage 4 for one code: the byte-ready nibbles of the anchor and residual.
+__device__ __forceinline__ void split(int I, float xc, uint32_t &qa, uint32_t &qr) {
+    int V = (I + 7) >> 4;
+    V = V > 7 ? 7 : V;
+    int r = 16 * V - I;
+    r = r < -8 ? -8 : (r > 7 ? 7 : r);
+    qa = (uint32_t)(xc < 0.0f ? -V - 1 : V) & 15u;
+    qr = (uint32_t)r & 15u;
+}
+
+// Workgroup (kv head, page, K or V).  Thread (quarter q = tid / 64, channel
+// pair cp = tid % 64) owns channels 2 cp, 2 cp + 1 of the page's tokens
+// 64 q .. 64 q + 63 (chunks 2 q, 2 q + 1): a wavefront reads whole 256-byte
+// token rows and writes whole 64-byte plane rows.  LAYOUT 0: one block per
+// sequence; 1: paged.
+template <int LAYOUT>
+__global__ __launch_bounds__(kHThreads) void hencode_kernel(
+    Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
+    const uint16_t *__restrict__ k, const uint16_t *__restrict__ v, uint8_t *__restrict__ k_anc,
+    uint8_t *__restrict__ v_anc, uint8_t *__restrict__ k_res, uint8_t *__restrict__ v_res,
+    HMetaPtrs meta, HTables tab) {
+    const int h = blockIdx.x;
+    const int p = blockIdx.y;
+    const int which = blockIdx.z;
+    const int tid = threadIdx.x;
+    const int cp = tid & 63;
+    const int q = tid >> 6;
+    const int Hkv = geo.Hkv;
+    const int t0 = p * kPage;
+    const int n = min(kPage, T - t0);
+    const uint16_t *src = which == 0 ? k : v;
+    uint8_t *anc = which == 0 ? k_anc : v_anc;
+    uint8_t *res = which == 0 ? k_res : v_res;
+    float *gmin_a = which == 0 ? meta.k_gmin : meta.v_gmin;
+    float *gsc_a = which == 0 ? meta.k_gscale : meta.v_gscale;
+    float *mu_a = which == 0 ? meta.k_mu : meta.v_mu;
+    float *sig_a = which == 0 ? meta.k_sigma : meta.v_sigma;
+
+    __shared__ float s_theta[128];
+    __shared__ float s_lo[4][kHeadDim], s_hi[4][kHeadDim];
+    if (tid < 128) s_theta[tid] = tab.theta[tid];
+
+    // the thread's 64 tokens x 2 channels (BF16 pairs)
+    uint32_t raw[64];
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+        const int tl = min(64 * q + i, n - 1);  // rows past the page re-read its last token
+        raw[i] = *reinterpret_cast<const uint32_t *>(src + ((size_t)(t0 + tl) * Hkv + h) * kHeadDim + 2 * cp);
+    }
+    const int mine = max(0, min(64, n - 64 * q));  // valid tokens of the thread
+
+    // ---- stage 1: page min / max per channel ----
+    float lo0 = INFINITY, hi0 = -INFINITY, lo1 = INFINITY, hi1 = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+        if (i < mine) {
+            const float x0 = bf16_to_f32(raw[i] & 0xffffu), x1 = bf16_to_f32(raw[i] >> 16);
+            lo0 = fminf(lo0, x0);
+            hi0 = fmaxf(hi0, x0);
+            lo1 = fminf(lo1, x1);
+            hi1 = fmaxf(hi1, x1);
+        }
+    }
+    s_lo[q][2 * cp] = lo0;
+    s_lo[q][2 * cp + 1] = lo1;
+    s_hi[q][2 * cp] = hi0;
+    s_hi[q][2 * cp + 1] = hi1;
+    __syncthreads();
+    float lo[2], hi[2], ig[2], gsc[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int d = 2 * cp + j;
+        lo[j] = fminf(fminf(s_lo[0][d], s_lo[1][d]), fminf(s_lo[2][d], s_lo[3][d]));
+        hi[j] = fmaxf(fmaxf(s_hi[0][d], s_hi[1][d]), fmaxf(s_hi[2][d], s_hi[3][d]));
+        if (lo[j] == 0.0f) lo[j] = 0.0f;  // -0 -> +0
+        if (hi[j] == 0.0f) hi[j] = 0.0f;
+        gsc[j] = hi[j] - lo[j];
+        ig[j] = range_recip(gsc[j]);
+    }
+    const size_t pm = (((size_t)b * Hkv + h) * geo.n_pages + p) * kHeadDim + 2 * cp;
+    if (q == 0) {
+        *reinterpret_cast<float2 *>(gmin_a + pm) = make_float2(lo[0], lo[1]);
+        *reinterpret_cast<float2 *>(gsc_a + pm) = make_float2(gsc[0], gsc[1]);
+    }
+
+    const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
+
+    // ---- stages 2-4, chunk by chunk ----
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        const int i0 = 32 * c;
+        const int cnt = max(0, min(kChunk, mine - i0));
+        if (cnt == 0) continue;  // uniform within the wavefront
+        float X[2][kChunk];
+        float mu[2], sig[2], is[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            float sum = 0.0f;
+#pragma unroll
+            for (int i = 0; i < kChunk; ++i) {
+                const uint32_t w = raw[i0 + i];
+                const float x = bf16_to_f32(j == 0 ? (w & 0xffffu) : (w >> 16));
+                X[j][i] = mul_rn(x - lo[j], ig[j]);
+                if (i < cnt) sum = sum + X[j][i];
+            }
+            mu[j] = sum / (float)cnt;
+            float s = 0.0f;
+#pragma unroll
+            for (int i = 0; i < kChunk; ++i)
+                if (i < cnt) s = fmaxf(s, fabsf(X[j][i] - mu[j]));
+            sig[j] = s;
+            is[j] = range_recip(s);
+        }
+        const size_t cm = (((size_t)b * Hkv + h) * geo.n_chunks + (size_t)t0 / kChunk + 2 * q + c) * kHeadDim + 2 * cp;
+        *reinterpret_cast<float2 *>(mu_a + cm) = make_float2(mu[0], mu[1]);
+        *reinterpret_cast<float2 *>(sig_a + cm) = make_float2(sig[0], sig[1]);
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) {
+            if (i < cnt) {  // uniform within the wavefront
+                uint32_t qa[2], qr[2];
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const float xc = X[j][i] - mu[j];
+                    float xf = fabsf(mul_rn(xc, is[j]));
+                    xf = xf > 1.0f ? 1.0f : xf;
+                    // the number of thresholds <= xf: binary search over the
+                    // 127 sorted thresholds (a NaN counts none)
+                    int I = 0;
+#pragma unroll
+                    for (int step = 64; step >= 1; step >>= 1)
+                        if (s_theta[I + step - 1] <= xf) I += step;
+                    split(I, xc, qa[j], qr[j]);
+                }
+                const int t = t0 + 64 * q + i0 + i;
+                int blk, tb;
+                if (LAYOUT == 0) {
+                    blk = bt_row[0];
+                    tb = t;
+                } else {
+                    const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
+                    blk = bt_row[bi];
+                    tb = t - bi * geo.bt;
+                }
+                if (blk >= 0 && blk < geo.num_blocks) {
+                    const size_t off = (((size_t)blk * Hkv + h) * geo.bt + tb) * kNibbleRow + cp;
+                    anc[off] = (uint8_t)(qa[0] | (qa[1] << 4));
+                    res[off] = (uint8_t)(qr[0] | (qr[1] << 4));
+                }
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ int sext4(uint32_t nib) { return (int)nib >= 8 ? (int)nib - 16 : (int)nib; }
+
+// Dequantization to BF16 [T][Hkv][128]: thread (token row, 8 dims), per
+// dimension I' = 16 V (anchor) or 16 V - Q_res (merged code), level from
+// the table, x = ((+-level * sigma) + mu) * gscale + gmin in fp32, rounded to
+// BF16 to nearest even.  FULL 0: anchor nibble planes; 1: code planes.
+template <int FULL, int LAYOUT>
+__global__ __launch_bounds__(kHThreads) void hdequant_kernel(
+    Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
+    const uint8_t *__restrict__ k_plane, const uint8_t *__restrict__ v_plane, HMetaPtrs meta,
+    HTables tab, uint16_t *__restrict__ k_out, uint16_t *__restrict__ v_out) {
+    __shared__ float s_level[128];
+    if (threadIdx.x < 128) s_level[threadIdx.x] = tab.level[threadIdx.x];
+    __syncthreads();
+    const int Hkv = geo.Hkv;
+    const size_t per = (size_t)T * Hkv * 16;  // (token, head, 8-dim piece) items per tensor
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
+    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * per; e += stride) {
+        const int which = e >= per ? 1 : 0;
+        const size_t r = e - (size_t)which * per;
+        const int d8 = (int)(r & 15);
+        const size_t th = r >> 4;  // t * Hkv + h
+        const int h = (int)(th % Hkv);
+        const int t = (int)(th / Hkv);
+        int blk, tb;
+        if (LAYOUT == 0) {
+            blk = bt_row[0];
+            tb = t;
+        } else {
+            const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
+            blk = bt_row[bi];
+            tb = t - bi * geo.bt;
+        }
+        if (blk < 0 || blk >= geo.num_blocks) continue;
+        const size_t row = ((size_t)blk * Hkv + h) * geo.bt + tb;
+        const uint8_t *plane = which == 0 ? k_plane : v_plane;
+        int qa[8], qr[8];
+        if (FULL) {
+            const uint2 cw = *reinterpret_cast<const uint2 *>(plane + row * kCodeRow + 8 * d8);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const uint32_t c = ((j < 4 ? cw.x : cw.y) >> (8 * (j & 3))) & 0xffu;
+                qa[j] = sext4(c >> 4);
+                qr[j] = sext4(c & 15u);
+            }
+        } else {
+            const uint32_t w = *reinterpret_cast<const uint32_t *>(plane + row * kNibbleRow + 4 * d8);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                qa[j] = sext4((w >> (4 * j)) & 15u);
+                qr[j] = 0;
+            }
+        }
+        const size_t pm = (((size_t)b * Hkv + h) * geo.n_pages + t / kPage) * kHeadDim + 8 * d8;
+        const size_t cm = (((size_t)b * Hkv + h) * geo.n_chunks + t / kChunk) * kHeadDim + 8 * d8;
+        const float *gmin_a = which == 0 ? meta.k_gmin : meta.v_gmin;
+        const float *gsc_a = which == 0 ? meta.k_gscale : meta.v_gscale;
+        const float *mu_a = which == 0 ? meta.k_mu : meta.v_mu;
+        const float *sig_a = which == 0 ? meta.k_sigma : meta.v_sigma;
+        float gm[8], gs[8], mu[8], sg[8];
+#pragma unroll
+        for (int k4 = 0; k4 < 2; ++k4) {
+            const float4 a = *reinterpret_cast<const float4 *>(gmin_a + pm + 4 * k4);
+            const float4 s = *reinterpret_cast<const float4 *>(gsc_a + pm + 4 * k4);
+            const float4 m = *reinterpret_cast<const float4 *>(mu_a + cm + 4 * k4);
+            const float4 g = *reinterpret_cast<const float4 *>(sig_a + cm + 4 * k4);
+            gm[4 * k4] = a.x; gm[4 * k4 + 1] = a.y; gm[4 * k4 + 2] = a.z; gm[4 * k4 + 3] = a.w;
+            gs[4 * k4] = s.x; gs[4 * k4 + 1] = s.y; gs[4 * k4 + 2] = s.z; gs[4 * k4 + 3] = s.w;
+            mu[4 * k4] = m.x; mu[4 * k4 + 1] = m.y; mu[4 * k4 + 2] = m.z; mu[4 * k4 + 3] = m.w;
+            sg[4 * k4] = g.x; sg[4 * k4 + 1] = g.y; sg[4 * k4 + 2] = g.z; sg[4 * k4 + 3] = g.w;
+        }
+        uint32_t o[4];
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) {
+            uint32_t hb[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int a = qa[j + u];
+                const int V = a >= 0 ? a : -a - 1;
+                int Ip = 16 * V - qr[j + u];
+                Ip = Ip < 0 ? 0 : (Ip > 127 ? 127 : Ip);
+                const float m = a >= 0 ? s_level[Ip] : -s_level[Ip];
+                const float xc = mul_rn(m, sg[j + u]);
+                const float X = xc + mu[j + u];
+                const float x = mul_rn(X, gs[j + u]) + gm[j + u];
+                hb[u] = bf16_rne(x);
+            }
+            o[j / 2] = hb[0] | (hb[1] << 16);
+        }
+        uint16_t *out = which == 0 ? k_out : v_out;
+        *reinterpret_cast<uint4 *>(out + ((size_t)t * Hkv + h) * kHeadDim + 8 * d8) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+}
+
+int shift_of(int bt) {
+    for (int sh = 0; sh < 31; ++sh)
+        if ((1 << sh) == bt) return sh;
+    return -1;
+}
+
+}  // namespace
+
+void make_htables(float alpha, HTables *t) {
+    const double la = log1p((double)alpha);
+    for (int k = 0; k < 127; ++k) t->theta[k] = (float)(expm1(((k + 0.5) / 127.0) * la) / (double)alpha);
+    t->theta[127] = INFINITY;
+    for (int i = 0; i < 128; ++i) t->level[i] = (float)(expm1((i / 127.0) * la) / (double)alpha);
+}
+
+hipError_t launch_hencode(const Geometry &g, int b, int T, const int32_t *block_table,
+                          const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
+                          uint8_t *k_res, uint8_t *v_res, HMetaPtrs meta, const HTables &tab,
+                          hipStream_t stream) {
+    if (T <= 0) return hipSuccess;
+    dim3 grid(g.Hkv, (T + kPage - 1) / kPage, 2);
+    if (g.max_blocks == 1)
+        hipLaunchKernelGGL(hencode_kernel<0>, grid, dim3(kHThreads), 0, stream, g, b, T, shift_of(g.bt),
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta, tab);
+    else
+        hipLaunchKernelGGL(hencode_kernel<1>, grid, dim3(kHThreads), 0, stream, g, b, T, shift_of(g.bt),
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta, tab);
+    return hipGetLastError();
+}
+
+hipError_t launch_hdequant(bool full, const Geometry &g, int b, int T, const int32_t *block_table,
+                           const uint8_t *k_plane, const uint8_t *v_plane, HMetaPtrs meta,
+                           const HTables &tab, uint16_t *k_out, uint16_t *v_out,
+                           hipStream_t stream) {
+    if (T <= 0) return hipSuccess;
+    size_t blocks = ((size_t)2 * T * g.Hkv * 16 + kHThreads - 1) / kHThreads;
+    if (blocks > 256 * 32) blocks = 256 * 32;
+    const dim3 grid((unsigned)blocks);
+    const int sh = shift_of(g.bt);
+    if (full) {
+        if (g.max_blocks == 1)
+            hipLaunchKernelGGL((hdequant_kernel<1, 0>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
+                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+        else
+            hipLaunchKernelGGL((hdequant_kernel<1, 1>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
+                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+    } else {
+        if (g.max_blocks == 1)
+            hipLaunchKernelGGL((hdequant_kernel<0, 0>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
+                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+        else
+            hipLaunchKernelGGL((hdequant_kernel<0, 1>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
+                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace lynx

@@ -21,6 +21,8 @@ struct Geometry {
     int num_blocks;    // valid block ids are [0, num_blocks)
     int max_tokens;    // metadata token stride
     int n_groups;      // ceil(max_tokens / 128): K metadata group stride
+    int n_pages;       // ceil(max_tokens / 256): hierarchical page stride
+    int n_chunks;      // ceil(max_tokens / 32): hierarchical chunk stride
 };
 
 struct MetaPtrs {
@@ -34,6 +36,28 @@ hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_t
 
 hipError_t launch_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t n_packed,
                         hipStream_t stream);
+
+// ---- hierarchical codec of Alg. 1 (hier.hip) ----------------------------------
+struct HMetaPtrs {
+    float *k_gmin, *k_gscale, *k_mu, *k_sigma;  // [B][Hkv][n_pages][128], [B][Hkv][n_chunks][128]
+    float *v_gmin, *v_gscale, *v_mu, *v_sigma;
+};
+// Per-alpha tables: decision thresholds theta[0..126] (theta[127] = +inf) and
+// reconstruction levels level[0..127], each the fp32 value of
+// expm1((k + 0.5) / 127 * log1p(alpha)) / alpha, expm1(i / 127 * log1p(alpha)) / alpha.
+struct HTables {
+    float theta[128];
+    float level[128];
+};
+void make_htables(float alpha, HTables *t);
+hipError_t launch_hencode(const Geometry &g, int b, int T, const int32_t *block_table,
+                          const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
+                          uint8_t *k_res, uint8_t *v_res, HMetaPtrs meta, const HTables &tab,
+                          hipStream_t stream);
+hipError_t launch_hdequant(bool full, const Geometry &g, int b, int T, const int32_t *block_table,
+                           const uint8_t *k_plane, const uint8_t *v_plane, HMetaPtrs meta,
+                           const HTables &tab, uint16_t *k_out, uint16_t *v_out,
+                           hipStream_t stream);
 
 // ---- serializer / deserializer (codec.hip) -----------------------------------
 // Object: tokens t0 .. t0 + n - 1 of one sequence, all kv heads.  Anchor

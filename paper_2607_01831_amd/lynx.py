@@ -42,6 +42,11 @@ class lynx_meta(ctypes.Structure):
 _lib = None
 
 
+class lynx_hmeta(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in
+                ("k_gmin", "k_gscale", "k_mu", "k_sigma", "v_gmin", "v_gscale", "v_mu", "v_sigma")]
+
+
 def load():
     """Load liblynx.so (raises if it has not been built)."""
     global _lib
@@ -69,6 +74,10 @@ def load():
         "lynx_kv_serialize": ([I32, I32, P, P, P, P, P], ctypes.c_int),
         "lynx_kv_deserialize_anchor": ([LP, I32, I32, I32, P, P, P, P, MP, P], ctypes.c_int),
         "lynx_kv_deserialize_residual": ([LP, I32, I32, I32, P, P, P, P, P, P, P], ctypes.c_int),
+        "lynx_hkv_encode": ([LP, I32, I32, P, P, P, ctypes.c_float, P, P, P, P,
+                             ctypes.POINTER(lynx_hmeta), P], ctypes.c_int),
+        "lynx_hkv_dequant": ([LP, I32, I32, P, I32, P, P, ctypes.c_float,
+                              ctypes.POINTER(lynx_hmeta), P, P, P], ctypes.c_int),
         "lynx_strerror": ([ctypes.c_int], ctypes.c_char_p),
     }
     for name, (args, res) in sigs.items():
@@ -241,6 +250,48 @@ def lynx_attn_verify(L: Layout, B: int, Hq: int, k: int, max_seq_len: int, seq_l
 # ----------------------------------------------------------------------------
 # Allocation helpers (torch device memory only)
 # ----------------------------------------------------------------------------
+
+@dataclass
+class HMeta:
+    """fp32 metadata of the hierarchical codec (device): page minimum and
+    range [B][Hkv][ceil(max_tokens/256)][128], chunk mean and scale
+    [B][Hkv][ceil(max_tokens/32)][128], for K and V."""
+    k_gmin: torch.Tensor
+    k_gscale: torch.Tensor
+    k_mu: torch.Tensor
+    k_sigma: torch.Tensor
+    v_gmin: torch.Tensor
+    v_gscale: torch.Tensor
+    v_mu: torch.Tensor
+    v_sigma: torch.Tensor
+
+    @staticmethod
+    def empty(L: Layout, B: int, device="cuda") -> "HMeta":
+        pg = (B, L.num_kv_heads, -(-L.max_tokens // 256), HEAD_DIM)
+        ch = (B, L.num_kv_heads, -(-L.max_tokens // 32), HEAD_DIM)
+        z = lambda shape: torch.zeros(shape, dtype=torch.float32, device=device)
+        return HMeta(z(pg), z(pg), z(ch), z(ch), z(pg), z(pg), z(ch), z(ch))
+
+    def c(self) -> lynx_hmeta:
+        return lynx_hmeta(*(_ptr(getattr(self, f)) for f, _ in lynx_hmeta._fields_))
+
+
+def lynx_hkv_encode(L: Layout, b: int, T: int, block_table, k, v, alpha: float, k_anc, v_anc,
+                    k_res, v_res, hmeta: HMeta, stream=None) -> None:
+    lay, met = L.c(), hmeta.c()
+    _check("lynx_hkv_encode", load().lynx_hkv_encode(
+        ctypes.byref(lay), b, T, _ptr(block_table), _ptr(k), _ptr(v), alpha, _ptr(k_anc),
+        _ptr(v_anc), _ptr(k_res), _ptr(v_res), ctypes.byref(met), _stream(stream)))
+
+
+def lynx_hkv_dequant(L: Layout, b: int, T: int, block_table, full: bool, k_plane, v_plane,
+                     alpha: float, hmeta: HMeta, k_out, v_out, stream=None) -> None:
+    """k_out, v_out: BF16 [T][Hkv][128] (device, written)."""
+    lay, met = L.c(), hmeta.c()
+    _check("lynx_hkv_dequant", load().lynx_hkv_dequant(
+        ctypes.byref(lay), b, T, _ptr(block_table), 1 if full else 0, _ptr(k_plane), _ptr(v_plane),
+        alpha, ctypes.byref(met), _ptr(k_out), _ptr(v_out), _stream(stream)))
+
 
 def lynx_serialized_bytes(num_kv_heads: int, n_tokens: int) -> tuple[int, int]:
     """(anchor_bytes, residual_bytes) of an object of n_tokens tokens."""

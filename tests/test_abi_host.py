@@ -178,3 +178,30 @@ def test_serdes_sizes_and_validation(lib):
                                             None) == E.LYNX_EINVAL
     assert lib.lynx_kv_deserialize_residual(ctypes.byref(lay), 0, 0, 4, 16, None, 16, 16, 16, 16,
                                             None) == E.LYNX_EINVAL
+
+
+def test_hierarchical_codec_validation(lib):
+    """The hierarchical encode / dequant reject bad arguments before
+    launching anything (no pointer below is dereferenced)."""
+    from paper_2607_01831_amd import lynx
+    E = lynx
+    L = _layout(max_blocks_per_seq=16, num_blocks=64, max_tokens=256)
+    lay = L.c()
+    hm = lynx.lynx_hmeta(*[16 * (i + 1) for i in range(8)])
+    enc = lambda alpha=255.0, T=10, hmp=ctypes.byref(hm), planes=(16, 16, 16, 16): lib.lynx_hkv_encode(
+        ctypes.byref(lay), 0, T, 16, 16, 16, alpha, *planes, hmp, None)
+    assert enc(alpha=0.0) == E.LYNX_EINVAL
+    assert enc(alpha=-1.0) == E.LYNX_EINVAL
+    assert enc(alpha=float("nan")) == E.LYNX_EINVAL
+    assert enc(T=257) == E.LYNX_EINVAL
+    assert enc(hmp=None) == E.LYNX_EINVAL
+    assert enc(planes=(16, 16, 24, 16)) == E.LYNX_EINVAL
+    bad = lynx.lynx_hmeta(16, 32, 48, 64, 80, 96, 112, 0)
+    assert enc(hmp=ctypes.byref(bad)) == E.LYNX_EINVAL
+    assert enc(T=0) == E.LYNX_OK
+    deq = lambda full=1, alpha=255.0, T=10: lib.lynx_hkv_dequant(
+        ctypes.byref(lay), 0, T, 16, full, 16, 16, alpha, ctypes.byref(hm), 16, 16, None)
+    assert deq(full=2) == E.LYNX_EINVAL
+    assert deq(alpha=0.0) == E.LYNX_EINVAL
+    assert deq(T=300) == E.LYNX_EINVAL
+    assert deq(T=0) == E.LYNX_OK
