@@ -88,6 +88,8 @@ def parse():
                    help="skip the decode-with-tail and draft-acceptance stages")
     p.add_argument("--paged-calls", type=int, default=20,
                    help="timed paged batch-decode calls (paged-b16-16k-64k; 0 skips the stage)")
+    p.add_argument("--no-hier", dest="hier", action="store_false",
+                   help="skip the hierarchical-codec stage")
     p.add_argument("--no-serdes", dest="serdes", action="store_false",
                    help="skip the serializer / deserializer pipeline stage")
     p.add_argument("--no-overlap-70b", dest="overlap_70b", action="store_false",
@@ -612,6 +614,98 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
     return {"serdes_pipeline": r}
 
 
+def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0, 1.0)):
+    """The paper's own hierarchical codec (Alg. 1) on the workload's layers:
+    encode, and dequantization of the anchor alone and of the merged codes
+    to BF16 pages, each timed over all layers in turn (HIP events); then the
+    compression error vNMSE = E ||o - o_hat||^2 / ||o_hat||^2 of the attention
+    output of each layer's decode query (first four layers, every query head)
+    for both codecs against the exact BF16 cache: the uniform codec through
+    the anchor-decode and verify kernels, the hierarchical one through its
+    BF16 pages and plain fp32 attention.  alpha is not given by the paper;
+    the first value is the one timed."""
+    import torch
+
+    from paper_2607_01831_amd import lynx
+
+    table = torch.zeros(1, 1, dtype=torch.int32, device=dev)
+    lens = torch.tensor([T], dtype=torch.int32, device=dev)
+    hp = lynx.KVPool.allocate(L, 1, device=dev)
+    hm = lynx.HMeta.empty(L, 1, device=dev)
+    ko = torch.empty(T, Hkv, 128, dtype=torch.bfloat16, device=dev)
+    vo = torch.empty_like(ko)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    a0 = alphas[0]
+
+    def timed(fn, reps=2):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = ev(), ev()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * n_layers)
+
+    enc = lambda: [lynx.lynx_hkv_encode(L, 0, T, table, K[l], V[l], a0, hp.k_anc, hp.v_anc, hp.k_res,
+                                        hp.v_res, hm) for l in range(n_layers)]
+    t_enc = timed(enc)
+    hp.merge()
+    t_da = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, False, hp.k_anc, hp.v_anc, a0, hm, ko, vo)
+                          for _ in range(n_layers)])
+    t_df = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, True, hp.k_codes, hp.v_codes, a0, hm, ko, vo)
+                          for _ in range(n_layers)])
+    elems = T * Hkv * 128 * 2
+    meta_b = 4.0 * 2 * (1 / 256 + 1 / 32)          # page and chunk fp32 pairs per element
+    r = {"alpha": a0,
+         "encode_us_per_layer": round(t_enc, 2),
+         "encode_GBps": round(elems * (2 + 1 + meta_b) / (t_enc * 1e-6) / 1e9, 1),
+         "dequant_anchor_us_per_layer": round(t_da, 2),
+         "dequant_anchor_GBps": round(elems * (0.5 + meta_b + 2) / (t_da * 1e-6) / 1e9, 1),
+         "dequant_full_us_per_layer": round(t_df, 2),
+         "dequant_full_GBps": round(elems * (1 + meta_b + 2) / (t_df * 1e-6) / 1e9, 1)}
+
+    G = Hq // Hkv
+
+    def attn(q, k, v):
+        """fp32 attention of one decode query [Hq][128] over BF16 k, v [T][Hkv][128]."""
+        kf = k.float().repeat_interleave(G, dim=1).permute(1, 0, 2)   # [Hq][T][128]
+        vf = v.float().repeat_interleave(G, dim=1).permute(1, 0, 2)
+        s = torch.einsum("hd,htd->ht", q.float(), kf) / 128 ** 0.5
+        return torch.einsum("ht,htd->hd", torch.softmax(s, dim=1), vf)
+
+    def vnmse(o, o_hat):
+        return float(((o - o_hat).pow(2).sum(dim=-1) / o_hat.pow(2).sum(dim=-1)).mean())
+
+    acc = {}
+    out = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device=dev)
+    outv = torch.empty(1, 1, Hq, 128, dtype=torch.bfloat16, device=dev)
+    ws = lynx.workspace(L, 1, Hq, 1, T, device=dev)
+    layers = range(min(4, n_layers))
+    for l in layers:
+        q = Q[l][0]
+        o = attn(q, K[l], V[l])
+        p = pools[l]
+        lynx.lynx_attn_anchor_decode(L, 1, Hq, T, lens, table, p.k_anc, p.v_anc, p.meta, Q[l], out, None, ws)
+        acc.setdefault("uniform_anchor", []).append(vnmse(o, out[0].float()))
+        lynx.lynx_attn_verify(L, 1, Hq, 1, T, lens, table, p.k_codes, p.v_codes, p.meta,
+                              Q[l].view(1, 1, Hq, 128), None, None, outv, ws)
+        acc.setdefault("uniform_full", []).append(vnmse(o, outv[0, 0].float()))
+        for a in alphas:
+            lynx.lynx_hkv_encode(L, 0, T, table, K[l], V[l], a, hp.k_anc, hp.v_anc, hp.k_res, hp.v_res, hm)
+            hp.merge()
+            for mode, full, (kp, vp) in (("anchor", False, (hp.k_anc, hp.v_anc)),
+                                         ("full", True, (hp.k_codes, hp.v_codes))):
+                lynx.lynx_hkv_dequant(L, 0, T, table, full, kp, vp, a, hm, ko, vo)
+                acc.setdefault(f"hier_{mode}_alpha{a:g}", []).append(vnmse(o, attn(q, ko, vo)))
+    torch.cuda.synchronize()
+    r["vnmse"] = {k: float(f"{sum(v) / len(v):.3g}") for k, v in acc.items()}
+    r["vnmse_layers"] = len(layers)
+    del hp, hm, ko, vo
+    return {"hier_codec": r}
+
+
 def cpu_baseline(w, layer_inputs, n_layers):
     """The CPU oracle, untuned, timed on this host on a bounded sample: the
     anchor decode of the first n_layers layers (all kv heads)."""
@@ -773,6 +867,7 @@ def main():
     paged = paged_decode_stage(args.paged_calls, dev) if args.paged_calls > 0 else None
     ovl = overlap_70b_stage(dev) if args.overlap_70b else None
     serdes = serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side) if args.serdes else None
+    hier = hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers) if args.hier else None
 
     # The speculative decoder's own pieces, timed alone: decode over the
     # anchors plus the 8 BF16 tokens it generated (32 layers), and greedy
@@ -864,6 +959,7 @@ def main():
             **(paged or {}),
             **(ovl or {}),
             **(serdes or {}),
+            **(hier or {}),
             **spec,
             "decode_hidden_behind_h2d": round(overlap, 3),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
