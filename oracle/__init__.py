@@ -61,13 +61,13 @@ def _load():
     lib.oracle_anchor_decode_tail.restype = I
     F = ctypes.c_float
     IP = ctypes.POINTER(ctypes.c_int)
-    lib.oracle_hsplit.argtypes = [I, I, IP, IP]
-    lib.oracle_hsplit.restype = None
-    lib.oracle_htables.argtypes = [F, P, P]
-    lib.oracle_htables.restype = None
-    lib.oracle_hencode.argtypes = [I, I, I, I, I, I, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_hsplit.argtypes = [I, I, I, IP, IP]
+    lib.oracle_hsplit.restype = I
+    lib.oracle_htables.argtypes = [F, I, P, P, P]
+    lib.oracle_htables.restype = I
+    lib.oracle_hencode.argtypes = [I, I, I, I, I, I, P, P, P, F, I, P, P, P, P, P, P, P, P, P, P, P, P]
     lib.oracle_hencode.restype = I
-    lib.oracle_hdequant.argtypes = [I, I, I, I, I, I, I, P, P, P, F, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_hdequant.argtypes = [I, I, I, I, I, I, I, I, P, P, P, F, P, P, P, P, P, P, P, P, P, P]
     lib.oracle_hdequant.restype = I
     _LIB = lib
     return lib
@@ -394,9 +394,10 @@ def deserialize_residual(L: Layout, b: int, t0: int, n: int, block_table: np.nda
 
 # --------------------------------------------------------------------------
 # Hierarchical non-linear codec (Alg. 1, Sec. 4.1): pages of 256 tokens and
-# chunks of 32 per channel, alpha-law transform to 7 bits and a sign, split
-# into a signed 4-bit anchor and a signed 4-bit correction.  The readings of
-# the garbled parts of the listing are stated in lynx_oracle.c.
+# chunks of 32 per channel, alpha-law transform to a magnitude code and a
+# sign, split into a signed 4-bit anchor and a signed 4-bit correction.  The
+# variants of the split and the readings of the garbled parts of the listing
+# are stated in lynx_oracle.c.
 # --------------------------------------------------------------------------
 
 H_PAGE = 256
@@ -427,47 +428,63 @@ class HMeta:
                                   self.v_gmin, self.v_gscale, self.v_mu, self.v_sigma)]
 
 
-def hsplit(I: int, S: int):
+H_VARIANTS = {"biased": 0, "centred": 1, "int4": 2}
+
+
+def _variant(variant) -> int:
+    return H_VARIANTS[variant] if isinstance(variant, str) else int(variant)
+
+
+def hsplit(I: int, S: int, variant="biased"):
     """Stage 4 of Alg. 1 for one code: (anchor, residual) nibble values."""
     a, r = ctypes.c_int(), ctypes.c_int()
-    _load().oracle_hsplit(int(I), int(S), ctypes.byref(a), ctypes.byref(r))
+    rc = _load().oracle_hsplit(_variant(variant), int(I), int(S), ctypes.byref(a), ctypes.byref(r))
+    if rc != 0:
+        raise ValueError(f"oracle_hsplit rejected ({variant}, {I})")
     return a.value, r.value
 
 
-def htables(alpha: float):
-    """(decision thresholds [127], reconstruction levels [128]) for alpha."""
+def htables(alpha: float, variant="biased"):
+    """(decision thresholds [M], reconstruction levels [M + 1], the centred
+    split's anchor-only levels [8]) for alpha; M = 127, or 7 for 'int4'."""
     theta = np.zeros(127, np.float32)
     level = np.zeros(128, np.float32)
-    _load().oracle_htables(alpha, _ptr(theta), _ptr(level))
-    return theta, level
+    alevel = np.zeros(8, np.float32)
+    M = _load().oracle_htables(alpha, _variant(variant), _ptr(theta), _ptr(level), _ptr(alevel))
+    if M < 0:
+        raise ValueError(f"unknown variant {variant}")
+    return theta[:M].copy(), level[:M + 1].copy(), alevel
 
 
 def hencode(L: Layout, b: int, T: int, block_table: np.ndarray, k_bits: np.ndarray,
-            v_bits: np.ndarray, alpha: float, planes: dict, hmeta: HMeta) -> None:
+            v_bits: np.ndarray, alpha: float, planes: dict, hmeta: HMeta,
+            variant="biased") -> None:
     """Hierarchical encode of sequence b (k_bits, v_bits: uint16 [T][Hkv][128])
-    into planes['k_anc'|'v_anc'|'k_res'|'v_res'] and hmeta row b."""
+    into planes['k_anc'|'v_anc'|'k_res'|'v_res'] ('int4': the anchor planes
+    only) and hmeta row b."""
     bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
     k_bits = np.ascontiguousarray(k_bits, dtype=np.uint16)
     v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
     assert k_bits.shape == (T, L.Hkv, HEAD_DIM) and v_bits.shape == k_bits.shape
     rc = _load().oracle_hencode(L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T, _ptr(bt_arr),
-                                _ptr(k_bits), _ptr(v_bits), alpha, _ptr(planes["k_anc"]),
-                                _ptr(planes["v_anc"]), _ptr(planes["k_res"]), _ptr(planes["v_res"]),
-                                *hmeta.ptrs())
+                                _ptr(k_bits), _ptr(v_bits), alpha, _variant(variant),
+                                _ptr(planes["k_anc"]), _ptr(planes["v_anc"]),
+                                _ptr(planes.get("k_res")), _ptr(planes.get("v_res")), *hmeta.ptrs())
     if rc != 0:
         raise ValueError(f"oracle_hencode rejected its arguments ({rc})")
 
 
 def hdequant(mode: str, L: Layout, b: int, T: int, block_table: np.ndarray,
-             k_plane: np.ndarray, v_plane: np.ndarray, alpha: float, hmeta: HMeta):
+             k_plane: np.ndarray, v_plane: np.ndarray, alpha: float, hmeta: HMeta,
+             variant="biased"):
     """Reconstructed K, V of sequence b as BF16 bits (uint16 [T][Hkv][128]):
     mode 'anchor' from the anchor nibble planes, 'full' from the merged code
-    planes."""
+    planes (not for 'int4')."""
     m = {"anchor": 0, "full": 1}[mode]
     bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
     k_out = np.zeros((T, L.Hkv, HEAD_DIM), np.uint16)
     v_out = np.zeros_like(k_out)
-    rc = _load().oracle_hdequant(m, L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T, _ptr(bt_arr),
+    rc = _load().oracle_hdequant(m, _variant(variant), L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T, _ptr(bt_arr),
                                  _ptr(k_plane), _ptr(v_plane), alpha, *hmeta.ptrs(), _ptr(k_out),
                                  _ptr(v_out))
     if rc != 0:

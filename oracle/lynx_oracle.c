@@ -515,37 +515,64 @@ int oracle_verify(int Hkv, int bt, int max_blocks, int max_tokens, int B, int Hq
  *   2. chunk isolation: mu = the mean of X over the chunk's tokens (an fp32
  *      sum in token order divided by the count), Xc = X - mu,
  *      sigma = max |Xc|, Xf = Xc * (1 / sigma), so |Xf| <= 1;
- *   3. non-linear transform: I = Round(127 ln(1 + a |Xf|) / ln(1 + a)), the
- *      sign S of Xc;
- *   4. split: V = (I + 7) >> 4 (the anchor magnitude, rounded half down),
- *      Q_res = 16 V - I (the correction), Q_anc = V for S >= 0 and -V - 1 for
- *      S < 0, both kept as 4-bit two's complement nibbles.
+ *   3. non-linear transform: I = Round(M ln(1 + a |Xf|) / ln(1 + a)), the
+ *      sign S of Xc, with M = 127 (seven magnitude bits and a sign);
+ *   4. split into a signed 4-bit anchor and a signed 4-bit residual, both
+ *      kept as two's complement nibbles; the anchor is the magnitude's
+ *      bucket V with the sign-aware map Q_anc = V for S >= 0 and -V - 1 for
+ *      S < 0, so a zero magnitude keeps its sign.
+ * Three variants of stage 4 (the variant argument):
+ *   0 (biased): the listing's split: V = (I + 7) >> 4, the magnitude rounded
+ *     half down to a multiple of 16, Q_res = 16 V - I.  V reaches 8 for
+ *     I >= 121, which 4 bits cannot hold with a sign: V is clamped to 7 and
+ *     Q_res to [-8, 7], so codes above 120 come back as 120.  The anchor
+ *     alone reconstructs code 16 V; anchor and residual 16 V - Q_res.
+ *   1 (centred): the lossless split that keeps all 128 magnitudes: V = I >> 4
+ *     (the top three magnitude bits: the anchor is the sign and the top
+ *     bits of the 8-bit code), Q_res = I - 16 V - 8, a correction centred on
+ *     the bucket's middle.  The anchor alone reconstructs code 16 V + 7.5,
+ *     the bucket's centre; anchor and residual 16 V + 8 + Q_res = I.  The
+ *     merged byte is then a complete 8-bit code: the single-precision 8-bit
+ *     configuration of Sec. 6.1.
+ *   2 (4-bit): the single-precision 4-bit configuration of Sec. 6.1: stage 3
+ *     with M = 7 (three magnitude bits and a sign), the anchor holding
+ *     Q = I or -I - 1 and no residual.
  * Readings where the listing is garbled or at odds with the 4-bit streams:
  *   - the sign is that of the centred value Xc (the listing's X_view is
  *     non-negative after stage 1);
  *   - no epsilon: a page (chunk) whose range (sigma) has no finite positive
  *     reciprocal normalizes to 0;
  *   - Round(Y) is decided as the number of decision thresholds theta_k
- *     (k = 0..126) with theta_k <= |Xf|, theta_k being the fp32 value of
- *     expm1(((k + 0.5) / 127) * log1p(a)) / a in IEEE double: the point
+ *     (k = 0..M-1) with theta_k <= |Xf|, theta_k being the fp32 value of
+ *     expm1(((k + 0.5) / M) * log1p(a)) / a in IEEE double: the point
  *     where the transform equals k + 1/2;
- *   - V reaches 8 for I >= 121, which 4 bits cannot hold with a sign: V is
- *     clamped to 7 and Q_res to [-8, 7], so codes above 120 come back as 120;
- *   - reconstruction maps I' = 16 V - Q_res (anchor only: I' = 16 V) to the
- *     level expm1((I' / 127) * log1p(a)) / a (fp32 of the double value),
- *     then x = ((+-level * sigma) + mu) * gscale + gmin, each step an fp32
+ *   - reconstruction maps a code index i to the level
+ *     expm1((i / M) * log1p(a)) / a (fp32 of the double value), then
+ *     x = ((+-level * sigma) + mu) * gscale + gmin, each step an fp32
  *     operation, rounded to BF16 to nearest even.
  */
 #define H_PAGE 256
 #define H_CHUNK 32
 
-static void h_tables(float alpha, float *theta, float *level)
+#define H_BIASED 0
+#define H_CENTRED 1
+#define H_INT4 2
+
+/* Magnitude levels M of stage 3: 127 (8-bit code), 7 (4-bit code). */
+static int h_levels(int variant) { return variant == H_INT4 ? 7 : 127; }
+
+/* Decision thresholds theta[0..M-1], levels level[0..M] and the centred
+ * split's anchor-only levels alevel[V] (code 16 V + 7.5, V = 0..7). */
+static void h_tables(float alpha, int variant, float *theta, float *level, float *alevel)
 {
     const double la = log1p((double)alpha);
-    for (int k = 0; k < 127; ++k)
-        theta[k] = (float)(expm1(((k + 0.5) / 127.0) * la) / (double)alpha);
-    for (int i = 0; i < 128; ++i)
-        level[i] = (float)(expm1((i / 127.0) * la) / (double)alpha);
+    const int M = h_levels(variant);
+    for (int k = 0; k < M; ++k)
+        theta[k] = (float)(expm1(((k + 0.5) / M) * la) / (double)alpha);
+    for (int i = 0; i <= M; ++i)
+        level[i] = (float)(expm1(((double)i / M) * la) / (double)alpha);
+    for (int v = 0; v < 8; ++v)
+        alevel[v] = (float)(expm1(((16 * v + 7.5) / 127.0) * la) / (double)alpha);
 }
 
 /* The reciprocal of a range, or 0 when it is not a finite positive value. */
@@ -555,22 +582,37 @@ static float range_recip(float r)
     return (r > 0.0f && v <= FLT_MAX) ? v : 0.0f;
 }
 
-/* Stage 4: the anchor and residual nibble values of (I, S). */
-void oracle_hsplit(int I, int S, int *q_anc, int *q_res)
+/* Stage 4: the anchor and residual nibble values of (I, S).  Returns 0, or
+ * -1 for an unknown variant or a code out of range. */
+int oracle_hsplit(int variant, int I, int S, int *q_anc, int *q_res)
 {
-    int V = (I + 7) >> 4;
-    if (V > 7) V = 7;
-    int r = 16 * V - I;
-    if (r < -8) r = -8;
-    if (r > 7) r = 7;
+    if (variant < H_BIASED || variant > H_INT4 || I < 0 || I > h_levels(variant)) return -1;
+    int V, r;
+    if (variant == H_BIASED) {
+        V = (I + 7) >> 4;
+        if (V > 7) V = 7;
+        r = 16 * V - I;
+        if (r < -8) r = -8;
+        if (r > 7) r = 7;
+    } else if (variant == H_CENTRED) {
+        V = I >> 4;
+        r = I - 16 * V - 8;
+    } else {
+        V = I;
+        r = 0;
+    }
     *q_anc = S < 0 ? -V - 1 : V;
     *q_res = r;
+    return 0;
 }
 
-/* Exposes the decision thresholds (127) and reconstruction levels (128). */
-void oracle_htables(float alpha, float *theta, float *level)
+/* Exposes the decision thresholds (M), reconstruction levels (M + 1) and the
+ * centred split's anchor-only levels (8).  Returns M, or -1. */
+int oracle_htables(float alpha, int variant, float *theta, float *level, float *alevel)
 {
-    h_tables(alpha, theta, level);
+    if (variant < H_BIASED || variant > H_INT4) return -1;
+    h_tables(alpha, variant, theta, level, alevel);
+    return h_levels(variant);
 }
 
 static int sext4(int nib) { return nib >= 8 ? nib - 16 : nib; }
@@ -586,19 +628,22 @@ static uint16_t float_to_bf16_rne(float f)
 
 /*
  * k, v: BF16 bits [T][Hkv][128] of sequence b.  Writes its rows of the
- * anchor and residual nibble planes and its metadata rows: gmin, gscale
+ * anchor and residual nibble planes (variant 2: the anchor plane only; the
+ * residual planes are not touched) and its metadata rows: gmin, gscale
  * [B][Hkv][ceil(max_tokens/256)][128], mu, sigma
  * [B][Hkv][ceil(max_tokens/32)][128], for K and V.  Returns 0, or -1.
  */
 int oracle_hencode(int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
                    const int32_t *block_table, const uint16_t *k, const uint16_t *v, float alpha,
-                   uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
+                   int variant, uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
                    float *k_gmin, float *k_gscale, float *k_mu, float *k_sigma,
                    float *v_gmin, float *v_gscale, float *v_mu, float *v_sigma)
 {
     if (Hkv < 1 || bt < 1 || T < 0 || T > max_tokens || !(alpha > 0.0f)) return -1;
-    float theta[127], level[128];
-    h_tables(alpha, theta, level);
+    if (variant < H_BIASED || variant > H_INT4) return -1;
+    float theta[127], level[128], alevel[8];
+    h_tables(alpha, variant, theta, level, alevel);
+    const int M = h_levels(variant);
     const int n_pages = (max_tokens + H_PAGE - 1) / H_PAGE;
     const int n_chunks = (max_tokens + H_CHUNK - 1) / H_CHUNK;
     const int32_t *bt_row = block_table + (size_t)b * max_blocks;
@@ -651,15 +696,15 @@ int oracle_hencode(int Hkv, int bt, int max_blocks, int max_tokens, int b, int T
                             float xf = fabsf(xc * is);
                             if (xf > 1.0f) xf = 1.0f;
                             int I = 0;
-                            while (I < 127 && theta[I] <= xf) ++I;
+                            while (I < M && theta[I] <= xf) ++I;
                             const int S = xc > 0.0f ? 1 : (xc < 0.0f ? -1 : 0);
                             int qa, qr;
-                            oracle_hsplit(I, S, &qa, &qr);
+                            oracle_hsplit(variant, I, S, &qa, &qr);
                             const int t = t0 + i;
                             if (bt_row[t / bt] < 0) return -1;
                             const size_t row = plane_row_offset(bt_row, Hkv, bt, h, t, NIBBLE_ROW);
                             put_nibble(anc + row, d, qa & 0xF);
-                            put_nibble(res + row, d, qr & 0xF);
+                            if (variant != H_INT4) put_nibble(res + row, d, qr & 0xF);
                         }
                     }
                 }
@@ -670,19 +715,22 @@ int oracle_hencode(int Hkv, int bt, int max_blocks, int max_tokens, int b, int T
 
 /*
  * Reconstruction of sequence b's K and V as BF16 bits [T][Hkv][128]:
- * mode 0 from the anchor nibble planes alone (I' = 16 V), mode 1 from the
- * merged code planes (byte of element e: anchor nibble << 4 | residual
- * nibble; I' = 16 V - Q_res).  Returns 0, or -1.
+ * mode 0 from the anchor nibble planes alone, mode 1 from the merged code
+ * planes (byte of element e: anchor nibble << 4 | residual nibble; not for
+ * variant 2).  The code index is, by variant: 0: 16 V (anchor),
+ * 16 V - Q_res (merged); 1: 16 V + 7.5 (anchor), 16 V + 8 + Q_res (merged);
+ * 2: V.  Returns 0, or -1.
  */
-int oracle_hdequant(int mode, int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
+int oracle_hdequant(int mode, int variant, int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
                     const int32_t *block_table, const uint8_t *k_plane, const uint8_t *v_plane,
                     float alpha, const float *k_gmin, const float *k_gscale, const float *k_mu,
                     const float *k_sigma, const float *v_gmin, const float *v_gscale,
                     const float *v_mu, const float *v_sigma, uint16_t *k_out, uint16_t *v_out)
 {
     if ((mode != 0 && mode != 1) || Hkv < 1 || T < 0 || T > max_tokens || !(alpha > 0.0f)) return -1;
-    float theta[127], level[128];
-    h_tables(alpha, theta, level);
+    if (variant < H_BIASED || variant > H_INT4 || (variant == H_INT4 && mode == 1)) return -1;
+    float theta[127], level[128], alevel[8];
+    h_tables(alpha, variant, theta, level, alevel);
     const int n_pages = (max_tokens + H_PAGE - 1) / H_PAGE;
     const int n_chunks = (max_tokens + H_CHUNK - 1) / H_CHUNK;
     const int32_t *bt_row = block_table + (size_t)b * max_blocks;
@@ -704,11 +752,24 @@ int oracle_hdequant(int mode, int Hkv, int bt, int max_blocks, int max_tokens, i
                         qa = sext4(row[d] >> 4);
                     }
                     const int V = qa >= 0 ? qa : -qa - 1;
-                    Ip = 16 * V;
-                    if (mode == 1) Ip -= sext4(row[d] & 0xF);
-                    if (Ip < 0) Ip = 0;
-                    if (Ip > 127) Ip = 127;
-                    const float m = qa >= 0 ? level[Ip] : -level[Ip];
+                    float lv;
+                    if (variant == H_BIASED) {
+                        Ip = 16 * V;
+                        if (mode == 1) Ip -= sext4(row[d] & 0xF);
+                        if (Ip < 0) Ip = 0;
+                        if (Ip > 127) Ip = 127;
+                        lv = level[Ip];
+                    } else if (variant == H_CENTRED) {
+                        if (mode == 1) {
+                            Ip = 16 * V + 8 + sext4(row[d] & 0xF);
+                            lv = level[Ip];
+                        } else {
+                            lv = alevel[V];
+                        }
+                    } else {
+                        lv = level[V];
+                    }
+                    const float m = qa >= 0 ? lv : -lv;
                     const size_t pm = (((size_t)b * Hkv + h) * n_pages + t / H_PAGE) * HEAD_DIM + d;
                     const size_t cm = (((size_t)b * Hkv + h) * n_chunks + t / H_CHUNK) * HEAD_DIM + d;
                     const float xc = m * sig_a[cm];

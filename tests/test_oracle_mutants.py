@@ -70,7 +70,13 @@ HIER_MUTANTS = {
                                  "const int S = 1;"),
     "mean_not_restored": ("const float X = xc + mu_a[cm];", "const float X = xc;"),
     "chunk_64": ("#define H_CHUNK 32", "#define H_CHUNK 64"),
-    "no_rounding_bias": ("int V = (I + 7) >> 4;", "int V = I >> 4;"),
+    "no_rounding_bias": ("V = (I + 7) >> 4;", "V = I >> 4;"),
+    "centred_correction_not_centred": ("r = I - 16 * V - 8;", "r = I - 16 * V;"),
+    "centred_anchor_at_bucket_floor": ("alevel[v] = (float)(expm1(((16 * v + 7.5) / 127.0)",
+                                       "alevel[v] = (float)(expm1(((16 * v + 0.0) / 127.0)"),
+    "int4_with_seven_bit_transform": ("return variant == H_INT4 ? 7 : 127;", "return 127;"),
+    "centred_merged_offset_dropped": ("Ip = 16 * V + 8 + sext4(row[d] & 0xF);",
+                                      "Ip = 16 * V + sext4(row[d] & 0xF);"),
 }
 
 
