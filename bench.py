@@ -615,15 +615,17 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
 
 
 def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0, 1.0)):
-    """The paper's own hierarchical codec (Alg. 1) on the workload's layers:
-    encode, and dequantization of the anchor alone and of the merged codes
-    to BF16 pages, each timed over all layers in turn (HIP events); then the
-    compression error vNMSE = E ||o - o_hat||^2 / ||o_hat||^2 of the attention
-    output of each layer's decode query (first four layers, every query head)
-    for both codecs against the exact BF16 cache: the uniform codec through
-    the anchor-decode and verify kernels, the hierarchical one through its
-    BF16 pages and plain fp32 attention.  alpha is not given by the paper;
-    the first value is the one timed."""
+    """The paper's own hierarchical codec (Alg. 1) on the workload's layers,
+    in its three variants (the listing's biased split, the centred split that
+    keeps every code, the single 4-bit code): encode, and dequantization of
+    the anchor alone and of the merged codes to BF16 pages, each timed over
+    all layers in turn (HIP events); then the compression error
+    vNMSE = E ||o_hat - o||^2 / ||o||^2, o the attention output of each
+    layer's decode query (first four layers, every query head) over the
+    exact BF16 cache and o_hat the same over a compressed one: the uniform
+    codec through the anchor-decode and verify kernels, the hierarchical one
+    through its BF16 pages and plain fp32 attention.  alpha is not given by
+    the paper; the first value is the one timed."""
     import torch
 
     from paper_2607_01831_amd import lynx
@@ -636,6 +638,7 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
     vo = torch.empty_like(ko)
     ev = lambda: torch.cuda.Event(enable_timing=True)
     a0 = alphas[0]
+    variants = {"biased": lynx.LYNX_HQ_BIASED, "centred": lynx.LYNX_HQ_CENTRED, "int4": lynx.LYNX_HQ_INT4}
 
     def timed(fn, reps=2):
         fn()
@@ -648,23 +651,30 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (reps * n_layers)
 
-    enc = lambda: [lynx.lynx_hkv_encode(L, 0, T, table, K[l], V[l], a0, hp.k_anc, hp.v_anc, hp.k_res,
-                                        hp.v_res, hm) for l in range(n_layers)]
-    t_enc = timed(enc)
-    hp.merge()
-    t_da = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, False, hp.k_anc, hp.v_anc, a0, hm, ko, vo)
-                          for _ in range(n_layers)])
-    t_df = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, True, hp.k_codes, hp.v_codes, a0, hm, ko, vo)
-                          for _ in range(n_layers)])
+    def encode(l, a, vid):
+        res = vid != lynx.LYNX_HQ_INT4
+        lynx.lynx_hkv_encode(L, 0, T, table, K[l], V[l], a, vid, hp.k_anc, hp.v_anc,
+                             hp.k_res if res else None, hp.v_res if res else None, hm)
+
     elems = T * Hkv * 128 * 2
     meta_b = 4.0 * 2 * (1 / 256 + 1 / 32)          # page and chunk fp32 pairs per element
-    r = {"alpha": a0,
-         "encode_us_per_layer": round(t_enc, 2),
-         "encode_GBps": round(elems * (2 + 1 + meta_b) / (t_enc * 1e-6) / 1e9, 1),
-         "dequant_anchor_us_per_layer": round(t_da, 2),
-         "dequant_anchor_GBps": round(elems * (0.5 + meta_b + 2) / (t_da * 1e-6) / 1e9, 1),
-         "dequant_full_us_per_layer": round(t_df, 2),
-         "dequant_full_GBps": round(elems * (1 + meta_b + 2) / (t_df * 1e-6) / 1e9, 1)}
+    r = {"alpha": a0, "timed": {}}
+    for name, vid in variants.items():
+        res = vid != lynx.LYNX_HQ_INT4
+        t_enc = timed(lambda: [encode(l, a0, vid) for l in range(n_layers)])
+        t_da = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, False, hp.k_anc, hp.v_anc, a0, vid, hm,
+                                                    ko, vo) for _ in range(n_layers)])
+        t = {"encode_us_per_layer": round(t_enc, 2),
+             "encode_GBps": round(elems * (2 + (1 if res else 0.5) + meta_b) / (t_enc * 1e-6) / 1e9, 1),
+             "dequant_anchor_us_per_layer": round(t_da, 2),
+             "dequant_anchor_GBps": round(elems * (0.5 + meta_b + 2) / (t_da * 1e-6) / 1e9, 1)}
+        if res:
+            hp.merge()
+            t_df = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, True, hp.k_codes, hp.v_codes, a0, vid,
+                                                        hm, ko, vo) for _ in range(n_layers)])
+            t["dequant_full_us_per_layer"] = round(t_df, 2)
+            t["dequant_full_GBps"] = round(elems * (1 + meta_b + 2) / (t_df * 1e-6) / 1e9, 1)
+        r["timed"][name] = t
 
     G = Hq // Hkv
 
@@ -675,8 +685,8 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
         s = torch.einsum("hd,htd->ht", q.float(), kf) / 128 ** 0.5
         return torch.einsum("ht,htd->hd", torch.softmax(s, dim=1), vf)
 
-    def vnmse(o, o_hat):
-        return float(((o - o_hat).pow(2).sum(dim=-1) / o_hat.pow(2).sum(dim=-1)).mean())
+    def vnmse(o_hat, o):
+        return float(((o_hat - o).pow(2).sum(dim=-1) / o.pow(2).sum(dim=-1)).mean())
 
     acc = {}
     out = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device=dev)
@@ -688,17 +698,21 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
         o = attn(q, K[l], V[l])
         p = pools[l]
         lynx.lynx_attn_anchor_decode(L, 1, Hq, T, lens, table, p.k_anc, p.v_anc, p.meta, Q[l], out, None, ws)
-        acc.setdefault("uniform_anchor", []).append(vnmse(o, out[0].float()))
+        acc.setdefault("uniform_anchor", []).append(vnmse(out[0].float(), o))
         lynx.lynx_attn_verify(L, 1, Hq, 1, T, lens, table, p.k_codes, p.v_codes, p.meta,
                               Q[l].view(1, 1, Hq, 128), None, None, outv, ws)
-        acc.setdefault("uniform_full", []).append(vnmse(o, outv[0, 0].float()))
+        acc.setdefault("uniform_full", []).append(vnmse(outv[0, 0].float(), o))
         for a in alphas:
-            lynx.lynx_hkv_encode(L, 0, T, table, K[l], V[l], a, hp.k_anc, hp.v_anc, hp.k_res, hp.v_res, hm)
-            hp.merge()
-            for mode, full, (kp, vp) in (("anchor", False, (hp.k_anc, hp.v_anc)),
-                                         ("full", True, (hp.k_codes, hp.v_codes))):
-                lynx.lynx_hkv_dequant(L, 0, T, table, full, kp, vp, a, hm, ko, vo)
-                acc.setdefault(f"hier_{mode}_alpha{a:g}", []).append(vnmse(o, attn(q, ko, vo)))
+            for name, vid in variants.items():
+                encode(l, a, vid)
+                modes = [("anchor", False, (hp.k_anc, hp.v_anc))]
+                if vid != lynx.LYNX_HQ_INT4:
+                    hp.merge()
+                    modes.append(("full", True, (hp.k_codes, hp.v_codes)))
+                for mode, full, (kp, vp) in modes:
+                    lynx.lynx_hkv_dequant(L, 0, T, table, full, kp, vp, a, vid, hm, ko, vo)
+                    key = f"{name}_alpha{a:g}" if vid == lynx.LYNX_HQ_INT4 else f"{name}_{mode}_alpha{a:g}"
+                    acc.setdefault(key, []).append(vnmse(attn(q, ko, vo), o))
     torch.cuda.synchronize()
     r["vnmse"] = {k: float(f"{sum(v) / len(v):.3g}") for k, v in acc.items()}
     r["vnmse_layers"] = len(layers)

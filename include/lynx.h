@@ -312,14 +312,29 @@ int lynx_kv_deserialize_residual(const lynx_layout *L, int32_t b, int32_t t0, in
  * quantizer, as an alternative to the uniform 8-bit one.  Per channel of a
  * kv head (K and V alike), over pages of 256 tokens and chunks of 32:
  * page normalization to [0, 1] (gmin, gscale), chunk centring and scaling
- * (mu, sigma), the alpha-law transform to a 7-bit magnitude I and a sign,
- * and the biased split: anchor V = min((I + 7) >> 4, 7) with the sign
+ * (mu, sigma), the alpha-law transform to a magnitude code I of M levels
+ * (I = Round(M ln(1 + alpha |x|) / ln(1 + alpha))) and a sign, and the split
+ * into 4-bit two's complement nibbles packed like the uniform codec's (same
+ * plane layout).  The anchor carries the sign with the sign-aware map
  * (Q_anc = V, or -V - 1 for a negative value, so a negative zero keeps its
- * sign), correction Q_res = clamp(16 V - I, -8, 7); both 4-bit two's
- * complement, packed like the uniform codec's nibbles (same plane layout).
- * Codes above 120 come back as 120: the listing's anchor reaches 8 there,
- * which four signed bits cannot hold.  alpha is not fixed by the paper.
+ * sign).  alpha is not fixed by the paper.  Variants (the variant argument):
+ *   LYNX_HQ_BIASED   the listing's biased split, M = 127: anchor
+ *                    V = min((I + 7) >> 4, 7), correction
+ *                    Q_res = clamp(16 V - I, -8, 7).  Codes above 120 come
+ *                    back as 120: the listing's anchor reaches 8 there,
+ *                    which four signed bits cannot hold.
+ *   LYNX_HQ_CENTRED  the split that keeps every code, M = 127: anchor
+ *                    V = I >> 4 (sign and top three bits), correction
+ *                    Q_res = I - 16 V - 8, centred on the bucket.  The anchor
+ *                    alone stands for the bucket's centre, code 16 V + 7.5;
+ *                    the merged byte is a complete 8-bit code (the paper's
+ *                    single-precision 8-bit configuration, Sec. 6.1).
+ *   LYNX_HQ_INT4     the single-precision 4-bit configuration (Sec. 6.1):
+ *                    M = 7, the anchor plane holds Q = I or -I - 1, no
+ *                    residual.
  */
+enum { LYNX_HQ_BIASED = 0, LYNX_HQ_CENTRED = 1, LYNX_HQ_INT4 = 2 };
+
 typedef struct lynx_hmeta {
     float *k_gmin, *k_gscale; /* [B][Hkv][ceil(max_tokens/256)][128] fp32 */
     float *k_mu, *k_sigma;    /* [B][Hkv][ceil(max_tokens/32)][128] fp32  */
@@ -329,29 +344,35 @@ typedef struct lynx_hmeta {
 
 /*
  * lynx_hkv_encode -- hierarchical encode of one sequence (one layer).
- *   Arguments as lynx_kv_encode, plus alpha (0 < alpha <= 1e30), and the
- *   hierarchical metadata (all 16-byte aligned): row b written for pages
- *   and chunks holding tokens < T.  Launches one kernel.
+ *   Arguments as lynx_kv_encode, plus alpha (0 < alpha <= 1e30), the
+ *   variant (LYNX_HQ_*), and the hierarchical metadata (all 16-byte
+ *   aligned): row b written for pages and chunks holding tokens < T.
+ *   LYNX_HQ_INT4 writes the anchor planes only: k_res and v_res may be NULL.
+ *   Launches one kernel.
  */
 int lynx_hkv_encode(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
-                    const void *k_bf16, const void *v_bf16, float alpha, uint8_t *k_anc,
-                    uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res, const lynx_hmeta *meta,
-                    void *stream);
+                    const void *k_bf16, const void *v_bf16, float alpha, int32_t variant,
+                    uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
+                    const lynx_hmeta *meta, void *stream);
 
 /*
  * lynx_hkv_dequant -- the deserializer's dequantization into BF16 pages
  * (Sec. 4.2): sequence b's K and V reconstructed as BF16 [T][Hkv][128]
  * (k_out_bf16, v_out_bf16, device, written).
- *   full 0: from the anchor nibble planes alone (code 16 V);
+ *   full 0: from the anchor nibble planes alone (code 16 V for
+ *           LYNX_HQ_BIASED, 16 V + 7.5 for LYNX_HQ_CENTRED, V for
+ *           LYNX_HQ_INT4);
  *   full 1: from the merged code planes of lynx_kv_merge (high nibble
- *           anchor, low nibble correction; code 16 V - Q_res).
+ *           anchor, low nibble correction; code 16 V - Q_res, or
+ *           16 V + 8 + Q_res); not for LYNX_HQ_INT4 (LYNX_EINVAL).
  *   x = ((+-level(code) * sigma) + mu) * gscale + gmin in fp32, rounded to
- *   BF16 to nearest even, level(i) = expm1(i / 127 * log1p(alpha)) / alpha.
+ *   BF16 to nearest even, level(i) = expm1(i / M * log1p(alpha)) / alpha.
  * Launches one kernel.
  */
 int lynx_hkv_dequant(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
                      int32_t full, const uint8_t *k_plane, const uint8_t *v_plane, float alpha,
-                     const lynx_hmeta *meta, void *k_out_bf16, void *v_out_bf16, void *stream);
+                     int32_t variant, const lynx_hmeta *meta, void *k_out_bf16, void *v_out_bf16,
+                     void *stream);
 
 /* Static, human-readable text for a lynx_status value. */
 const char *lynx_strerror(int status);

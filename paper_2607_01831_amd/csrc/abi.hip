@@ -318,49 +318,59 @@ int check_hmeta(const lynx_hmeta *m, lynx::HMetaPtrs *hp) {
     return LYNX_OK;
 }
 bool alpha_ok(float a) { return a > 0.0f && a <= 1e30f; }
+bool variant_ok(int32_t v) { return v == LYNX_HQ_BIASED || v == LYNX_HQ_CENTRED || v == LYNX_HQ_INT4; }
+static_assert(LYNX_HQ_BIASED == lynx::kHBiased && LYNX_HQ_CENTRED == lynx::kHCentred &&
+                  LYNX_HQ_INT4 == lynx::kHInt4,
+              "codec variant values");
 }  // namespace
 
 extern "C" {
 
 int lynx_hkv_encode(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
-                    const void *k_bf16, const void *v_bf16, float alpha, uint8_t *k_anc,
-                    uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res, const lynx_hmeta *meta,
-                    void *stream) {
+                    const void *k_bf16, const void *v_bf16, float alpha, int32_t variant,
+                    uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
+                    const lynx_hmeta *meta, void *stream) {
     Geometry g;
     lynx::HMetaPtrs hp;
     int rc = check_layout(L, &g);
     if (rc != LYNX_OK) return rc;
     if ((rc = check_hmeta(meta, &hp)) != LYNX_OK) return rc;
-    if (!alpha_ok(alpha) || b < 0 || T < 0 || T > layout_capacity(g)) return LYNX_EINVAL;
+    if (!alpha_ok(alpha) || !variant_ok(variant) || b < 0 || T < 0 || T > layout_capacity(g))
+        return LYNX_EINVAL;
     if (T == 0) return LYNX_OK;
-    const void *ptrs[] = {block_table, k_bf16, v_bf16, k_anc, v_anc, k_res, v_res};
+    const void *ptrs[] = {block_table, k_bf16, v_bf16, k_anc, v_anc};
     for (const void *p : ptrs)
         if (!p || !aligned16(p)) return LYNX_EINVAL;
+    if (variant != LYNX_HQ_INT4)
+        for (const void *p : {(const void *)k_res, (const void *)v_res})
+            if (!p || !aligned16(p)) return LYNX_EINVAL;
     lynx::HTables tab;
-    lynx::make_htables(alpha, &tab);
+    lynx::make_htables(alpha, variant, &tab);
     hipError_t e = lynx::launch_hencode(g, b, T, block_table, static_cast<const uint16_t *>(k_bf16),
                                         static_cast<const uint16_t *>(v_bf16), k_anc, v_anc, k_res,
-                                        v_res, hp, tab, static_cast<hipStream_t>(stream));
+                                        v_res, hp, tab, variant, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
 
 int lynx_hkv_dequant(const lynx_layout *L, int32_t b, int32_t T, const int32_t *block_table,
                      int32_t full, const uint8_t *k_plane, const uint8_t *v_plane, float alpha,
-                     const lynx_hmeta *meta, void *k_out_bf16, void *v_out_bf16, void *stream) {
+                     int32_t variant, const lynx_hmeta *meta, void *k_out_bf16, void *v_out_bf16,
+                     void *stream) {
     Geometry g;
     lynx::HMetaPtrs hp;
     int rc = check_layout(L, &g);
     if (rc != LYNX_OK) return rc;
     if ((rc = check_hmeta(meta, &hp)) != LYNX_OK) return rc;
-    if (!alpha_ok(alpha) || (full != 0 && full != 1) || b < 0 || T < 0 || T > layout_capacity(g))
+    if (!alpha_ok(alpha) || !variant_ok(variant) || (full != 0 && full != 1) ||
+        (full == 1 && variant == LYNX_HQ_INT4) || b < 0 || T < 0 || T > layout_capacity(g))
         return LYNX_EINVAL;
     if (T == 0) return LYNX_OK;
     const void *ptrs[] = {block_table, k_plane, v_plane, k_out_bf16, v_out_bf16};
     for (const void *p : ptrs)
         if (!p || !aligned16(p)) return LYNX_EINVAL;
     lynx::HTables tab;
-    lynx::make_htables(alpha, &tab);
-    hipError_t e = lynx::launch_hdequant(full == 1, g, b, T, block_table, k_plane, v_plane, hp, tab,
+    lynx::make_htables(alpha, variant, &tab);
+    hipError_t e = lynx::launch_hdequant(full == 1, g, b, T, block_table, k_plane, v_plane, hp, tab, variant,
                                          static_cast<uint16_t *>(k_out_bf16),
                                          static_cast<uint16_t *>(v_out_bf16),
                                          static_cast<hipStream_t>(stream));

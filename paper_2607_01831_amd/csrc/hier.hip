@@ -1,6 +1,6 @@
 // The hierarchical non-linear codec of Alg. 1 (Sec. 4.1) for gfx950:
-// encode (page normalization, chunk isolation, alpha-law transform, biased
-// split into a signed 4-bit anchor and a signed 4-bit correction) and the
+// encode (page normalization, chunk isolation, alpha-law transform, split
+// into a signed 4-bit anchor and a signed 4-bit correction) and the
 // deserializer's dequantization of the anchor alone or of the merged codes
 // into BF16 pages (Sec. 4.2 Anchor and Residual phases).
 //
@@ -10,11 +10,13 @@
 //      (1 / gscale);
 //   2. mu = the chunk's mean of X (fp32 sum in token order / count),
 //      Xc = X - mu, sigma = max |Xc|, Xf = Xc * (1 / sigma);
-//   3. I = Round(127 ln(1 + a|Xf|) / ln(1 + a)): the number of decision
-//      thresholds theta_k <= |Xf| (a binary search over the sorted table);
-//      S = sign(Xc);
-//   4. V = min((I + 7) >> 4, 7), Q_res = clamp(16 V - I, -8, 7),
-//      Q_anc = V, or -V - 1 for S < 0.
+//   3. I = Round(M ln(1 + a|Xf|) / ln(1 + a)): the number of decision
+//      thresholds theta_k <= |Xf| (a binary search over the sorted table,
+//      padded with +inf); S = sign(Xc); M = 127, or 7 for the 4-bit code;
+//   4. by variant, with the sign-aware anchor Q_anc = V, or -V - 1 for S < 0:
+//      biased:  V = min((I + 7) >> 4, 7), Q_res = clamp(16 V - I, -8, 7);
+//      centred: V = I >> 4, Q_res = I - 16 V - 8 (every code kept);
+//      4-bit:   V = I, no correction.
 // A range whose reciprocal is not finite and positive normalizes to 0.  Every
 // fp32 product that an add follows is rounded on its own (mul_rn), so no
 // fused multiply-add changes a result.
@@ -53,12 +55,23 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
     return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Stage 4 for one code: the byte-ready nibbles of the anchor and residual.
-__device__ __forceinline__ void split(int I, float xc, uint32_t &qa, uint32_t &qr) {
-    int V = (I + 7) >> 4;
-    V = V > 7 ? 7 : V;
-    int r = 16 * V - I;
-    r = r < -8 ? -8 : (r > 7 ? 7 : r);
+// Stage 4 of every variant in one branch-free form: V = min((I + bias) >> sh,
+// 7), Q_res = clamp(sgn (16 V - I) - off, -8, 7), with (bias, sh, sgn, off)
+// = (7, 4, 1, 0) for the biased split, (0, 4, -1, 8) for the centred one
+// (V = I >> 4, Q_res = I - 16 V - 8, never clamped) and (0, 0, 1, 0) for the
+// 4-bit code (V = I; no residual is written).
+struct SplitRule {
+    int bias, sh, sgn, off;
+};
+__device__ __forceinline__ SplitRule split_rule(int variant) {
+    if (variant == kHBiased) return {7, 4, 1, 0};
+    if (variant == kHCentred) return {0, 4, -1, 8};
+    return {0, 0, 1, 0};
+}
+// The byte-ready nibbles of the anchor and residual of one code.
+__device__ __forceinline__ void split(const SplitRule &sr, int I, float xc, uint32_t &qa, uint32_t &qr) {
+    const int V = min((I + sr.bias) >> sr.sh, 7);
+    const int r = min(max(sr.sgn * (16 * V - I) - sr.off, -8), 7);
     qa = (uint32_t)(xc < 0.0f ? -V - 1 : V) & 15u;
     qr = (uint32_t)r & 15u;
 }
@@ -67,13 +80,13 @@ __device__ __forceinline__ void split(int I, float xc, uint32_t &qa, uint32_t &q
 // pair cp = tid % 64) owns channels 2 cp, 2 cp + 1 of the page's tokens
 // 64 q .. 64 q + 63 (chunks 2 q, 2 q + 1): a wavefront reads whole 256-byte
 // token rows and writes whole 64-byte plane rows.  LAYOUT 0: one block per
-// sequence; 1: paged.
+// sequence; 1: paged.  The 4-bit variant writes the anchor planes only.
 template <int LAYOUT>
 __global__ __launch_bounds__(kHThreads) void hencode_kernel(
     Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
     const uint16_t *__restrict__ k, const uint16_t *__restrict__ v, uint8_t *__restrict__ k_anc,
     uint8_t *__restrict__ v_anc, uint8_t *__restrict__ k_res, uint8_t *__restrict__ v_res,
-    HMetaPtrs meta, HTables tab) {
+    HMetaPtrs meta, HTables tab, int variant) {
     const int h = blockIdx.x;
     const int p = blockIdx.y;
     const int which = blockIdx.z;
@@ -83,6 +96,8 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
     const int Hkv = geo.Hkv;
     const int t0 = p * kPage;
     const int n = min(kPage, T - t0);
+    const SplitRule sr = split_rule(variant);
+    const bool has_res = variant != kHInt4;
     const uint16_t *src = which == 0 ? k : v;
     uint8_t *anc = which == 0 ? k_anc : v_anc;
     uint8_t *res = which == 0 ? k_res : v_res;
@@ -184,7 +199,7 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
 #pragma unroll
                     for (int step = 64; step >= 1; step >>= 1)
                         if (s_theta[I + step - 1] <= xf) I += step;
-                    split(I, xc, qa[j], qr[j]);
+                    split(sr, I, xc, qa[j], qr[j]);
                 }
                 const int t = t0 + 64 * q + i0 + i;
                 int blk, tb;
@@ -199,7 +214,7 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
                 if (blk >= 0 && blk < geo.num_blocks) {
                     const size_t off = (((size_t)blk * Hkv + h) * geo.bt + tb) * kNibbleRow + cp;
                     anc[off] = (uint8_t)(qa[0] | (qa[1] << 4));
-                    res[off] = (uint8_t)(qr[0] | (qr[1] << 4));
+                    if (has_res) res[off] = (uint8_t)(qr[0] | (qr[1] << 4));
                 }
             }
         }
@@ -209,16 +224,20 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
 __device__ __forceinline__ int sext4(uint32_t nib) { return (int)nib >= 8 ? (int)nib - 16 : (int)nib; }
 
 // Dequantization to BF16 [T][Hkv][128]: thread (token row, 8 dims), per
-// dimension I' = 16 V (anchor) or 16 V - Q_res (merged code), level from
-// the table, x = ((+-level * sigma) + mu) * gscale + gmin in fp32, rounded to
-// BF16 to nearest even.  FULL 0: anchor nibble planes; 1: code planes.
+// dimension the level of the code the variant names (biased: 16 V for the
+// anchor, 16 V - Q_res for the merged code; centred: the bucket centre
+// 16 V + 7.5, or 16 V + 8 + Q_res; 4-bit: V), x = ((+-level * sigma) + mu) *
+// gscale + gmin in fp32, rounded to BF16 to nearest even.  FULL 0: anchor
+// nibble planes; 1: code planes.
 template <int FULL, int LAYOUT>
 __global__ __launch_bounds__(kHThreads) void hdequant_kernel(
     Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
     const uint8_t *__restrict__ k_plane, const uint8_t *__restrict__ v_plane, HMetaPtrs meta,
-    HTables tab, uint16_t *__restrict__ k_out, uint16_t *__restrict__ v_out) {
+    HTables tab, int variant, uint16_t *__restrict__ k_out, uint16_t *__restrict__ v_out) {
     __shared__ float s_level[128];
+    __shared__ float s_alevel[8];
     if (threadIdx.x < 128) s_level[threadIdx.x] = tab.level[threadIdx.x];
+    if (threadIdx.x < 8) s_alevel[threadIdx.x] = tab.alevel[threadIdx.x];
     __syncthreads();
     const int Hkv = geo.Hkv;
     const size_t per = (size_t)T * Hkv * 16;  // (token, head, 8-dim piece) items per tensor
@@ -286,9 +305,17 @@ __global__ __launch_bounds__(kHThreads) void hdequant_kernel(
             for (int u = 0; u < 2; ++u) {
                 const int a = qa[j + u];
                 const int V = a >= 0 ? a : -a - 1;
-                int Ip = 16 * V - qr[j + u];
-                Ip = Ip < 0 ? 0 : (Ip > 127 ? 127 : Ip);
-                const float m = a >= 0 ? s_level[Ip] : -s_level[Ip];
+                float lv;
+                if (variant == kHBiased) {
+                    int Ip = 16 * V - qr[j + u];
+                    Ip = Ip < 0 ? 0 : (Ip > 127 ? 127 : Ip);
+                    lv = s_level[Ip];
+                } else if (variant == kHCentred) {
+                    lv = FULL ? s_level[16 * V + 8 + qr[j + u]] : s_alevel[V];
+                } else {
+                    lv = s_level[V];
+                }
+                const float m = a >= 0 ? lv : -lv;
                 const float xc = mul_rn(m, sg[j + u]);
                 const float X = xc + mu[j + u];
                 const float x = mul_rn(X, gs[j + u]) + gm[j + u];
@@ -309,31 +336,34 @@ int shift_of(int bt) {
 
 }  // namespace
 
-void make_htables(float alpha, HTables *t) {
+void make_htables(float alpha, int variant, HTables *t) {
     const double la = log1p((double)alpha);
-    for (int k = 0; k < 127; ++k) t->theta[k] = (float)(expm1(((k + 0.5) / 127.0) * la) / (double)alpha);
-    t->theta[127] = INFINITY;
-    for (int i = 0; i < 128; ++i) t->level[i] = (float)(expm1((i / 127.0) * la) / (double)alpha);
+    const int M = variant == kHInt4 ? 7 : 127;
+    for (int k = 0; k < 128; ++k)
+        t->theta[k] = k < M ? (float)(expm1(((k + 0.5) / M) * la) / (double)alpha) : INFINITY;
+    for (int i = 0; i < 128; ++i)
+        t->level[i] = (float)(expm1(((double)(i < M ? i : M) / M) * la) / (double)alpha);
+    for (int v = 0; v < 8; ++v) t->alevel[v] = (float)(expm1(((16 * v + 7.5) / 127.0) * la) / (double)alpha);
 }
 
 hipError_t launch_hencode(const Geometry &g, int b, int T, const int32_t *block_table,
                           const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
                           uint8_t *k_res, uint8_t *v_res, HMetaPtrs meta, const HTables &tab,
-                          hipStream_t stream) {
+                          int variant, hipStream_t stream) {
     if (T <= 0) return hipSuccess;
     dim3 grid(g.Hkv, (T + kPage - 1) / kPage, 2);
     if (g.max_blocks == 1)
         hipLaunchKernelGGL(hencode_kernel<0>, grid, dim3(kHThreads), 0, stream, g, b, T, shift_of(g.bt),
-                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta, tab);
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta, tab, variant);
     else
         hipLaunchKernelGGL(hencode_kernel<1>, grid, dim3(kHThreads), 0, stream, g, b, T, shift_of(g.bt),
-                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta, tab);
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta, tab, variant);
     return hipGetLastError();
 }
 
 hipError_t launch_hdequant(bool full, const Geometry &g, int b, int T, const int32_t *block_table,
                            const uint8_t *k_plane, const uint8_t *v_plane, HMetaPtrs meta,
-                           const HTables &tab, uint16_t *k_out, uint16_t *v_out,
+                           const HTables &tab, int variant, uint16_t *k_out, uint16_t *v_out,
                            hipStream_t stream) {
     if (T <= 0) return hipSuccess;
     size_t blocks = ((size_t)2 * T * g.Hkv * 16 + kHThreads - 1) / kHThreads;
@@ -343,17 +373,17 @@ hipError_t launch_hdequant(bool full, const Geometry &g, int b, int T, const int
     if (full) {
         if (g.max_blocks == 1)
             hipLaunchKernelGGL((hdequant_kernel<1, 0>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
-                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+                               block_table, k_plane, v_plane, meta, tab, variant, k_out, v_out);
         else
             hipLaunchKernelGGL((hdequant_kernel<1, 1>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
-                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+                               block_table, k_plane, v_plane, meta, tab, variant, k_out, v_out);
     } else {
         if (g.max_blocks == 1)
             hipLaunchKernelGGL((hdequant_kernel<0, 0>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
-                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+                               block_table, k_plane, v_plane, meta, tab, variant, k_out, v_out);
         else
             hipLaunchKernelGGL((hdequant_kernel<0, 1>), grid, dim3(kHThreads), 0, stream, g, b, T, sh,
-                               block_table, k_plane, v_plane, meta, tab, k_out, v_out);
+                               block_table, k_plane, v_plane, meta, tab, variant, k_out, v_out);
     }
     return hipGetLastError();
 }

@@ -42,21 +42,28 @@ struct HMetaPtrs {
     float *k_gmin, *k_gscale, *k_mu, *k_sigma;  // [B][Hkv][n_pages][128], [B][Hkv][n_chunks][128]
     float *v_gmin, *v_gscale, *v_mu, *v_sigma;
 };
-// Per-alpha tables: decision thresholds theta[0..126] (theta[127] = +inf) and
-// reconstruction levels level[0..127], each the fp32 value of
-// expm1((k + 0.5) / 127 * log1p(alpha)) / alpha, expm1(i / 127 * log1p(alpha)) / alpha.
+// Codec variants (the values of lynx.h's LYNX_HQ_*).
+constexpr int kHBiased = 0;
+constexpr int kHCentred = 1;
+constexpr int kHInt4 = 2;
+// Per-(alpha, variant) tables, with M = 127 (7 for the 4-bit code): decision
+// thresholds theta[k] = expm1((k + 0.5) / M * log1p(alpha)) / alpha for
+// k < M, +inf beyond; levels level[i] = expm1(i / M * log1p(alpha)) / alpha
+// (i <= M); the centred split's anchor-only levels alevel[V] at code
+// 16 V + 7.5 of 127.  Each the fp32 value of the double expression.
 struct HTables {
     float theta[128];
     float level[128];
+    float alevel[8];
 };
-void make_htables(float alpha, HTables *t);
+void make_htables(float alpha, int variant, HTables *t);
 hipError_t launch_hencode(const Geometry &g, int b, int T, const int32_t *block_table,
                           const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
                           uint8_t *k_res, uint8_t *v_res, HMetaPtrs meta, const HTables &tab,
-                          hipStream_t stream);
+                          int variant, hipStream_t stream);
 hipError_t launch_hdequant(bool full, const Geometry &g, int b, int T, const int32_t *block_table,
                            const uint8_t *k_plane, const uint8_t *v_plane, HMetaPtrs meta,
-                           const HTables &tab, uint16_t *k_out, uint16_t *v_out,
+                           const HTables &tab, int variant, uint16_t *k_out, uint16_t *v_out,
                            hipStream_t stream);
 
 // ---- serializer / deserializer (codec.hip) -----------------------------------

@@ -74,9 +74,9 @@ def load():
         "lynx_kv_serialize": ([I32, I32, P, P, P, P, P], ctypes.c_int),
         "lynx_kv_deserialize_anchor": ([LP, I32, I32, I32, P, P, P, P, MP, P], ctypes.c_int),
         "lynx_kv_deserialize_residual": ([LP, I32, I32, I32, P, P, P, P, P, P, P], ctypes.c_int),
-        "lynx_hkv_encode": ([LP, I32, I32, P, P, P, ctypes.c_float, P, P, P, P,
+        "lynx_hkv_encode": ([LP, I32, I32, P, P, P, ctypes.c_float, I32, P, P, P, P,
                              ctypes.POINTER(lynx_hmeta), P], ctypes.c_int),
-        "lynx_hkv_dequant": ([LP, I32, I32, P, I32, P, P, ctypes.c_float,
+        "lynx_hkv_dequant": ([LP, I32, I32, P, I32, P, P, ctypes.c_float, I32,
                               ctypes.POINTER(lynx_hmeta), P, P, P], ctypes.c_int),
         "lynx_strerror": ([ctypes.c_int], ctypes.c_char_p),
     }
@@ -276,21 +276,26 @@ class HMeta:
         return lynx_hmeta(*(_ptr(getattr(self, f)) for f, _ in lynx_hmeta._fields_))
 
 
-def lynx_hkv_encode(L: Layout, b: int, T: int, block_table, k, v, alpha: float, k_anc, v_anc,
-                    k_res, v_res, hmeta: HMeta, stream=None) -> None:
+# codec variants of the hierarchical codec (lynx.h LYNX_HQ_*)
+LYNX_HQ_BIASED, LYNX_HQ_CENTRED, LYNX_HQ_INT4 = 0, 1, 2
+
+
+def lynx_hkv_encode(L: Layout, b: int, T: int, block_table, k, v, alpha: float, variant: int,
+                    k_anc, v_anc, k_res, v_res, hmeta: HMeta, stream=None) -> None:
+    """k_res, v_res may be None for LYNX_HQ_INT4."""
     lay, met = L.c(), hmeta.c()
     _check("lynx_hkv_encode", load().lynx_hkv_encode(
-        ctypes.byref(lay), b, T, _ptr(block_table), _ptr(k), _ptr(v), alpha, _ptr(k_anc),
+        ctypes.byref(lay), b, T, _ptr(block_table), _ptr(k), _ptr(v), alpha, variant, _ptr(k_anc),
         _ptr(v_anc), _ptr(k_res), _ptr(v_res), ctypes.byref(met), _stream(stream)))
 
 
 def lynx_hkv_dequant(L: Layout, b: int, T: int, block_table, full: bool, k_plane, v_plane,
-                     alpha: float, hmeta: HMeta, k_out, v_out, stream=None) -> None:
+                     alpha: float, variant: int, hmeta: HMeta, k_out, v_out, stream=None) -> None:
     """k_out, v_out: BF16 [T][Hkv][128] (device, written)."""
     lay, met = L.c(), hmeta.c()
     _check("lynx_hkv_dequant", load().lynx_hkv_dequant(
         ctypes.byref(lay), b, T, _ptr(block_table), 1 if full else 0, _ptr(k_plane), _ptr(v_plane),
-        alpha, ctypes.byref(met), _ptr(k_out), _ptr(v_out), _stream(stream)))
+        alpha, variant, ctypes.byref(met), _ptr(k_out), _ptr(v_out), _stream(stream)))
 
 
 def lynx_serialized_bytes(num_kv_heads: int, n_tokens: int) -> tuple[int, int]:

@@ -188,8 +188,11 @@ def test_hierarchical_codec_validation(lib):
     L = _layout(max_blocks_per_seq=16, num_blocks=64, max_tokens=256)
     lay = L.c()
     hm = lynx.lynx_hmeta(*[16 * (i + 1) for i in range(8)])
-    enc = lambda alpha=255.0, T=10, hmp=ctypes.byref(hm), planes=(16, 16, 16, 16): lib.lynx_hkv_encode(
-        ctypes.byref(lay), 0, T, 16, 16, 16, alpha, *planes, hmp, None)
+    enc = lambda alpha=255.0, T=10, hmp=ctypes.byref(hm), planes=(16, 16, 16, 16), variant=0: \
+        lib.lynx_hkv_encode(ctypes.byref(lay), 0, T, 16, 16, 16, alpha, variant, *planes, hmp, None)
+    assert enc(variant=3) == E.LYNX_EINVAL
+    assert enc(variant=-1) == E.LYNX_EINVAL
+    assert enc(variant=E.LYNX_HQ_CENTRED, planes=(16, 16, None, 16)) == E.LYNX_EINVAL
     assert enc(alpha=0.0) == E.LYNX_EINVAL
     assert enc(alpha=-1.0) == E.LYNX_EINVAL
     assert enc(alpha=float("nan")) == E.LYNX_EINVAL
@@ -199,9 +202,11 @@ def test_hierarchical_codec_validation(lib):
     bad = lynx.lynx_hmeta(16, 32, 48, 64, 80, 96, 112, 0)
     assert enc(hmp=ctypes.byref(bad)) == E.LYNX_EINVAL
     assert enc(T=0) == E.LYNX_OK
-    deq = lambda full=1, alpha=255.0, T=10: lib.lynx_hkv_dequant(
-        ctypes.byref(lay), 0, T, 16, full, 16, 16, alpha, ctypes.byref(hm), 16, 16, None)
+    deq = lambda full=1, alpha=255.0, T=10, variant=0: lib.lynx_hkv_dequant(
+        ctypes.byref(lay), 0, T, 16, full, 16, 16, alpha, variant, ctypes.byref(hm), 16, 16, None)
     assert deq(full=2) == E.LYNX_EINVAL
+    assert deq(variant=7) == E.LYNX_EINVAL
+    assert deq(full=1, variant=E.LYNX_HQ_INT4) == E.LYNX_EINVAL   # the 4-bit code has no residual
     assert deq(alpha=0.0) == E.LYNX_EINVAL
     assert deq(T=300) == E.LYNX_EINVAL
     assert deq(T=0) == E.LYNX_OK
