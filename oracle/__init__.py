@@ -61,6 +61,8 @@ def _load():
     lib.oracle_anchor_decode_tail.restype = I
     F = ctypes.c_float
     IP = ctypes.POINTER(ctypes.c_int)
+    lib.oracle_accept_sample.argtypes = [I, I, I, P, P, P, P, P, P]
+    lib.oracle_accept_sample.restype = I
     lib.oracle_hsplit.argtypes = [I, I, I, IP, IP]
     lib.oracle_hsplit.restype = I
     lib.oracle_htables.argtypes = [F, I, P, P, P]
@@ -232,6 +234,28 @@ def accept_greedy(target_logits: np.ndarray, draft_tokens: np.ndarray):
         next_token[b] = int(np.argmax(logits[b, n]))
     return accepted, next_token
 
+
+
+def accept_sample(p: np.ndarray, q: np.ndarray, draft_tokens: np.ndarray, u: np.ndarray):
+    """Acceptance of k sampled drafts (Sec. 4.3 with the speculative-sampling
+    rule; readings in lynx_oracle.c).  p: fp32 [B][k+1][V] target
+    probabilities, q: fp32 [B][k][V] draft probabilities, draft_tokens: int
+    [B][k], u: fp32 [B][k+1] uniforms.  Returns (accepted int32 [B],
+    next_token int32 [B])."""
+    p = np.ascontiguousarray(p, np.float32)
+    q = np.ascontiguousarray(q, np.float32)
+    drafts = np.ascontiguousarray(draft_tokens, np.int32)
+    u = np.ascontiguousarray(u, np.float32)
+    B, k1, V = p.shape
+    k = k1 - 1
+    assert q.shape == (B, k, V) and drafts.shape == (B, k) and u.shape == (B, k + 1)
+    accepted = np.zeros(B, np.int32)
+    next_token = np.zeros(B, np.int32)
+    rc = _load().oracle_accept_sample(B, k, V, _ptr(p), _ptr(q), _ptr(drafts), _ptr(u),
+                                      _ptr(accepted), _ptr(next_token))
+    if rc != 0:
+        raise ValueError("oracle_accept_sample rejected its arguments")
+    return accepted, next_token
 
 def verify(L: Layout, Hq: int, seq_lens: np.ndarray, block_table: np.ndarray,
            k_codes: np.ndarray, v_codes: np.ndarray, meta: Meta, q_bits: np.ndarray,

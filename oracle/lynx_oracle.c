@@ -782,3 +782,96 @@ int oracle_hdequant(int mode, int variant, int Hkv, int bt, int max_blocks, int 
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Acceptance of drafts by sampling (Sec. 4.3)                               */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. 4.3 keeps the longest prefix of the drafts the target model agrees
+ * with and corrects the first divergence.  With sampled drafts the agreement
+ * test is the standard speculative-sampling rule: draft i (token x, drawn
+ * from the draft distribution q_i) is kept with probability
+ * min(1, p_i(x) / q_i(x)), p_i the target's distribution; at the first draft
+ * not kept, n, the next token is drawn from the residual weights
+ * max(p_n - q_n, 0); when all k are kept, the bonus token is drawn from
+ * p_k.  The emitted tokens are then distributed as the target's.
+ * Readings (the paper fixes none of the mechanics):
+ *   - the random numbers are inputs: u[b][i] (i < k) for the test of draft
+ *     i, u[b][k] for the draw;
+ *   - draft i is kept when u[b][i] * q_i(x) <= p_i(x), the fp32 product
+ *     rounded once; a token outside [0, V) is not kept;
+ *   - each weight is clamped to [0, 1] (NaN counts 0); if every residual
+ *     weight is 0 the draw uses p_n, and if that is all 0 too, next_token is
+ *     -1;
+ *   - the draw is inverse-CDF sampling with every step exact: weights
+ *     w_v = floor(r_v * 2^40), S = sum w_v, U = floor(u[b][k] * 2^32) clamped
+ *     to [0, 2^32 - 1] (NaN -> 0), t = floor(S * U / 2^32), and the token is
+ *     the smallest v whose inclusive prefix sum of w exceeds t.
+ */
+static uint64_t sample_weight(float r)
+{
+    r = r > 0.0f ? r : 0.0f; /* NaN and negatives count 0 */
+    r = r < 1.0f ? r : 1.0f;
+    return (uint64_t)(r * 1099511627776.0f); /* 2^40: an exact scaling, then truncation */
+}
+
+static uint32_t sample_uniform(float u)
+{
+    const float s = u * 4294967296.0f; /* 2^32 */
+    if (!(s > 0.0f)) return 0u;
+    if (s >= 4294967296.0f) return 0xFFFFFFFFu;
+    return (uint32_t)s;
+}
+
+/* Residual weight of token v: p_v - q_v (q != NULL) or p_v. */
+static float sample_residual(const float *p, const float *q, int v)
+{
+    return q ? p[v] - q[v] : p[v];
+}
+
+/* The draw over the residual weights; -1 if S = 0. */
+static int32_t sample_draw(int V, const float *p, const float *q, float u)
+{
+    uint64_t S = 0;
+    for (int v = 0; v < V; ++v) S += sample_weight(sample_residual(p, q, v));
+    if (S == 0) return -1;
+    const unsigned __int128 prod = (unsigned __int128)S * sample_uniform(u);
+    const uint64_t t = (uint64_t)(prod >> 32);
+    uint64_t acc = 0;
+    for (int v = 0; v < V; ++v) {
+        acc += sample_weight(sample_residual(p, q, v));
+        if (acc > t) return v;
+    }
+    return -1; /* not reached: t < S */
+}
+
+/*
+ * p: [B][k+1][V] target probabilities, q: [B][k][V] draft probabilities,
+ * drafts: int32 [B][k], u: [B][k+1] uniforms.  Writes accepted[B] (0..k)
+ * and next_token[B].  Returns 0, or -1 on bad sizes.
+ */
+int oracle_accept_sample(int B, int k, int V, const float *p, const float *q,
+                         const int32_t *drafts, const float *u, int32_t *accepted,
+                         int32_t *next_token)
+{
+    if (B < 0 || k < 1 || V < 1) return -1;
+    for (int b = 0; b < B; ++b) {
+        const float *pb = p + (size_t)b * (k + 1) * V;
+        const float *qb = q + (size_t)b * k * V;
+        const float *ub = u + (size_t)b * (k + 1);
+        int n = 0;
+        while (n < k) {
+            const int32_t x = drafts[(size_t)b * k + n];
+            if (x < 0 || x >= V) break;
+            const float prod = ub[n] * qb[(size_t)n * V + x];
+            if (!(prod <= pb[(size_t)n * V + x])) break;
+            ++n;
+        }
+        accepted[b] = n;
+        int32_t tok = -1;
+        if (n < k) tok = sample_draw(V, pb + (size_t)n * V, qb + (size_t)n * V, ub[k]);
+        if (tok < 0) tok = sample_draw(V, pb + (size_t)n * V, NULL, ub[k]);
+        next_token[b] = tok;
+    }
+    return 0;
+}

@@ -94,3 +94,30 @@ def test_hier_pins_catch_mutant(name, tmp_path):
                         "tests/test_oracle_hier.py"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+# Planted mistakes in the acceptance of sampled drafts, each of which the pins
+# in test_oracle_spec_sample.py must catch.
+SAMPLE_MUTANTS = {
+    "residual_without_draft": ("return q ? p[v] - q[v] : p[v];", "return p[v];"),
+    "keep_test_inverted": ("if (!(prod <= pb[(size_t)n * V + x])) break;",
+                           "if (!(prod >= pb[(size_t)n * V + x])) break;"),
+    "draw_reuses_rejected_uniform": ("qb + (size_t)n * V, ub[k]);", "qb + (size_t)n * V, ub[n]);"),
+    "draw_by_first_prefix_reaching_t": ("if (acc > t) return v;", "if (acc >= t) return v;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SAMPLE_MUTANTS))
+def test_sample_pins_catch_mutant(name, tmp_path):
+    find, repl = SAMPLE_MUTANTS[name]
+    assert SRC.count(find) == 1, f"mutation anchor for {name} not unique/present"
+    src = tmp_path / "mutant.c"
+    src.write_text(SRC.replace(find, repl))
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-shared", "-fPIC",
+                    "-pthread", str(src), "-o", str(lib), "-lm"], check=True)
+    env = dict(os.environ, LYNX_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        "tests/test_oracle_spec_sample.py"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
