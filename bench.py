@@ -915,6 +915,20 @@ def main():
         torch.cuda.synchronize()
         spec["accept_greedy_k8_vocab128256_us"] = round(e0.elapsed_time(e1) * 1e3 / 20, 2)
         spec["accept_greedy_all_kept"] = int(acc.item()) == nq
+        # acceptance of sampled drafts over the same vocabulary: target and
+        # draft distributions (softmax of the scores and of perturbed ones)
+        probs = torch.softmax(logits, dim=2).contiguous()
+        qprobs = torch.softmax(logits[:, :nq] + 0.5 * torch.randn(1, nq, vocab, generator=g).to(dev),
+                               dim=2).contiguous()
+        uni = torch.rand(1, nq + 1, generator=g).to(dev)
+        for _ in range(3):
+            lynx.lynx_spec_accept_sample(probs, qprobs, drafts, uni, acc, nxt, aws)
+        e0.record(main_s)
+        for _ in range(20):
+            lynx.lynx_spec_accept_sample(probs, qprobs, drafts, uni, acc, nxt, aws)
+        e1.record(main_s)
+        torch.cuda.synchronize()
+        spec["accept_sample_k8_vocab128256_us"] = round(e0.elapsed_time(e1) * 1e3 / 20, 2)
 
     def ms(a, b):
         return sum(r[a].elapsed_time(r[b]) for r in recs) / len(recs)

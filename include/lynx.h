@@ -207,8 +207,9 @@ int lynx_attn_anchor_decode_tail(const lynx_layout *L, int32_t B, int32_t Hq,
 
 /*
  * lynx_spec_accept_workspace_bytes -- device workspace of
- * lynx_spec_accept_greedy for B sequences, k drafts and a vocabulary of
- * `vocab` entries.  Returns 0 on invalid arguments.
+ * lynx_spec_accept_greedy and lynx_spec_accept_sample for B sequences, k
+ * drafts and a vocabulary of `vocab` entries.  Returns 0 on invalid
+ * arguments.
  */
 size_t lynx_spec_accept_workspace_bytes(int32_t B, int32_t k, int32_t vocab);
 
@@ -236,6 +237,41 @@ int lynx_spec_accept_greedy(int32_t B, int32_t k, int32_t vocab, const float *ta
                             const int32_t *draft_tokens, int32_t *accepted,
                             int32_t *next_token, void *workspace, size_t workspace_bytes,
                             void *stream);
+
+/*
+ * lynx_spec_accept_sample -- acceptance of sampled drafts (Sec. 4.3's
+ * longest-prefix rule in its speculative-sampling form).  Draft i, token x
+ * drawn from the draft model's distribution q_i, is kept when
+ * u[i] * q_i(x) <= p_i(x) (fp32 product), i.e. with probability
+ * min(1, p_i(x) / q_i(x)); a token outside [0, vocab) is not kept.  At the
+ * first draft not kept, n, the next token is drawn from the weights
+ * max(p_n - q_n, 0); when all k are kept, the bonus token from p_k.  The
+ * emitted tokens are then distributed as the target model's.
+ * The draw is exact, so its outcome depends on the inputs alone: weights
+ * w_v = floor(r_v * 2^40) with r_v clamped to [0, 1] (NaN counts 0),
+ * S = sum w_v, U = floor(u[k] * 2^32) clamped to [0, 2^32 - 1] (NaN 0),
+ * t = floor(S * U / 2^32); the token is the smallest v whose inclusive
+ * prefix sum of w exceeds t.  If the residual weights are all 0 the draw
+ * uses p_n; if those are all 0 too, next_token is -1.
+ *
+ *   B, k, vocab   sequences (<= 65535), drafts per sequence (1..64),
+ *                 vocabulary size (1..2^23)
+ *   target_probs  fp32 [B][k+1][vocab] (device): the target's probabilities
+ *                 at each draft position and the one after the last
+ *   draft_probs   fp32 [B][k][vocab] (device): the draft model's
+ *   draft_tokens  int32 [B][k] (device)
+ *   uniforms      fp32 [B][k+1] (device): uniform numbers in [0, 1) drawn by
+ *                 the caller, one per draft test and one for the draw
+ *   accepted      int32 [B] (device, written): drafts kept (0..k)
+ *   next_token    int32 [B] (device, written): the drawn token, or -1
+ *   workspace     >= lynx_spec_accept_workspace_bytes(B, k, vocab)
+ *                 (LYNX_EWORKSPACE otherwise)
+ * All pointers 16-byte aligned.  Launches two kernels.
+ */
+int lynx_spec_accept_sample(int32_t B, int32_t k, int32_t vocab, const float *target_probs,
+                            const float *draft_probs, const int32_t *draft_tokens,
+                            const float *uniforms, int32_t *accepted, int32_t *next_token,
+                            void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Serializer / deserializer (Sec. 4.2 Prioritized Transmission; Sec. 5

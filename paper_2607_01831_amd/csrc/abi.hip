@@ -203,8 +203,8 @@ int lynx_attn_verify(const lynx_layout *L, int32_t B, int32_t Hq, int32_t k,
 
 size_t lynx_spec_accept_workspace_bytes(int32_t B, int32_t k, int32_t vocab) {
     if (B < 0 || B > 65535 || k < 1 || k > 64 || vocab < 1) return 0;
-    return (size_t)B * (size_t)(k + 1) * (size_t)lynx::spec_accept_chunks(vocab) *
-           (sizeof(float) + sizeof(int32_t));
+    // greedy: a (score, index) pair per chunk; sampled: two uint64 sums
+    return (size_t)B * (size_t)(k + 1) * (size_t)lynx::spec_accept_chunks(vocab) * 2 * sizeof(uint64_t);
 }
 
 int lynx_spec_accept_greedy(int32_t B, int32_t k, int32_t vocab, const float *target_logits,
@@ -221,6 +221,23 @@ int lynx_spec_accept_greedy(int32_t B, int32_t k, int32_t vocab, const float *ta
     hipError_t e = lynx::launch_spec_accept_greedy(B, k, vocab, target_logits, draft_tokens,
                                                    accepted, next_token, workspace,
                                                    static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_spec_accept_sample(int32_t B, int32_t k, int32_t vocab, const float *target_probs,
+                            const float *draft_probs, const int32_t *draft_tokens,
+                            const float *uniforms, int32_t *accepted, int32_t *next_token,
+                            void *workspace, size_t workspace_bytes, void *stream) {
+    if (B < 0 || B > 65535 || k < 1 || k > 64 || vocab < 1 || vocab > (1 << 23)) return LYNX_EINVAL;
+    if (B == 0) return LYNX_OK;
+    const void *ptrs[] = {target_probs, draft_probs, draft_tokens, uniforms, accepted, next_token};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    const size_t need = lynx_spec_accept_workspace_bytes(B, k, vocab);
+    if (!workspace || !aligned16(workspace) || workspace_bytes < need) return LYNX_EWORKSPACE;
+    hipError_t e = lynx::launch_spec_accept_sample(B, k, vocab, target_probs, draft_probs,
+                                                   draft_tokens, uniforms, accepted, next_token,
+                                                   workspace, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
 

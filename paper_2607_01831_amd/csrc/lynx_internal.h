@@ -149,7 +149,13 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
                             const uint16_t *k_new, const uint16_t *v_new, int tail_count,
                             uint16_t *out, float *lse, void *workspace, hipStream_t stream);
 
-// ---- greedy acceptance of drafts (spec.hip) -----------------------------------
+// ---- acceptance of drafts (spec.hip) ------------------------------------------
+// Sampled acceptance workspace: B * (k + 1) * spec_accept_chunks(vocab) pairs of
+// uint64 chunk sums.
+hipError_t launch_spec_accept_sample(int B, int k, int vocab, const float *p, const float *q,
+                                     const int32_t *drafts, const float *u, int32_t *accepted,
+                                     int32_t *next_token, void *workspace, hipStream_t stream);
+// greedy acceptance
 // Workspace: B * (k + 1) * spec_accept_chunks(vocab) (score, index) pairs.
 int spec_accept_chunks(int vocab);
 hipError_t launch_spec_accept_greedy(int B, int k, int vocab, const float *logits,

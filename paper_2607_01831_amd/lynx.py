@@ -70,6 +70,7 @@ def load():
                                           SZ, P], ctypes.c_int),
         "lynx_spec_accept_workspace_bytes": ([I32, I32, I32], SZ),
         "lynx_spec_accept_greedy": ([I32, I32, I32, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "lynx_spec_accept_sample": ([I32, I32, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "lynx_serialized_bytes": ([I32, I32, ctypes.POINTER(SZ), ctypes.POINTER(SZ)], ctypes.c_int),
         "lynx_kv_serialize": ([I32, I32, P, P, P, P, P], ctypes.c_int),
         "lynx_kv_deserialize_anchor": ([LP, I32, I32, I32, P, P, P, P, MP, P], ctypes.c_int),
@@ -233,6 +234,22 @@ def lynx_spec_accept_greedy(target_logits, draft_tokens, accepted, next_token,
     _check("lynx_spec_accept_greedy", load().lynx_spec_accept_greedy(
         B, k1 - 1, V, _ptr(target_logits), _ptr(draft_tokens), _ptr(accepted), _ptr(next_token),
         _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def lynx_spec_accept_sample(target_probs, draft_probs, draft_tokens, uniforms, accepted,
+                            next_token, workspace_buf=None, stream=None) -> None:
+    """target_probs fp32 [B][k+1][V], draft_probs fp32 [B][k][V], draft_tokens
+    int32 [B][k], uniforms fp32 [B][k+1]; writes accepted and next_token
+    (int32 [B]).  workspace_buf: None allocates
+    lynx_spec_accept_workspace_bytes() bytes with torch."""
+    B, k1, V = (int(x) for x in target_probs.shape)
+    ws = workspace_buf
+    if ws is None:
+        n = lynx_spec_accept_workspace_bytes(B, k1 - 1, V)
+        ws = torch.empty(max(n, 16), dtype=torch.uint8, device=target_probs.device)
+    _check("lynx_spec_accept_sample", load().lynx_spec_accept_sample(
+        B, k1 - 1, V, _ptr(target_probs), _ptr(draft_probs), _ptr(draft_tokens), _ptr(uniforms),
+        _ptr(accepted), _ptr(next_token), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def lynx_attn_verify(L: Layout, B: int, Hq: int, k: int, max_seq_len: int, seq_lens,

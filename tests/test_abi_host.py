@@ -138,7 +138,7 @@ def test_tail_and_acceptance_validation(lib):
                                             None, None, 0, None) == E.LYNX_EWORKSPACE
     # acceptance: workspace size, bad k / vocab, misaligned logits, short workspace
     n = lynx.lynx_spec_accept_workspace_bytes(4, 8, 128256)
-    assert n == 4 * 9 * ((128256 + 4095) // 4096) * 8
+    assert n == 4 * 9 * ((128256 + 4095) // 4096) * 16
     assert lynx.lynx_spec_accept_workspace_bytes(4, 0, 100) == 0
     assert lynx.lynx_spec_accept_workspace_bytes(4, 65, 100) == 0
     assert lynx.lynx_spec_accept_workspace_bytes(4, 8, 0) == 0
@@ -146,6 +146,17 @@ def test_tail_and_acceptance_validation(lib):
     assert lib.lynx_spec_accept_greedy(2, 4, 100, 20, 16, 16, 16, 16, 1 << 20, None) == E.LYNX_EINVAL
     assert lib.lynx_spec_accept_greedy(2, 4, 100, 16, 16, 16, 16, 16, 8, None) == E.LYNX_EWORKSPACE
     assert lib.lynx_spec_accept_greedy(0, 4, 100, None, None, None, None, None, 0, None) == E.LYNX_OK
+    smp = lambda B=2, k=4, V=100, ptrs=(16, 16, 16, 16, 16, 16), wsb=1 << 20: \
+        lib.lynx_spec_accept_sample(B, k, V, *ptrs, 16, wsb, None)
+    assert smp(wsb=16) == E.LYNX_EWORKSPACE
+    assert smp(k=0) == E.LYNX_EINVAL
+    assert smp(k=65) == E.LYNX_EINVAL
+    assert smp(V=0) == E.LYNX_EINVAL
+    assert smp(V=(1 << 23) + 1) == E.LYNX_EINVAL
+    assert smp(B=65536) == E.LYNX_EINVAL
+    assert smp(ptrs=(16, 16, 16, None, 16, 16)) == E.LYNX_EINVAL
+    assert smp(ptrs=(16, 16, 16, 16, 20, 16)) == E.LYNX_EINVAL
+    assert smp(B=0, ptrs=(None,) * 6) == E.LYNX_OK
 
 
 def test_serdes_sizes_and_validation(lib):

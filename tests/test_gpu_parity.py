@@ -449,3 +449,63 @@ def test_spec_accept_greedy(B, k, V):
     assert np.array_equal(acc.cpu().numpy(), ref_acc)
     assert np.array_equal(nxt.cpu().numpy(), ref_nxt)
     assert np.array_equal(ref_acc, cut)
+
+
+def _sample_inputs(B, k, V, seed):
+    """Target / draft distributions with drafts drawn from q, the uniforms,
+    and planted edge cases: drafts outside the vocabulary, p = q rows (no
+    residual), all-zero rows, NaN and out-of-range weights, uniforms at 0, 1
+    and beyond."""
+    rng = np.random.default_rng(seed)
+    p = rng.dirichlet(np.full(V, 0.3), size=(B, k + 1)).astype(np.float32)
+    q = rng.dirichlet(np.full(V, 0.3), size=(B, k)).astype(np.float32)
+    # some draft rows close to the target's, so that drafts are often kept
+    mix = rng.random((B, k, 1)).astype(np.float32) < 0.5
+    q = np.where(mix, 0.8 * p[:, :k] + 0.2 * q, q).astype(np.float32)
+    cq = np.cumsum(q.astype(np.float64), axis=2)
+    r = rng.random((B, k, 1)) * cq[:, :, -1:]
+    drafts = np.minimum((cq < r).sum(axis=2), V - 1).astype(np.int32)
+    u = rng.random((B, k + 1), dtype=np.float32)
+    for b in range(B):
+        case = b % 8
+        if case == 1:
+            drafts[b, rng.integers(k)] = V + b        # outside the vocabulary
+        elif case == 2:
+            drafts[b, 0] = -1
+        elif case == 3:
+            q[b, 0] = p[b, 0]                        # no residual at a rejection
+            u[b, 0] = 1.5
+        elif case == 4:
+            p[b, 0] = 0.0                            # nothing to draw: -1
+            u[b, 0] = 0.9
+        elif case == 5:
+            p[b, -1, :: max(1, V // 7)] = np.nan     # NaN weights count 0
+            p[b, -1, 1::max(1, V // 5)] = 3.0        # above one counts 1
+            u[b, :k] = 0.0                           # every draft kept: the bonus
+        elif case == 6:
+            u[b, k] = 0.0 if b % 16 == 6 else 0.99999994
+        elif case == 7:
+            u[b, k] = np.nan
+    return p, q, drafts, u
+
+
+@pytest.mark.parametrize("B,k,V", [(8, 8, 128256), (16, 4, 1001), (37, 1, 12295), (9, 64, 4096),
+                                   (8, 3, 7), (8, 2, 1), (300, 6, 1000)])
+def test_spec_accept_sample(B, k, V):
+    """Acceptance of sampled drafts, bit-exact against the oracle (accepted
+    counts and drawn tokens) on random distributions and the planted edge
+    cases; float4 rows (V % 4 == 0) and scalar rows."""
+    p, q, drafts, u = _sample_inputs(B, k, V, seed=B * 7919 + k * 31 + V)
+    acc = torch.empty(B, dtype=torch.int32, device="cuda")
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    note(f"spec_accept_sample B={B} k={k} V={V}")
+    lynx.lynx_spec_accept_sample(torch.from_numpy(p).cuda(), torch.from_numpy(q).cuda(),
+                                 torch.from_numpy(drafts).cuda(), torch.from_numpy(u).cuda(), acc, nxt)
+    torch.cuda.synchronize()
+    ref_acc, ref_nxt = oracle.accept_sample(p, q, drafts, u)
+    got_acc, got_nxt = acc.cpu().numpy(), nxt.cpu().numpy()
+    assert np.array_equal(got_acc, ref_acc), np.nonzero(got_acc != ref_acc)
+    assert np.array_equal(got_nxt, ref_nxt), np.nonzero(got_nxt != ref_nxt)
+    # the cases cover both outcomes
+    assert (ref_acc < k).any() or B < 8
+    assert (ref_nxt == -1).any() or B < 5
