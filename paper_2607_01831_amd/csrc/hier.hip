@@ -11,8 +11,9 @@
 //   2. mu = the chunk's mean of X (fp32 sum in token order / count),
 //      Xc = X - mu, sigma = max |Xc|, Xf = Xc * (1 / sigma);
 //   3. I = Round(M ln(1 + a|Xf|) / ln(1 + a)): the number of decision
-//      thresholds theta_k <= |Xf| (a binary search over the sorted table,
-//      padded with +inf); S = sign(Xc); M = 127, or 7 for the 4-bit code;
+//      thresholds theta_k <= |Xf|, found from the transform evaluated in
+//      fp32 (within one of the count) and one exact step against the two
+//      thresholds around it; S = sign(Xc); M = 127, or 7 for the 4-bit code;
 //   4. by variant, with the sign-aware anchor Q_anc = V, or -V - 1 for S < 0:
 //      biased:  V = min((I + 7) >> 4, 7), Q_res = clamp(16 V - I, -8, 7);
 //      centred: V = I >> 4, Q_res = I - 16 V - 8 (every code kept);
@@ -106,9 +107,9 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
     float *mu_a = which == 0 ? meta.k_mu : meta.v_mu;
     float *sig_a = which == 0 ? meta.k_sigma : meta.v_sigma;
 
-    __shared__ float s_theta[128];
+    __shared__ float s_theta[130];  // -inf, theta[0..127], +inf
     __shared__ float s_lo[4][kHeadDim], s_hi[4][kHeadDim];
-    if (tid < 128) s_theta[tid] = tab.theta[tid];
+    if (tid < 130) s_theta[tid] = tid == 0 ? -INFINITY : (tid <= 128 ? tab.theta[tid - 1] : INFINITY);
 
     // the thread's 64 tokens x 2 channels (BF16 pairs)
     uint32_t raw[64];
@@ -193,12 +194,14 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
                     const float xc = X[j][i] - mu[j];
                     float xf = fabsf(mul_rn(xc, is[j]));
                     xf = xf > 1.0f ? 1.0f : xf;
-                    // the number of thresholds <= xf: binary search over the
-                    // 127 sorted thresholds (a NaN counts none)
-                    int I = 0;
-#pragma unroll
-                    for (int step = 64; step >= 1; step >>= 1)
-                        if (s_theta[I + step - 1] <= xf) I += step;
+                    // the number of thresholds <= xf: the transform's own
+                    // value rounded (within one of the count: its fp32 error
+                    // is far below half a code), then one exact step against
+                    // the thresholds on either side (a NaN counts none)
+                    const float ye = tab.linear ? xf : __log2f(1.0f + tab.alpha * xf);
+                    const float y = fminf(fmaxf(ye * tab.yscale + 0.5f, 0.0f), (float)tab.levels);
+                    const int I0 = (int)y;
+                    const int I = I0 - (s_theta[I0] > xf ? 1 : 0) + (s_theta[I0 + 1] <= xf ? 1 : 0);
                     split(sr, I, xc, qa[j], qr[j]);
                 }
                 const int t = t0 + 64 * q + i0 + i;
@@ -344,6 +347,10 @@ void make_htables(float alpha, int variant, HTables *t) {
     for (int i = 0; i < 128; ++i)
         t->level[i] = (float)(expm1(((double)(i < M ? i : M) / M) * la) / (double)alpha);
     for (int v = 0; v < 8; ++v) t->alevel[v] = (float)(expm1(((16 * v + 7.5) / 127.0) * la) / (double)alpha);
+    t->alpha = alpha;
+    t->levels = M;
+    t->linear = alpha < 1e-3f ? 1 : 0;
+    t->yscale = t->linear ? (float)M : (float)(M / log2(1.0 + (double)alpha));
 }
 
 hipError_t launch_hencode(const Geometry &g, int b, int T, const int32_t *block_table,

@@ -51,10 +51,15 @@ constexpr int kHInt4 = 2;
 // k < M, +inf beyond; levels level[i] = expm1(i / M * log1p(alpha)) / alpha
 // (i <= M); the centred split's anchor-only levels alevel[V] at code
 // 16 V + 7.5 of 127.  Each the fp32 value of the double expression.
+// The encode's first guess at a code: yscale * log2(1 + alpha |Xf|), or
+// yscale * |Xf| when `linear` (alpha < 1e-3), with yscale = M / log2(1 + alpha)
+// (or M), is within one of the count the thresholds decide.
 struct HTables {
     float theta[128];
     float level[128];
     float alevel[8];
+    float alpha, yscale;
+    int linear, levels;
 };
 void make_htables(float alpha, int variant, HTables *t);
 hipError_t launch_hencode(const Geometry &g, int b, int T, const int32_t *block_table,

@@ -85,6 +85,16 @@ def test_hier_contiguous(T, Hkv, alpha, variant):
     run_case(k, v, alpha, variant=variant)
 
 
+@pytest.mark.parametrize("alpha", [1e-4, 9.99e-4, 1e-3, 0.01, 0.3, 3.0, 1e4, 1e30])
+def test_hier_alpha_range(alpha):
+    """The encode finds each code from the transform's fp32 value and one
+    exact step against the thresholds around it; across the range of alpha
+    (both sides of the switch to the linear first guess at 1e-3) the codes
+    stay those the oracle's thresholds decide."""
+    k, v = random_kv(2048, 2, seed=2200)
+    run_case(k, v, alpha, variant="centred")
+
+
 @pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("T,bt", [(700, 16), (513, 32), (129, 8)])
 def test_hier_paged(T, bt, variant):
