@@ -83,7 +83,7 @@ __device__ __forceinline__ void split(const SplitRule &sr, int I, float xc, uint
 // token rows and writes whole 64-byte plane rows.  LAYOUT 0: one block per
 // sequence; 1: paged.  The 4-bit variant writes the anchor planes only.
 template <int LAYOUT>
-__global__ __launch_bounds__(kHThreads) void hencode_kernel(
+__global__ __launch_bounds__(kHThreads, 3) void hencode_kernel(
     Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
     const uint16_t *__restrict__ k, const uint16_t *__restrict__ v, uint8_t *__restrict__ k_anc,
     uint8_t *__restrict__ v_anc, uint8_t *__restrict__ k_res, uint8_t *__restrict__ v_res,
@@ -120,17 +120,16 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
     }
     const int mine = max(0, min(64, n - 64 * q));  // valid tokens of the thread
 
-    // ---- stage 1: page min / max per channel ----
+    // ---- stage 1: page min / max per channel (rows past the page repeat
+    // its last token, which leaves a minimum or maximum unchanged) ----
     float lo0 = INFINITY, hi0 = -INFINITY, lo1 = INFINITY, hi1 = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 64; ++i) {
-        if (i < mine) {
-            const float x0 = bf16_to_f32(raw[i] & 0xffffu), x1 = bf16_to_f32(raw[i] >> 16);
-            lo0 = fminf(lo0, x0);
-            hi0 = fmaxf(hi0, x0);
-            lo1 = fminf(lo1, x1);
-            hi1 = fmaxf(hi1, x1);
-        }
+        const float x0 = bf16_to_f32(raw[i] & 0xffffu), x1 = bf16_to_f32(raw[i] >> 16);
+        lo0 = fminf(lo0, x0);
+        hi0 = fmaxf(hi0, x0);
+        lo1 = fminf(lo1, x1);
+        hi1 = fmaxf(hi1, x1);
     }
     s_lo[q][2 * cp] = lo0;
     s_lo[q][2 * cp + 1] = lo1;
@@ -155,6 +154,11 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
     }
 
     const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
+    // LAYOUT 0: the thread's plane bytes for its first token; token i of
+    // the quarter is i rows (64 bytes) further
+    const int blk0 = bt_row[0];
+    const bool ok0 = LAYOUT == 0 && blk0 >= 0 && blk0 < geo.num_blocks;
+    const size_t off0 = (((size_t)blk0 * Hkv + h) * geo.bt + (size_t)(t0 + 64 * q)) * kNibbleRow + cp;
 
     // ---- stages 2-4, chunk by chunk ----
 #pragma unroll
@@ -166,19 +170,27 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
         float mu[2], sig[2], is[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            float sum = 0.0f;
 #pragma unroll
             for (int i = 0; i < kChunk; ++i) {
                 const uint32_t w = raw[i0 + i];
                 const float x = bf16_to_f32(j == 0 ? (w & 0xffffu) : (w >> 16));
                 X[j][i] = mul_rn(x - lo[j], ig[j]);
-                if (i < cnt) sum = sum + X[j][i];
+            }
+            // the sum in token order over the chunk's tokens
+            float sum = 0.0f;
+            if (cnt == kChunk) {  // uniform
+#pragma unroll
+                for (int i = 0; i < kChunk; ++i) sum = sum + X[j][i];
+            } else {
+#pragma unroll
+                for (int i = 0; i < kChunk; ++i)
+                    if (i < cnt) sum = sum + X[j][i];
             }
             mu[j] = sum / (float)cnt;
+            // rows past the page repeat its last token, inside this chunk
             float s = 0.0f;
 #pragma unroll
-            for (int i = 0; i < kChunk; ++i)
-                if (i < cnt) s = fmaxf(s, fabsf(X[j][i] - mu[j]));
+            for (int i = 0; i < kChunk; ++i) s = fmaxf(s, fabsf(X[j][i] - mu[j]));
             sig[j] = s;
             is[j] = range_recip(s);
         }
@@ -204,20 +216,21 @@ __global__ __launch_bounds__(kHThreads) void hencode_kernel(
                     const int I = I0 - (s_theta[I0] > xf ? 1 : 0) + (s_theta[I0 + 1] <= xf ? 1 : 0);
                     split(sr, I, xc, qa[j], qr[j]);
                 }
-                const int t = t0 + 64 * q + i0 + i;
-                int blk, tb;
+                const uint8_t ab = (uint8_t)(qa[0] | (qa[1] << 4)), rb = (uint8_t)(qr[0] | (qr[1] << 4));
                 if (LAYOUT == 0) {
-                    blk = bt_row[0];
-                    tb = t;
+                    if (ok0) {
+                        anc[off0 + (size_t)(i0 + i) * kNibbleRow] = ab;
+                        if (has_res) res[off0 + (size_t)(i0 + i) * kNibbleRow] = rb;
+                    }
                 } else {
+                    const int t = t0 + 64 * q + i0 + i;
                     const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
-                    blk = bt_row[bi];
-                    tb = t - bi * geo.bt;
-                }
-                if (blk >= 0 && blk < geo.num_blocks) {
-                    const size_t off = (((size_t)blk * Hkv + h) * geo.bt + tb) * kNibbleRow + cp;
-                    anc[off] = (uint8_t)(qa[0] | (qa[1] << 4));
-                    if (has_res) res[off] = (uint8_t)(qr[0] | (qr[1] << 4));
+                    const int blk = bt_row[bi];
+                    if (blk >= 0 && blk < geo.num_blocks) {
+                        const size_t off = (((size_t)blk * Hkv + h) * geo.bt + (t - bi * geo.bt)) * kNibbleRow + cp;
+                        anc[off] = ab;
+                        if (has_res) res[off] = rb;
+                    }
                 }
             }
         }
