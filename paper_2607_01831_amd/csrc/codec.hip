@@ -120,12 +120,16 @@ __device__ __forceinline__ void quantize_split8(const float *x, const float *zer
     res = __builtin_amdgcn_perm(r1 | (r1 >> 4), r0 | (r0 >> 4), 0x06040200u);
 }
 
+typedef unsigned int u32v4 __attribute__((ext_vector_type(4)));
+
 // One workgroup encodes one 128-token window of one kv head for K and V.
 // Thread (tr = tid / 16, m = tid % 16) owns dims 8m..8m+7 of the window's
 // tokens tr, tr+16, ..., tr+112: every 16-byte load is part of a fully used
 // 256-byte token row, and a token's 16 owners are the 16 lanes of one DPP
 // row.  LAYOUT 0: one block per sequence; 1: paged; 2: a transmission-buffer
-// object (planes [Hkv][T][64], no block table).
+// object (planes [Hkv][T][64], no block table).  The BF16 input is read once
+// and the planes are not read back by this kernel: nontemporal loads and
+// stores (4.27 -> 4.8 TB/s on a 32K layer).
 template <int LAYOUT>
 __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
@@ -153,8 +157,10 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     for (int i = 0; i < 8; ++i) {
         const int tl = min(tr + 16 * i, n - 1);  // rows past the window re-read its last token
         const size_t e = ((size_t)(t0 + tl) * Hkv + h) * kHeadDim + 8 * m;
-        kraw[i] = *reinterpret_cast<const uint4 *>(k + e);
-        vraw[i] = *reinterpret_cast<const uint4 *>(v + e);
+        const u32v4 kk = __builtin_nontemporal_load(reinterpret_cast<const u32v4 *>(k + e));
+        const u32v4 vv = __builtin_nontemporal_load(reinterpret_cast<const u32v4 *>(v + e));
+        kraw[i] = make_uint4(kk.x, kk.y, kk.z, kk.w);
+        vraw[i] = make_uint4(vv.x, vv.y, vv.z, vv.w);
     }
 
     // Plane row of token t (the block lookup of a paged cache is checked).
@@ -253,8 +259,8 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
                                      vinv[i], vinv[i], vinv[i], vinv[i]};
                 uint32_t a, r;
                 quantize_split8(x, zv, iv, a, r);
-                *reinterpret_cast<uint32_t *>(v_anc + off) = a;
-                *reinterpret_cast<uint32_t *>(v_res + off) = r;
+                __builtin_nontemporal_store(a, reinterpret_cast<uint32_t *>(v_anc + off));
+                __builtin_nontemporal_store(r, reinterpret_cast<uint32_t *>(v_res + off));
             }
         }
     }
@@ -278,8 +284,8 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
                 unpack8(kraw[i], x);
                 uint32_t a, r;
                 quantize_split8(x, kz, ki, a, r);
-                *reinterpret_cast<uint32_t *>(k_anc + off) = a;
-                *reinterpret_cast<uint32_t *>(k_res + off) = r;
+                __builtin_nontemporal_store(a, reinterpret_cast<uint32_t *>(k_anc + off));
+                __builtin_nontemporal_store(r, reinterpret_cast<uint32_t *>(k_res + off));
             }
         }
     }
