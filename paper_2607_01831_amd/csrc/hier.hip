@@ -239,7 +239,7 @@ __global__ __launch_bounds__(kHThreads, 3) void hencode_kernel(
 
 __device__ __forceinline__ int sext4(uint32_t nib) { return (int)nib >= 8 ? (int)nib - 16 : (int)nib; }
 
-// Dequantization to BF16 [T][Hkv][128]: thread (token row, 8 dims), per
+// Dequantization to BF16 [T][Hkv][128]: thread (8 tokens, 8 dims), per
 // dimension the level of the code the variant names (biased: 16 V for the
 // anchor, 16 V - Q_res for the merged code; centred: the bucket centre
 // 16 V + 7.5, or 16 V + 8 + Q_res; 4-bit: V), x = ((+-level * sigma) + mu) *
@@ -256,47 +256,22 @@ __global__ __launch_bounds__(kHThreads) void hdequant_kernel(
     if (threadIdx.x < 8) s_alevel[threadIdx.x] = tab.alevel[threadIdx.x];
     __syncthreads();
     const int Hkv = geo.Hkv;
-    const size_t per = (size_t)T * Hkv * 16;  // (token, head, 8-dim piece) items per tensor
+    // item (tensor, token octet, head, 8-dim piece), the piece fastest: a
+    // thread loads the page and chunk scalars of its 8 dims once and
+    // reconstructs 8 consecutive tokens (an octet never straddles a chunk)
+    const int n_oct = (T + 7) / 8;
+    const size_t per = (size_t)n_oct * Hkv * 16;
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
     for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * per; e += stride) {
         const int which = e >= per ? 1 : 0;
         const size_t r = e - (size_t)which * per;
         const int d8 = (int)(r & 15);
-        const size_t th = r >> 4;  // t * Hkv + h
-        const int h = (int)(th % Hkv);
-        const int t = (int)(th / Hkv);
-        int blk, tb;
-        if (LAYOUT == 0) {
-            blk = bt_row[0];
-            tb = t;
-        } else {
-            const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
-            blk = bt_row[bi];
-            tb = t - bi * geo.bt;
-        }
-        if (blk < 0 || blk >= geo.num_blocks) continue;
-        const size_t row = ((size_t)blk * Hkv + h) * geo.bt + tb;
-        const uint8_t *plane = which == 0 ? k_plane : v_plane;
-        int qa[8], qr[8];
-        if (FULL) {
-            const uint2 cw = *reinterpret_cast<const uint2 *>(plane + row * kCodeRow + 8 * d8);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t c = ((j < 4 ? cw.x : cw.y) >> (8 * (j & 3))) & 0xffu;
-                qa[j] = sext4(c >> 4);
-                qr[j] = sext4(c & 15u);
-            }
-        } else {
-            const uint32_t w = *reinterpret_cast<const uint32_t *>(plane + row * kNibbleRow + 4 * d8);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                qa[j] = sext4((w >> (4 * j)) & 15u);
-                qr[j] = 0;
-            }
-        }
-        const size_t pm = (((size_t)b * Hkv + h) * geo.n_pages + t / kPage) * kHeadDim + 8 * d8;
-        const size_t cm = (((size_t)b * Hkv + h) * geo.n_chunks + t / kChunk) * kHeadDim + 8 * d8;
+        const size_t oh = r >> 4;  // octet * Hkv + h
+        const int h = (int)(oh % Hkv);
+        const int t0 = 8 * (int)(oh / Hkv);
+        const size_t pm = (((size_t)b * Hkv + h) * geo.n_pages + t0 / kPage) * kHeadDim + 8 * d8;
+        const size_t cm = (((size_t)b * Hkv + h) * geo.n_chunks + t0 / kChunk) * kHeadDim + 8 * d8;
         const float *gmin_a = which == 0 ? meta.k_gmin : meta.v_gmin;
         const float *gsc_a = which == 0 ? meta.k_gscale : meta.v_gscale;
         const float *mu_a = which == 0 ? meta.k_mu : meta.v_mu;
@@ -313,34 +288,70 @@ __global__ __launch_bounds__(kHThreads) void hdequant_kernel(
             mu[4 * k4] = m.x; mu[4 * k4 + 1] = m.y; mu[4 * k4 + 2] = m.z; mu[4 * k4 + 3] = m.w;
             sg[4 * k4] = g.x; sg[4 * k4 + 1] = g.y; sg[4 * k4 + 2] = g.z; sg[4 * k4 + 3] = g.w;
         }
-        uint32_t o[4];
-#pragma unroll
-        for (int j = 0; j < 8; j += 2) {
-            uint32_t hb[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const int a = qa[j + u];
-                const int V = a >= 0 ? a : -a - 1;
-                float lv;
-                if (variant == kHBiased) {
-                    int Ip = 16 * V - qr[j + u];
-                    Ip = Ip < 0 ? 0 : (Ip > 127 ? 127 : Ip);
-                    lv = s_level[Ip];
-                } else if (variant == kHCentred) {
-                    lv = FULL ? s_level[16 * V + 8 + qr[j + u]] : s_alevel[V];
-                } else {
-                    lv = s_level[V];
-                }
-                const float m = a >= 0 ? lv : -lv;
-                const float xc = mul_rn(m, sg[j + u]);
-                const float X = xc + mu[j + u];
-                const float x = mul_rn(X, gs[j + u]) + gm[j + u];
-                hb[u] = bf16_rne(x);
-            }
-            o[j / 2] = hb[0] | (hb[1] << 16);
-        }
+        const uint8_t *plane = which == 0 ? k_plane : v_plane;
         uint16_t *out = which == 0 ? k_out : v_out;
-        *reinterpret_cast<uint4 *>(out + ((size_t)t * Hkv + h) * kHeadDim + 8 * d8) = make_uint4(o[0], o[1], o[2], o[3]);
+        const int nt = min(8, T - t0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            if (k >= nt) break;
+            const int t = t0 + k;
+            int blk, tb;
+            if (LAYOUT == 0) {
+                blk = bt_row[0];
+                tb = t;
+            } else {
+                const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
+                blk = bt_row[bi];
+                tb = t - bi * geo.bt;
+            }
+            if (blk < 0 || blk >= geo.num_blocks) continue;
+            const size_t row = ((size_t)blk * Hkv + h) * geo.bt + tb;
+            int qa[8], qr[8];
+            if (FULL) {
+                const uint2 cw = *reinterpret_cast<const uint2 *>(plane + row * kCodeRow + 8 * d8);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const uint32_t c = ((j < 4 ? cw.x : cw.y) >> (8 * (j & 3))) & 0xffu;
+                    qa[j] = sext4(c >> 4);
+                    qr[j] = sext4(c & 15u);
+                }
+            } else {
+                const uint32_t w = *reinterpret_cast<const uint32_t *>(plane + row * kNibbleRow + 4 * d8);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    qa[j] = sext4((w >> (4 * j)) & 15u);
+                    qr[j] = 0;
+                }
+            }
+            uint32_t o[4];
+#pragma unroll
+            for (int j = 0; j < 8; j += 2) {
+                uint32_t hb[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int a = qa[j + u];
+                    const int V = a >= 0 ? a : -a - 1;
+                    float lv;
+                    if (variant == kHBiased) {
+                        int Ip = 16 * V - qr[j + u];
+                        Ip = Ip < 0 ? 0 : (Ip > 127 ? 127 : Ip);
+                        lv = s_level[Ip];
+                    } else if (variant == kHCentred) {
+                        lv = FULL ? s_level[16 * V + 8 + qr[j + u]] : s_alevel[V];
+                    } else {
+                        lv = s_level[V];
+                    }
+                    const float m = a >= 0 ? lv : -lv;
+                    const float xc = mul_rn(m, sg[j + u]);
+                    const float X = xc + mu[j + u];
+                    const float x = mul_rn(X, gs[j + u]) + gm[j + u];
+                    hb[u] = bf16_rne(x);
+                }
+                o[j / 2] = hb[0] | (hb[1] << 16);
+            }
+            *reinterpret_cast<uint4 *>(out + ((size_t)t * Hkv + h) * kHeadDim + 8 * d8) =
+                make_uint4(o[0], o[1], o[2], o[3]);
+        }
     }
 }
 
@@ -386,7 +397,7 @@ hipError_t launch_hdequant(bool full, const Geometry &g, int b, int T, const int
                            const HTables &tab, int variant, uint16_t *k_out, uint16_t *v_out,
                            hipStream_t stream) {
     if (T <= 0) return hipSuccess;
-    size_t blocks = ((size_t)2 * T * g.Hkv * 16 + kHThreads - 1) / kHThreads;
+    size_t blocks = ((size_t)2 * ((T + 7) / 8) * g.Hkv * 16 + kHThreads - 1) / kHThreads;
     if (blocks > 256 * 32) blocks = 256 * 32;
     const dim3 grid((unsigned)blocks);
     const int sh = shift_of(g.bt);
