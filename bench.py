@@ -632,8 +632,12 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
 
     table = torch.zeros(1, 1, dtype=torch.int32, device=dev)
     lens = torch.tensor([T], dtype=torch.int32, device=dev)
-    hp = lynx.KVPool.allocate(L, 1, device=dev)
-    hm = lynx.HMeta.empty(L, 1, device=dev)
+    # layer l encodes into pool l % R and is dequantized from there: R pools
+    # hold more than the last-level cache, so every timed call starts cold
+    R = 12
+    hps = [lynx.KVPool.allocate(L, 1, device=dev) for _ in range(R)]
+    hms = [lynx.HMeta.empty(L, 1, device=dev) for _ in range(R)]
+    hp, hm = hps[0], hms[0]
     ko = torch.empty(T, Hkv, 128, dtype=torch.bfloat16, device=dev)
     vo = torch.empty_like(ko)
     ev = lambda: torch.cuda.Event(enable_timing=True)
@@ -651,10 +655,11 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (reps * n_layers)
 
-    def encode(l, a, vid):
+    def encode(l, a, vid, into=None):
         res = vid != lynx.LYNX_HQ_INT4
-        lynx.lynx_hkv_encode(L, 0, T, table, K[l], V[l], a, vid, hp.k_anc, hp.v_anc,
-                             hp.k_res if res else None, hp.v_res if res else None, hm)
+        p, m = (hps[l % R], hms[l % R]) if into is None else into
+        lynx.lynx_hkv_encode(L, 0, T, table, K[l], V[l], a, vid, p.k_anc, p.v_anc,
+                             p.k_res if res else None, p.v_res if res else None, m)
 
     elems = T * Hkv * 128 * 2
     meta_b = 4.0 * 2 * (1 / 256 + 1 / 32)          # page and chunk fp32 pairs per element
@@ -662,16 +667,18 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
     for name, vid in variants.items():
         res = vid != lynx.LYNX_HQ_INT4
         t_enc = timed(lambda: [encode(l, a0, vid) for l in range(n_layers)])
-        t_da = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, False, hp.k_anc, hp.v_anc, a0, vid, hm,
-                                                    ko, vo) for _ in range(n_layers)])
+        t_da = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, False, hps[l % R].k_anc, hps[l % R].v_anc,
+                                                    a0, vid, hms[l % R], ko, vo) for l in range(n_layers)])
         t = {"encode_us_per_layer": round(t_enc, 2),
              "encode_GBps": round(elems * (2 + (1 if res else 0.5) + meta_b) / (t_enc * 1e-6) / 1e9, 1),
              "dequant_anchor_us_per_layer": round(t_da, 2),
              "dequant_anchor_GBps": round(elems * (0.5 + meta_b + 2) / (t_da * 1e-6) / 1e9, 1)}
         if res:
-            hp.merge()
-            t_df = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, True, hp.k_codes, hp.v_codes, a0, vid,
-                                                        hm, ko, vo) for _ in range(n_layers)])
+            for p in hps:
+                p.merge()
+            t_df = timed(lambda: [lynx.lynx_hkv_dequant(L, 0, T, table, True, hps[l % R].k_codes,
+                                                        hps[l % R].v_codes, a0, vid, hms[l % R], ko, vo)
+                                  for l in range(n_layers)])
             t["dequant_full_us_per_layer"] = round(t_df, 2)
             t["dequant_full_GBps"] = round(elems * (1 + meta_b + 2) / (t_df * 1e-6) / 1e9, 1)
         r["timed"][name] = t
@@ -704,7 +711,7 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
         acc.setdefault("uniform_full", []).append(vnmse(outv[0, 0].float(), o))
         for a in alphas:
             for name, vid in variants.items():
-                encode(l, a, vid)
+                encode(l, a, vid, into=(hp, hm))
                 modes = [("anchor", False, (hp.k_anc, hp.v_anc))]
                 if vid != lynx.LYNX_HQ_INT4:
                     hp.merge()
@@ -716,7 +723,7 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
     torch.cuda.synchronize()
     r["vnmse"] = {k: float(f"{sum(v) / len(v):.3g}") for k, v in acc.items()}
     r["vnmse_layers"] = len(layers)
-    del hp, hm, ko, vo
+    del hp, hm, hps, hms, ko, vo
     return {"hier_codec": r}
 
 
