@@ -616,7 +616,7 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
 
 def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0, 1.0)):
     """The paper's own hierarchical codec (Alg. 1) on the workload's layers,
-    in its three variants (the listing's biased split, the centred split that
+    in its three variants (Alg. 1's biased split, the centred split that
     keeps every code, the single 4-bit code): encode, and dequantization of
     the anchor alone and of the merged codes to BF16 pages, each timed over
     all layers in turn (HIP events); then the compression error
@@ -769,8 +769,8 @@ def main():
         summarize_pmc(*args.summarize_pmc)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
-              "multi-GPU path (DESIGN.md describes how it would shard).", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no "
+              "multi-GPU path; it would shard by kv head or along the context.", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -354,10 +354,10 @@ int lynx_kv_deserialize_residual(const lynx_layout *L, int32_t b, int32_t t0, in
  * plane layout).  The anchor carries the sign with the sign-aware map
  * (Q_anc = V, or -V - 1 for a negative value, so a negative zero keeps its
  * sign).  alpha is not fixed by the paper.  Variants (the variant argument):
- *   LYNX_HQ_BIASED   the listing's biased split, M = 127: anchor
+ *   LYNX_HQ_BIASED   Alg. 1's biased split, M = 127: anchor
  *                    V = min((I + 7) >> 4, 7), correction
  *                    Q_res = clamp(16 V - I, -8, 7).  Codes above 120 come
- *                    back as 120: the listing's anchor reaches 8 there,
+ *                    back as 120: Alg. 1's anchor reaches 8 there,
  *                    which four signed bits cannot hold.
  *   LYNX_HQ_CENTRED  the split that keeps every code, M = 127: anchor
  *                    V = I >> 4 (sign and top three bits), correction

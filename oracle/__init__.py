@@ -420,7 +420,7 @@ def deserialize_residual(L: Layout, b: int, t0: int, n: int, block_table: np.nda
 # Hierarchical non-linear codec (Alg. 1, Sec. 4.1): pages of 256 tokens and
 # chunks of 32 per channel, alpha-law transform to a magnitude code and a
 # sign, split into a signed 4-bit anchor and a signed 4-bit correction.  The
-# variants of the split and the readings of the garbled parts of the listing
+# variants of the split and the readings of the garbled parts of Alg. 1
 # are stated in lynx_oracle.c.
 # --------------------------------------------------------------------------
 

@@ -522,7 +522,7 @@ int oracle_verify(int Hkv, int bt, int max_blocks, int max_tokens, int B, int Hq
  *      bucket V with the sign-aware map Q_anc = V for S >= 0 and -V - 1 for
  *      S < 0, so a zero magnitude keeps its sign.
  * Three variants of stage 4 (the variant argument):
- *   0 (biased): the listing's split: V = (I + 7) >> 4, the magnitude rounded
+ *   0 (biased): Alg. 1's split: V = (I + 7) >> 4, the magnitude rounded
  *     half down to a multiple of 16, Q_res = 16 V - I.  V reaches 8 for
  *     I >= 121, which 4 bits cannot hold with a sign: V is clamped to 7 and
  *     Q_res to [-8, 7], so codes above 120 come back as 120.  The anchor
@@ -537,8 +537,8 @@ int oracle_verify(int Hkv, int bt, int max_blocks, int max_tokens, int B, int Hq
  *   2 (4-bit): the single-precision 4-bit configuration of Sec. 6.1: stage 3
  *     with M = 7 (three magnitude bits and a sign), the anchor holding
  *     Q = I or -I - 1 and no residual.
- * Readings where the listing is garbled or at odds with the 4-bit streams:
- *   - the sign is that of the centred value Xc (the listing's X_view is
+ * Readings where Alg. 1 is garbled or at odds with the 4-bit streams:
+ *   - the sign is that of the centred value Xc (Alg. 1's X_view is
  *     non-negative after stage 1);
  *   - no epsilon: a page (chunk) whose range (sigma) has no finite positive
  *     reciprocal normalizes to 0;

@@ -15,7 +15,7 @@ only.  What the pins rest on, other than the oracle itself:
   - a worked example computed by hand (alpha = 1);
   - error bounds of the reconstruction.
 
-The split has three variants (stated in lynx_oracle.c): the listing's biased
+The split has three variants (stated in lynx_oracle.c): Alg. 1's biased
 split with the 4-bit clamp, the centred split that keeps every code, and the
 single 4-bit code.  The centred and 4-bit ones are pinned by the same kinds
 of facts: the transform with M = 7 for the 4-bit code, the split's stated
