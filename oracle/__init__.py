@@ -61,6 +61,12 @@ def _load():
     lib.oracle_anchor_decode_tail.restype = I
     F = ctypes.c_float
     IP = ctypes.POINTER(ctypes.c_int)
+    lib.oracle_encode_split.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_encode_split.restype = I
+    lib.oracle_merge_split.argtypes = [I, ctypes.c_size_t, P, P, P]
+    lib.oracle_merge_split.restype = I
+    lib.oracle_dequant_anchor_split.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P]
+    lib.oracle_dequant_anchor_split.restype = I
     lib.oracle_accept_sample.argtypes = [I, I, I, P, P, P, P, P, P]
     lib.oracle_accept_sample.restype = I
     lib.oracle_hsplit.argtypes = [I, I, I, IP, IP]
@@ -513,4 +519,55 @@ def hdequant(mode: str, L: Layout, b: int, T: int, block_table: np.ndarray,
                                  _ptr(v_out))
     if rc != 0:
         raise ValueError(f"oracle_hdequant rejected its arguments ({rc})")
+    return k_out, v_out
+
+
+# --------------------------------------------------------------------------
+# Split widths other than 4 + 4 (Sec. 7): an A-bit anchor c >> (8 - A) and an
+# (8 - A)-bit residual, rows of 128 elements as little-endian bit strings
+# (16 W bytes a row); the readings are stated in lynx_oracle.c.
+# --------------------------------------------------------------------------
+
+def encode_split(A: int, L: Layout, b: int, T: int, block_table: np.ndarray, k_bits: np.ndarray,
+                 v_bits: np.ndarray, planes: dict, meta: Meta) -> None:
+    """Encode sequence b into planes['k_anc'|'v_anc'] (rows of 16 A bytes),
+    planes['k_res'|'v_res'] (rows of 16 (8 - A) bytes) and meta (as encode)."""
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    k_bits = np.ascontiguousarray(k_bits, dtype=np.uint16)
+    v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
+    rc = _load().oracle_encode_split(A, L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T, _ptr(bt_arr),
+                                     _ptr(k_bits), _ptr(v_bits), _ptr(planes["k_anc"]),
+                                     _ptr(planes["v_anc"]), _ptr(planes["k_res"]), _ptr(planes["v_res"]),
+                                     _ptr(meta.k_scale), _ptr(meta.k_zero), _ptr(meta.v_scale),
+                                     _ptr(meta.v_zero))
+    if rc != 0:
+        raise ValueError(f"oracle_encode_split rejected its arguments ({rc})")
+
+
+def merge_split(A: int, anc: np.ndarray, res: np.ndarray) -> np.ndarray:
+    """Rows of A-bit anchors and (8 - A)-bit residuals -> rows of 128 codes."""
+    anc = np.ascontiguousarray(anc, dtype=np.uint8)
+    res = np.ascontiguousarray(res, dtype=np.uint8)
+    n_rows = anc.size // (16 * A)
+    assert anc.size == n_rows * 16 * A and res.size == n_rows * 16 * (8 - A)
+    codes = np.zeros(n_rows * HEAD_DIM, np.uint8)
+    if _load().oracle_merge_split(A, n_rows, _ptr(anc), _ptr(res), _ptr(codes)) != 0:
+        raise ValueError("oracle_merge_split rejected its arguments")
+    return codes
+
+
+def dequant_anchor_split(A: int, L: Layout, b: int, T: int, block_table: np.ndarray,
+                         k_anc: np.ndarray, v_anc: np.ndarray, meta: Meta):
+    """K, V of sequence b from the A-bit anchors alone, as BF16 bits
+    (uint16 [T][Hkv][128])."""
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    k_out = np.zeros((T, L.Hkv, HEAD_DIM), np.uint16)
+    v_out = np.zeros_like(k_out)
+    rc = _load().oracle_dequant_anchor_split(A, L.Hkv, L.bt, L.max_blocks, L.max_tokens, b, T,
+                                             _ptr(bt_arr), _ptr(k_anc), _ptr(v_anc),
+                                             _ptr(meta.k_scale), _ptr(meta.k_zero),
+                                             _ptr(meta.v_scale), _ptr(meta.v_zero),
+                                             _ptr(k_out), _ptr(v_out))
+    if rc != 0:
+        raise ValueError(f"oracle_dequant_anchor_split rejected its arguments ({rc})")
     return k_out, v_out

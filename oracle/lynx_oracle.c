@@ -875,3 +875,136 @@ int oracle_accept_sample(int B, int k, int V, const float *p, const float *q,
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Split widths other than 4 + 4 (the paper's future work, Sec. 7)           */
+/* ------------------------------------------------------------------------ */
+/*
+ * The uniform codec's 8-bit code c split into an anchor of A bits, c >> R,
+ * and a residual of R = 8 - A bits, c & (2^R - 1), for A in {2, 4, 6}.
+ * A plane row holds the 128 elements of one token and kv head as a
+ * little-endian bit string: element e at bits e W .. e W + W - 1 (W = A or
+ * R), byte j holding bits 8 j .. 8 j + 7, so a row is 16 W bytes.  W = 4 is
+ * the nibble layout of the 4 + 4 planes.  Merging gives back c = (a << R) | r.
+ * The anchor alone stands for code 2^R a + (2^R - 1) / 2, the middle of the
+ * codes it covers, dequantized as the fp32 fmaf(code, scale, zero) rounded
+ * to BF16 to nearest even (the BF16 pages of the paper's anchor phase).
+ */
+static void put_field(uint8_t *row, int e, int w, int val)
+{
+    for (int i = 0; i < w; ++i) {
+        const int bit = e * w + i;
+        const uint8_t m = (uint8_t)(1u << (bit % 8));
+        if ((val >> i) & 1)
+            row[bit / 8] |= m;
+        else
+            row[bit / 8] &= (uint8_t)~m;
+    }
+}
+
+static int get_field(const uint8_t *row, int e, int w)
+{
+    int v = 0;
+    for (int i = 0; i < w; ++i) {
+        const int bit = e * w + i;
+        v |= ((row[bit / 8] >> (bit % 8)) & 1) << i;
+    }
+    return v;
+}
+
+static int split_ok(int A) { return A == 2 || A == 4 || A == 6; }
+
+/* As oracle_encode, with anchor rows of 16 A bytes and residual rows of
+ * 16 (8 - A) bytes.  Returns 0, or -1. */
+int oracle_encode_split(int A, int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
+                        const int32_t *block_table, const uint16_t *k, const uint16_t *v,
+                        uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
+                        float *k_scale, float *k_zero, float *v_scale, float *v_zero)
+{
+    if (!split_ok(A) || Hkv < 1 || bt < 1 || T < 0 || T > max_tokens ||
+        (size_t)(T + bt - 1) / (size_t)bt > (size_t)max_blocks)
+        return -1;
+    const int R = 8 - A;
+    const int32_t *bt_row = block_table + (size_t)b * (size_t)max_blocks;
+    const int n_groups_max = (max_tokens + K_GROUP - 1) / K_GROUP;
+    float vals[K_GROUP > HEAD_DIM ? K_GROUP : HEAD_DIM];
+    for (int h = 0; h < Hkv; ++h) {
+        for (int g = 0; g * K_GROUP < T; ++g) {
+            const int t0 = g * K_GROUP;
+            const int t1 = t0 + K_GROUP < T ? t0 + K_GROUP : T;
+            for (int d = 0; d < HEAD_DIM; ++d) {
+                for (int t = t0; t < t1; ++t)
+                    vals[t - t0] = bf16_bits_to_float(k[((size_t)t * Hkv + h) * HEAD_DIM + d]);
+                float scale, zero, inv;
+                group_stats(vals, t1 - t0, &scale, &zero, &inv);
+                for (int t = t0; t < t1; ++t) {
+                    const int c = quantize(vals[t - t0], zero, inv);
+                    put_field(k_anc + plane_row_offset(bt_row, Hkv, bt, h, t, 16 * A), d, A, c >> R);
+                    put_field(k_res + plane_row_offset(bt_row, Hkv, bt, h, t, 16 * R), d, R,
+                              c & ((1 << R) - 1));
+                }
+                const size_t km = (((size_t)b * Hkv + h) * n_groups_max + g) * HEAD_DIM + d;
+                k_scale[km] = scale;
+                k_zero[km] = zero;
+            }
+        }
+        for (int t = 0; t < T; ++t) {
+            for (int d = 0; d < HEAD_DIM; ++d)
+                vals[d] = bf16_bits_to_float(v[((size_t)t * Hkv + h) * HEAD_DIM + d]);
+            float scale, zero, inv;
+            group_stats(vals, HEAD_DIM, &scale, &zero, &inv);
+            for (int d = 0; d < HEAD_DIM; ++d) {
+                const int c = quantize(vals[d], zero, inv);
+                put_field(v_anc + plane_row_offset(bt_row, Hkv, bt, h, t, 16 * A), d, A, c >> R);
+                put_field(v_res + plane_row_offset(bt_row, Hkv, bt, h, t, 16 * R), d, R,
+                          c & ((1 << R) - 1));
+            }
+            const size_t vm = ((size_t)b * Hkv + h) * (size_t)max_tokens + t;
+            v_scale[vm] = scale;
+            v_zero[vm] = zero;
+        }
+    }
+    return 0;
+}
+
+/* n_rows rows of anchors (16 A bytes each) and residuals (16 (8 - A)) ->
+ * n_rows rows of 128 codes.  Returns 0, or -1. */
+int oracle_merge_split(int A, size_t n_rows, const uint8_t *anc, const uint8_t *res, uint8_t *codes)
+{
+    if (!split_ok(A)) return -1;
+    const int R = 8 - A;
+    for (size_t r = 0; r < n_rows; ++r)
+        for (int e = 0; e < HEAD_DIM; ++e)
+            codes[r * HEAD_DIM + e] = (uint8_t)((get_field(anc + r * 16 * A, e, A) << R) |
+                                                get_field(res + r * 16 * R, e, R));
+    return 0;
+}
+
+/* Sequence b's K and V from the anchors alone as BF16 bits [T][Hkv][128].
+ * Returns 0, or -1. */
+int oracle_dequant_anchor_split(int A, int Hkv, int bt, int max_blocks, int max_tokens, int b, int T,
+                                const int32_t *block_table, const uint8_t *k_anc,
+                                const uint8_t *v_anc, const float *k_scale, const float *k_zero,
+                                const float *v_scale, const float *v_zero, uint16_t *k_out,
+                                uint16_t *v_out)
+{
+    if (!split_ok(A) || Hkv < 1 || T < 0 || T > max_tokens) return -1;
+    const int R = 8 - A;
+    const float half = (float)((1 << R) - 1) / 2.0f;
+    const int32_t *bt_row = block_table + (size_t)b * (size_t)max_blocks;
+    const int n_groups_max = (max_tokens + K_GROUP - 1) / K_GROUP;
+    for (int t = 0; t < T; ++t)
+        for (int h = 0; h < Hkv; ++h) {
+            const size_t off = plane_row_offset(bt_row, Hkv, bt, h, t, 16 * A);
+            const size_t vm = ((size_t)b * Hkv + h) * (size_t)max_tokens + t;
+            for (int d = 0; d < HEAD_DIM; ++d) {
+                const size_t km = (((size_t)b * Hkv + h) * n_groups_max + t / K_GROUP) * HEAD_DIM + d;
+                const float qk = (float)(get_field(k_anc + off, d, A) << R) + half;
+                const float qv = (float)(get_field(v_anc + off, d, A) << R) + half;
+                const size_t o = ((size_t)t * Hkv + h) * HEAD_DIM + d;
+                k_out[o] = float_to_bf16_rne(fmaf(qk, k_scale[km], k_zero[km]));
+                v_out[o] = float_to_bf16_rne(fmaf(qv, v_scale[vm], v_zero[vm]));
+            }
+        }
+    return 0;
+}

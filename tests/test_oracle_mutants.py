@@ -121,3 +121,30 @@ def test_sample_pins_catch_mutant(name, tmp_path):
                         "tests/test_oracle_spec_sample.py"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+# Planted mistakes in the split widths, each of which the pins in
+# test_oracle_split.py must catch.
+SPLIT_MUTANTS = {
+    "field_bits_reversed": ("v |= ((row[bit / 8] >> (bit % 8)) & 1) << i;",
+                            "v |= ((row[bit / 8] >> (bit % 8)) & 1) << (w - 1 - i);"),
+    "merge_shifts_by_anchor_width": ("codes[r * HEAD_DIM + e] = (uint8_t)((get_field(anc + r * 16 * A, e, A) << R) |",
+                                     "codes[r * HEAD_DIM + e] = (uint8_t)((get_field(anc + r * 16 * A, e, A) << A) |"),
+    "anchor_value_at_bucket_floor": ("const float half = (float)((1 << R) - 1) / 2.0f;", "const float half = 0.0f;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SPLIT_MUTANTS))
+def test_split_pins_catch_mutant(name, tmp_path):
+    find, repl = SPLIT_MUTANTS[name]
+    assert SRC.count(find) == 1, f"mutation anchor for {name} not unique/present"
+    src = tmp_path / "mutant.c"
+    src.write_text(SRC.replace(find, repl))
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-shared", "-fPIC",
+                    "-pthread", str(src), "-o", str(lib), "-lm"], check=True)
+    env = dict(os.environ, LYNX_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        "tests/test_oracle_split.py"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
