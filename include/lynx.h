@@ -344,6 +344,50 @@ int lynx_kv_deserialize_residual(const lynx_layout *L, int32_t b, int32_t t0, in
                                  uint8_t *v_codes, void *stream);
 
 /*
+ * Split widths other than 4 + 4 (the paper leaves them to future work,
+ * Sec. 7): the same 8-bit codes as lynx_kv_encode, split into an anchor of
+ * A = anchor_bits bits (code >> (8 - A)) and a residual of R = 8 - A bits
+ * (code & (2^R - 1)), A in {2, 4, 6}.  A plane row (one token of one kv
+ * head) holds the 128 fields as a little-endian bit string: element e at
+ * bits e W .. e W + W - 1 (W = A or R), so anchor rows are 16 A bytes and
+ * residual rows 16 R bytes, at row index ((block * Hkv + h) * bt + t % bt)
+ * as in the 4 + 4 planes.  A = 4 gives exactly the 4 + 4 planes.  Merged
+ * codes are those of lynx_kv_merge, so lynx_attn_verify reads them as is.
+ */
+
+/*
+ * lynx_kv_encode_split -- encode one sequence (one layer) with an A + R
+ * split.  Arguments as lynx_kv_encode; the planes hold rows of 16 A (anchor)
+ * and 16 R (residual) bytes.  Launches one kernel.
+ */
+int lynx_kv_encode_split(const lynx_layout *L, int32_t anchor_bits, int32_t b, int32_t T,
+                         const int32_t *block_table, const void *k_bf16, const void *v_bf16,
+                         uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
+                         const lynx_meta *meta, void *stream);
+
+/*
+ * lynx_kv_merge_split -- n_rows rows of A-bit anchors (16 A bytes each) and
+ * R-bit residuals (16 R bytes) into n_rows rows of 128 code bytes, row for
+ * row (device, 16-byte aligned; codes must not overlap an input).  Launches
+ * one kernel.
+ */
+int lynx_kv_merge_split(int32_t anchor_bits, size_t n_rows, const uint8_t *anc, const uint8_t *res,
+                        uint8_t *codes, void *stream);
+
+/*
+ * lynx_kv_dequant_anchor_split -- the anchor phase's BF16 pages for an
+ * A + R split (Sec. 4.2 dequantizes anchors into BF16 pages): sequence b's
+ * K and V [T][Hkv][128] (device, written) from the anchor planes alone, the
+ * anchor a standing for code 2^R a + (2^R - 1) / 2, the middle of the codes
+ * it covers: x = fmaf(code, scale, zero) in fp32, rounded to BF16 to
+ * nearest even.  Launches one kernel.
+ */
+int lynx_kv_dequant_anchor_split(const lynx_layout *L, int32_t anchor_bits, int32_t b, int32_t T,
+                                 const int32_t *block_table, const uint8_t *k_anc,
+                                 const uint8_t *v_anc, const lynx_meta *meta, void *k_out_bf16,
+                                 void *v_out_bf16, void *stream);
+
+/*
  * The hierarchical non-linear codec of Alg. 1 (Sec. 4.1), the paper's own
  * quantizer, as an alternative to the uniform 8-bit one.  Per channel of a
  * kv head (K and V alike), over pages of 256 tokens and chunks of 32:

@@ -112,6 +112,65 @@ int lynx_kv_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
 
+int lynx_kv_encode_split(const lynx_layout *L, int32_t anchor_bits, int32_t b, int32_t T,
+                         const int32_t *block_table, const void *k_bf16, const void *v_bf16,
+                         uint8_t *k_anc, uint8_t *v_anc, uint8_t *k_res, uint8_t *v_res,
+                         const lynx_meta *meta, void *stream) {
+    if (anchor_bits != 2 && anchor_bits != 4 && anchor_bits != 6) return LYNX_EINVAL;
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_layout(L, &g);
+    if (rc != LYNX_OK) return rc;
+    if ((rc = check_meta(meta, &mp)) != LYNX_OK) return rc;
+    if (b < 0 || T < 0 || T > layout_capacity(g)) return LYNX_EINVAL;
+    if (T == 0) return LYNX_OK;
+    const void *ptrs[] = {block_table, k_bf16, v_bf16, k_anc, v_anc, k_res, v_res};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    hipError_t e = lynx::launch_encode(g, b, T, block_table, static_cast<const uint16_t *>(k_bf16),
+                                       static_cast<const uint16_t *>(v_bf16), k_anc, v_anc, k_res,
+                                       v_res, mp, static_cast<hipStream_t>(stream), anchor_bits);
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_kv_merge_split(int32_t anchor_bits, size_t n_rows, const uint8_t *anc, const uint8_t *res,
+                        uint8_t *codes, void *stream) {
+    if (anchor_bits != 2 && anchor_bits != 4 && anchor_bits != 6) return LYNX_EINVAL;
+    if (n_rows == 0) return LYNX_OK;
+    if (n_rows > ((size_t)1 << 40)) return LYNX_EINVAL;
+    if (!anc || !res || !codes || !aligned16(anc) || !aligned16(res) || !aligned16(codes))
+        return LYNX_EINVAL;
+    const size_t na = n_rows * 16 * (size_t)anchor_bits, nr = n_rows * 16 * (size_t)(8 - anchor_bits);
+    const uintptr_t c0 = reinterpret_cast<uintptr_t>(codes), c1 = c0 + n_rows * lynx::kCodeRow;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(anc), r0 = reinterpret_cast<uintptr_t>(res);
+    if ((a0 < c1 && c0 < a0 + na) || (r0 < c1 && c0 < r0 + nr)) return LYNX_EINVAL;
+    hipError_t e = lynx::launch_merge_split(anchor_bits, anc, res, codes, n_rows,
+                                            static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+int lynx_kv_dequant_anchor_split(const lynx_layout *L, int32_t anchor_bits, int32_t b, int32_t T,
+                                 const int32_t *block_table, const uint8_t *k_anc,
+                                 const uint8_t *v_anc, const lynx_meta *meta, void *k_out_bf16,
+                                 void *v_out_bf16, void *stream) {
+    if (anchor_bits != 2 && anchor_bits != 4 && anchor_bits != 6) return LYNX_EINVAL;
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_layout(L, &g);
+    if (rc != LYNX_OK) return rc;
+    if ((rc = check_meta(meta, &mp)) != LYNX_OK) return rc;
+    if (b < 0 || T < 0 || T > layout_capacity(g)) return LYNX_EINVAL;
+    if (T == 0) return LYNX_OK;
+    const void *ptrs[] = {block_table, k_anc, v_anc, k_out_bf16, v_out_bf16};
+    for (const void *p : ptrs)
+        if (!p || !aligned16(p)) return LYNX_EINVAL;
+    hipError_t e = lynx::launch_dequant_anchor_split(anchor_bits, g, b, T, block_table, k_anc, v_anc, mp,
+                                                     static_cast<uint16_t *>(k_out_bf16),
+                                                     static_cast<uint16_t *>(v_out_bf16),
+                                                     static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
 size_t lynx_attn_workspace_bytes(const lynx_layout *L, int32_t B, int32_t Hq,
                                  int32_t num_queries, int32_t max_seq_len) {
     Geometry g;

@@ -122,6 +122,48 @@ __device__ __forceinline__ void quantize_split8(const float *x, const float *zer
 
 typedef unsigned int u32v4 __attribute__((ext_vector_type(4)));
 
+// Eight values -> eight codes (bytes 0..7 of the result), as quantize_split8.
+__device__ __forceinline__ uint64_t quantize8(const float *x, const float *zero, const float *inv) {
+    uint32_t w[2] = {0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float y = (x[j] - zero[j]) * inv[j];
+        w[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(y, (uint32_t)(j & 3), w[j >> 2]);
+    }
+    return (uint64_t)w[0] | ((uint64_t)w[1] << 32);
+}
+
+// Codes of 8 dims (8 m .. 8 m + 7) of one plane row, split A + (8 - A):
+// the A-bit anchors and the R-bit residuals as little-endian bit strings
+// (A and R bytes), stored at byte A m of the anchor row (16 A bytes) and
+// R m of the residual row.  A = 4 is the nibble path of quantize_split8.
+template <int A>
+__device__ __forceinline__ void store_split(const float *x, const float *zero, const float *inv,
+                                            uint8_t *anc, uint8_t *res, size_t row, int m) {
+    if constexpr (A == 4) {
+        uint32_t a, r;
+        quantize_split8(x, zero, inv, a, r);
+        __builtin_nontemporal_store(a, reinterpret_cast<uint32_t *>(anc + row * kNibbleRow + 4 * m));
+        __builtin_nontemporal_store(r, reinterpret_cast<uint32_t *>(res + row * kNibbleRow + 4 * m));
+    } else {
+        constexpr int R = 8 - A;
+        const uint64_t c = quantize8(x, zero, inv);
+        uint64_t an = 0, rs = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint64_t cj = (c >> (8 * j)) & 0xFFu;
+            an |= (cj >> R) << (A * j);
+            rs |= (cj & ((1u << R) - 1u)) << (R * j);
+        }
+        uint16_t *ap = reinterpret_cast<uint16_t *>(anc + row * (16 * A) + A * m);
+        uint16_t *rp = reinterpret_cast<uint16_t *>(res + row * (16 * R) + R * m);
+#pragma unroll
+        for (int i = 0; i < A / 2; ++i) __builtin_nontemporal_store((uint16_t)(an >> (16 * i)), ap + i);
+#pragma unroll
+        for (int i = 0; i < R / 2; ++i) __builtin_nontemporal_store((uint16_t)(rs >> (16 * i)), rp + i);
+    }
+}
+
 // One workgroup encodes one 128-token window of one kv head for K and V.
 // Thread (tr = tid / 16, m = tid % 16) owns dims 8m..8m+7 of the window's
 // tokens tr, tr+16, ..., tr+112: every 16-byte load is part of a fully used
@@ -129,8 +171,10 @@ typedef unsigned int u32v4 __attribute__((ext_vector_type(4)));
 // row.  LAYOUT 0: one block per sequence; 1: paged; 2: a transmission-buffer
 // object (planes [Hkv][T][64], no block table).  The BF16 input is read once
 // and the planes are not read back by this kernel: nontemporal loads and
-// stores (4.27 -> 4.8 TB/s on a 32K layer).
-template <int LAYOUT>
+// stores (4.27 -> 4.8 TB/s on a 32K layer).  A: anchor bits (4, or the
+// other split widths 2 and 6, whose plane rows are 16 A and 16 (8 - A)
+// bytes).
+template <int LAYOUT, int A = 4>
 __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
     const uint16_t *__restrict__ k, const uint16_t *__restrict__ v, uint8_t *__restrict__ k_anc,
@@ -249,7 +293,7 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
         const int tl = tr + 16 * i;
         if (tl < n) {
             bool ok;
-            const size_t off = plane_row(t0 + tl, ok) * kNibbleRow + 4 * m;
+            const size_t row = plane_row(t0 + tl, ok);
             if (ok) {
                 float x[8];
                 unpack8(vraw[i], x);
@@ -257,10 +301,7 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
                                      vzero[i], vzero[i], vzero[i], vzero[i]};
                 const float iv[8] = {vinv[i], vinv[i], vinv[i], vinv[i],
                                      vinv[i], vinv[i], vinv[i], vinv[i]};
-                uint32_t a, r;
-                quantize_split8(x, zv, iv, a, r);
-                __builtin_nontemporal_store(a, reinterpret_cast<uint32_t *>(v_anc + off));
-                __builtin_nontemporal_store(r, reinterpret_cast<uint32_t *>(v_res + off));
+                store_split<A>(x, zv, iv, v_anc, v_res, row, m);
             }
         }
     }
@@ -278,14 +319,11 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
         const int tl = tr + 16 * i;
         if (tl < n) {
             bool ok;
-            const size_t off = plane_row(t0 + tl, ok) * kNibbleRow + 4 * m;
+            const size_t row = plane_row(t0 + tl, ok);
             if (ok) {
                 float x[8];
                 unpack8(kraw[i], x);
-                uint32_t a, r;
-                quantize_split8(x, kz, ki, a, r);
-                __builtin_nontemporal_store(a, reinterpret_cast<uint32_t *>(k_anc + off));
-                __builtin_nontemporal_store(r, reinterpret_cast<uint32_t *>(k_res + off));
+                store_split<A>(x, kz, ki, k_anc, k_res, row, m);
             }
         }
     }
@@ -446,20 +484,35 @@ unsigned copy_blocks(size_t work) {
 
 }  // namespace
 
-hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_table,
+template <int A>
+void launch_encode_width(const Geometry &g, int b, int T, int bt_shift, const int32_t *block_table,
                          const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
                          uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream) {
-    if (T <= 0) return hipSuccess;
     dim3 grid(g.Hkv, (T + kKGroup - 1) / kKGroup);
+    if (g.max_blocks == 1)
+        hipLaunchKernelGGL((encode_kernel<0, A>), grid, dim3(kEncodeThreads), 0, stream, g, b, T, bt_shift,
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
+    else
+        hipLaunchKernelGGL((encode_kernel<1, A>), grid, dim3(kEncodeThreads), 0, stream, g, b, T, bt_shift,
+                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
+}
+
+hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_table,
+                         const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
+                         uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream,
+                         int anchor_bits) {
+    if (T <= 0) return hipSuccess;
     int bt_shift = -1;
     for (int sh = 0; sh < 31; ++sh)
         if ((1 << sh) == g.bt) bt_shift = sh;
-    if (g.max_blocks == 1)
-        hipLaunchKernelGGL(encode_kernel<0>, grid, dim3(kEncodeThreads), 0, stream, g, b, T, bt_shift,
-                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
+    if (anchor_bits == 4)
+        launch_encode_width<4>(g, b, T, bt_shift, block_table, k, v, k_anc, v_anc, k_res, v_res, meta, stream);
+    else if (anchor_bits == 2)
+        launch_encode_width<2>(g, b, T, bt_shift, block_table, k, v, k_anc, v_anc, k_res, v_res, meta, stream);
+    else if (anchor_bits == 6)
+        launch_encode_width<6>(g, b, T, bt_shift, block_table, k, v, k_anc, v_anc, k_res, v_res, meta, stream);
     else
-        hipLaunchKernelGGL(encode_kernel<1>, grid, dim3(kEncodeThreads), 0, stream, g, b, T, bt_shift,
-                           block_table, k, v, k_anc, v_anc, k_res, v_res, meta);
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
@@ -523,6 +576,164 @@ hipError_t launch_deserialize_residual(const Geometry &g, int b, int t0, int n,
     hipLaunchKernelGGL(deserialize_residual_kernel, dim3(copy_blocks(work)), dim3(kCopyThreads), 0,
                        stream, g, b, t0, n, bt_shift_of(g.bt), block_table, buf, k_anc, v_anc,
                        k_codes, v_codes);
+    return hipGetLastError();
+}
+
+namespace {
+
+// Merge of A-bit anchor rows and R-bit residual rows: thread per 8 elements
+// of a row (A + R bytes in, 8 code bytes out), grid-stride.
+template <int A>
+__global__ __launch_bounds__(kMergeThreads) void merge_split_kernel(const uint8_t *__restrict__ anc,
+                                                                    const uint8_t *__restrict__ res,
+                                                                    uint8_t *__restrict__ codes,
+                                                                    size_t n_pieces) {
+    constexpr int R = 8 - A;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_pieces; i += stride) {
+        const uint16_t *ap = reinterpret_cast<const uint16_t *>(anc + A * i);
+        const uint16_t *rp = reinterpret_cast<const uint16_t *>(res + R * i);
+        uint64_t an = 0, rs = 0;
+#pragma unroll
+        for (int k = 0; k < A / 2; ++k) an |= (uint64_t)ap[k] << (16 * k);
+#pragma unroll
+        for (int k = 0; k < R / 2; ++k) rs |= (uint64_t)rp[k] << (16 * k);
+        uint64_t c = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint64_t a = (an >> (A * j)) & ((1u << A) - 1u);
+            const uint64_t r = (rs >> (R * j)) & ((1u << R) - 1u);
+            c |= ((a << R) | r) << (8 * j);
+        }
+        *reinterpret_cast<uint2 *>(codes + 8 * i) = make_uint2((uint32_t)c, (uint32_t)(c >> 32));
+    }
+}
+
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (u >> 16) | 0x40u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Anchor phase for other split widths: K and V of one sequence from the A-bit
+// anchors as BF16 [T][Hkv][128]; the anchor stands for code
+// 2^R a + (2^R - 1) / 2, x = fmaf(code, scale, zero) rounded to BF16.
+// Thread per (token, head, 8 dims), grid-stride.
+template <int A, int LAYOUT>
+__global__ __launch_bounds__(kMergeThreads) void dequant_anchor_split_kernel(
+    Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
+    const uint8_t *__restrict__ k_anc, const uint8_t *__restrict__ v_anc, MetaPtrs meta,
+    uint16_t *__restrict__ k_out, uint16_t *__restrict__ v_out) {
+    constexpr int R = 8 - A;
+    constexpr float kHalf = (float)((1 << R) - 1) / 2.0f;
+    const int Hkv = geo.Hkv;
+    const size_t per = (size_t)T * Hkv * 16;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
+    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * per; e += stride) {
+        const int which = e >= per ? 1 : 0;
+        const size_t r = e - (size_t)which * per;
+        const int m = (int)(r & 15);
+        const size_t th = r >> 4;
+        const int h = (int)(th % Hkv);
+        const int t = (int)(th / Hkv);
+        int blk, tb;
+        if (LAYOUT == 0) {
+            blk = bt_row[0];
+            tb = t;
+        } else {
+            const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
+            blk = bt_row[bi];
+            tb = t - bi * geo.bt;
+        }
+        if (blk < 0 || blk >= geo.num_blocks) continue;
+        const size_t row = ((size_t)blk * Hkv + h) * geo.bt + tb;
+        const uint16_t *ap = reinterpret_cast<const uint16_t *>((which == 0 ? k_anc : v_anc) + row * (16 * A) + A * m);
+        uint64_t an = 0;
+#pragma unroll
+        for (int k = 0; k < A / 2; ++k) an |= (uint64_t)ap[k] << (16 * k);
+        float sc[8], zr[8];
+        if (which == 0) {
+            const size_t km = (((size_t)b * Hkv + h) * geo.n_groups + t / kKGroup) * kHeadDim + 8 * m;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                sc[j] = meta.k_scale[km + j];
+                zr[j] = meta.k_zero[km + j];
+            }
+        } else {
+            const size_t vm = ((size_t)b * Hkv + h) * geo.max_tokens + t;
+            const float s0 = meta.v_scale[vm], z0 = meta.v_zero[vm];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                sc[j] = s0;
+                zr[j] = z0;
+            }
+        }
+        uint32_t o[4];
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) {
+            const float q0 = (float)(((an >> (A * j)) & ((1u << A) - 1u)) << R) + kHalf;
+            const float q1 = (float)(((an >> (A * (j + 1))) & ((1u << A) - 1u)) << R) + kHalf;
+            o[j / 2] = f32_to_bf16_bits(fmaf(q0, sc[j], zr[j])) | (f32_to_bf16_bits(fmaf(q1, sc[j + 1], zr[j + 1])) << 16);
+        }
+        uint16_t *out = which == 0 ? k_out : v_out;
+        *reinterpret_cast<uint4 *>(out + ((size_t)t * Hkv + h) * kHeadDim + 8 * m) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_merge_split(int anchor_bits, const uint8_t *anc, const uint8_t *res, uint8_t *codes,
+                              size_t n_rows, hipStream_t stream) {
+    if (n_rows == 0) return hipSuccess;
+    const size_t n_pieces = n_rows * 16;
+    size_t blocks = (n_pieces + kMergeThreads - 1) / kMergeThreads;
+    if (blocks > 256 * 32) blocks = 256 * 32;
+    if (anchor_bits == 2)
+        hipLaunchKernelGGL(merge_split_kernel<2>, dim3((unsigned)blocks), dim3(kMergeThreads), 0, stream, anc, res,
+                           codes, n_pieces);
+    else if (anchor_bits == 4)
+        hipLaunchKernelGGL(merge_split_kernel<4>, dim3((unsigned)blocks), dim3(kMergeThreads), 0, stream, anc, res,
+                           codes, n_pieces);
+    else if (anchor_bits == 6)
+        hipLaunchKernelGGL(merge_split_kernel<6>, dim3((unsigned)blocks), dim3(kMergeThreads), 0, stream, anc, res,
+                           codes, n_pieces);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+template <int A>
+static void launch_dequant_split_width(const Geometry &g, int b, int T, int sh, const int32_t *block_table,
+                                       const uint8_t *k_anc, const uint8_t *v_anc, MetaPtrs meta,
+                                       uint16_t *k_out, uint16_t *v_out, dim3 grid, hipStream_t stream) {
+    if (g.max_blocks == 1)
+        hipLaunchKernelGGL((dequant_anchor_split_kernel<A, 0>), grid, dim3(kMergeThreads), 0, stream, g, b, T, sh,
+                           block_table, k_anc, v_anc, meta, k_out, v_out);
+    else
+        hipLaunchKernelGGL((dequant_anchor_split_kernel<A, 1>), grid, dim3(kMergeThreads), 0, stream, g, b, T, sh,
+                           block_table, k_anc, v_anc, meta, k_out, v_out);
+}
+
+hipError_t launch_dequant_anchor_split(int anchor_bits, const Geometry &g, int b, int T,
+                                       const int32_t *block_table, const uint8_t *k_anc,
+                                       const uint8_t *v_anc, MetaPtrs meta, uint16_t *k_out,
+                                       uint16_t *v_out, hipStream_t stream) {
+    if (T <= 0) return hipSuccess;
+    size_t blocks = ((size_t)2 * T * g.Hkv * 16 + kMergeThreads - 1) / kMergeThreads;
+    if (blocks > 256 * 32) blocks = 256 * 32;
+    const dim3 grid((unsigned)blocks);
+    int sh = -1;
+    for (int k = 0; k < 31; ++k)
+        if ((1 << k) == g.bt) sh = k;
+    if (anchor_bits == 2)
+        launch_dequant_split_width<2>(g, b, T, sh, block_table, k_anc, v_anc, meta, k_out, v_out, grid, stream);
+    else if (anchor_bits == 4)
+        launch_dequant_split_width<4>(g, b, T, sh, block_table, k_anc, v_anc, meta, k_out, v_out, grid, stream);
+    else if (anchor_bits == 6)
+        launch_dequant_split_width<6>(g, b, T, sh, block_table, k_anc, v_anc, meta, k_out, v_out, grid, stream);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

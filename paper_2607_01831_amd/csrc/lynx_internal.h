@@ -32,8 +32,16 @@ struct MetaPtrs {
 // ---- encode / merge (codec.hip) ---------------------------------------------
 hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_table,
                          const uint16_t *k, const uint16_t *v, uint8_t *k_anc, uint8_t *v_anc,
-                         uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream);
-
+                         uint8_t *k_res, uint8_t *v_res, MetaPtrs meta, hipStream_t stream,
+                         int anchor_bits = 4);
+// Split widths other than 4 + 4: rows of 16 A-bit anchors per 16 A bytes
+// (little-endian bit strings) and 16 (8 - A) residual bytes.
+hipError_t launch_merge_split(int anchor_bits, const uint8_t *anc, const uint8_t *res, uint8_t *codes,
+                              size_t n_rows, hipStream_t stream);
+hipError_t launch_dequant_anchor_split(int anchor_bits, const Geometry &g, int b, int T,
+                                       const int32_t *block_table, const uint8_t *k_anc,
+                                       const uint8_t *v_anc, MetaPtrs meta, uint16_t *k_out,
+                                       uint16_t *v_out, hipStream_t stream);
 hipError_t launch_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t n_packed,
                         hipStream_t stream);
 

@@ -79,6 +79,9 @@ def load():
                              ctypes.POINTER(lynx_hmeta), P], ctypes.c_int),
         "lynx_hkv_dequant": ([LP, I32, I32, P, I32, P, P, ctypes.c_float, I32,
                               ctypes.POINTER(lynx_hmeta), P, P, P], ctypes.c_int),
+        "lynx_kv_encode_split": ([LP, I32, I32, I32, P, P, P, P, P, P, P, MP, P], ctypes.c_int),
+        "lynx_kv_merge_split": ([I32, SZ, P, P, P, P], ctypes.c_int),
+        "lynx_kv_dequant_anchor_split": ([LP, I32, I32, I32, P, P, P, MP, P, P, P], ctypes.c_int),
         "lynx_strerror": ([ctypes.c_int], ctypes.c_char_p),
     }
     for name, (args, res) in sigs.items():
@@ -291,6 +294,32 @@ class HMeta:
 
     def c(self) -> lynx_hmeta:
         return lynx_hmeta(*(_ptr(getattr(self, f)) for f, _ in lynx_hmeta._fields_))
+
+
+def lynx_kv_encode_split(L: Layout, anchor_bits: int, b: int, T: int, block_table, k, v, k_anc, v_anc,
+                         k_res, v_res, meta: Meta, stream=None) -> None:
+    """k, v: BF16 [T][Hkv][128]; planes: uint8 device tensors of rows of
+    16 anchor_bits (anchor) and 16 (8 - anchor_bits) (residual) bytes."""
+    lay, met = L.c(), meta.c()
+    _check("lynx_kv_encode_split", load().lynx_kv_encode_split(
+        ctypes.byref(lay), anchor_bits, b, T, _ptr(block_table), _ptr(k), _ptr(v), _ptr(k_anc),
+        _ptr(v_anc), _ptr(k_res), _ptr(v_res), ctypes.byref(met), _stream(stream)))
+
+
+def lynx_kv_merge_split(anchor_bits: int, anc, res, codes, stream=None) -> None:
+    """Rows of A-bit anchors and (8 - A)-bit residuals -> rows of 128 codes."""
+    n_rows = anc.numel() // (16 * anchor_bits)
+    _check("lynx_kv_merge_split", load().lynx_kv_merge_split(
+        anchor_bits, n_rows, _ptr(anc), _ptr(res), _ptr(codes), _stream(stream)))
+
+
+def lynx_kv_dequant_anchor_split(L: Layout, anchor_bits: int, b: int, T: int, block_table, k_anc, v_anc,
+                                 meta: Meta, k_out, v_out, stream=None) -> None:
+    """k_out, v_out: BF16 [T][Hkv][128] (device, written)."""
+    lay, met = L.c(), meta.c()
+    _check("lynx_kv_dequant_anchor_split", load().lynx_kv_dequant_anchor_split(
+        ctypes.byref(lay), anchor_bits, b, T, _ptr(block_table), _ptr(k_anc), _ptr(v_anc),
+        ctypes.byref(met), _ptr(k_out), _ptr(v_out), _stream(stream)))
 
 
 # codec variants of the hierarchical codec (lynx.h LYNX_HQ_*)

@@ -191,6 +191,33 @@ def test_serdes_sizes_and_validation(lib):
                                             None) == E.LYNX_EINVAL
 
 
+def test_split_width_validation(lib):
+    """The split-width calls reject bad widths, sizes and overlaps before
+    launching anything."""
+    from paper_2607_01831_amd import lynx
+    E = lynx
+    L = _layout(max_blocks_per_seq=16, num_blocks=64, max_tokens=256)
+    lay = L.c()
+    m = lynx.lynx_meta(16, 32, 48, 64)
+    enc = lambda A=2, T=10, planes=(16, 16, 16, 16): lib.lynx_kv_encode_split(
+        ctypes.byref(lay), A, 0, T, 16, 16, 16, *planes, ctypes.byref(m), None)
+    assert enc(A=3) == E.LYNX_EINVAL
+    assert enc(A=8) == E.LYNX_EINVAL
+    assert enc(T=257) == E.LYNX_EINVAL
+    assert enc(planes=(16, 16, 24, 16)) == E.LYNX_EINVAL
+    assert enc(T=0) == E.LYNX_OK
+    assert lib.lynx_kv_merge_split(5, 10, 16, 4096, 8192, None) == E.LYNX_EINVAL
+    assert lib.lynx_kv_merge_split(2, 0, None, None, None, None) == E.LYNX_OK
+    assert lib.lynx_kv_merge_split(2, 10, 16, 4096, 24, None) == E.LYNX_EINVAL    # misaligned
+    # codes over the anchor rows (10 rows: anchors 320 bytes, codes 1280)
+    assert lib.lynx_kv_merge_split(2, 10, 1024, 8192, 512, None) == E.LYNX_EINVAL
+    deq = lambda A=6, T=10: lib.lynx_kv_dequant_anchor_split(
+        ctypes.byref(lay), A, 0, T, 16, 16, 16, ctypes.byref(m), 16, 16, None)
+    assert deq(A=1) == E.LYNX_EINVAL
+    assert deq(T=-1) == E.LYNX_EINVAL
+    assert deq(T=0) == E.LYNX_OK
+
+
 def test_hierarchical_codec_validation(lib):
     """The hierarchical encode / dequant reject bad arguments before
     launching anything (no pointer below is dereferenced)."""
