@@ -90,6 +90,8 @@ def parse():
                    help="timed paged batch-decode calls (paged-b16-16k-64k; 0 skips the stage)")
     p.add_argument("--no-hier", dest="hier", action="store_false",
                    help="skip the hierarchical-codec stage")
+    p.add_argument("--no-split-widths", dest="split_widths", action="store_false",
+                   help="skip the 2 + 6 / 6 + 2 split stage")
     p.add_argument("--no-serdes", dest="serdes", action="store_false",
                    help="skip the serializer / deserializer pipeline stage")
     p.add_argument("--no-overlap-70b", dest="overlap_70b", action="store_false",
@@ -727,6 +729,62 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
     return {"hier_codec": r}
 
 
+def split_widths_stage(dev, T, Hkv, K, V, n_layers):
+    """The 2 + 6 and 6 + 2 splits on the workload's layers: encode of every
+    layer into its own planes (so the merge below reads cold planes), merge of
+    the whole cache (one call per plane kind) and the anchor phase's BF16
+    pages (layers in turn), HIP events; bytes as for the 4 + 4 codec, with
+    A / 8 and (8 - A) / 8 bytes per element for the two planes."""
+    import torch
+
+    from paper_2607_01831_amd import lynx
+
+    table = torch.zeros(1, 1, dtype=torch.int32, device=dev)
+    L = lynx.contiguous_layout(Hkv, 1, T)
+    rows = T * Hkv
+    elems = rows * 128 * 2
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    r = {}
+    for A in (2, 6):
+        R = 8 - A
+        anc = torch.empty(2, n_layers, rows * 16 * A, dtype=torch.uint8, device=dev)
+        res = torch.empty(2, n_layers, rows * 16 * R, dtype=torch.uint8, device=dev)
+        codes = torch.empty(2, n_layers, rows * 128, dtype=torch.uint8, device=dev)
+        metas = [lynx.Meta.empty(L, 1, device=dev) for _ in range(n_layers)]
+        ko = torch.empty(T, Hkv, 128, dtype=torch.bfloat16, device=dev)
+        vo = torch.empty_like(ko)
+
+        def enc():
+            for l in range(n_layers):
+                lynx.lynx_kv_encode_split(L, A, 0, T, table, K[l], V[l], anc[0, l], anc[1, l], res[0, l],
+                                          res[1, l], metas[l])
+
+        def merge():
+            for w in range(2):
+                lynx.lynx_kv_merge_split(A, anc[w], res[w], codes[w])
+
+        def deq():
+            for l in range(n_layers):
+                lynx.lynx_kv_dequant_anchor_split(L, A, 0, T, table, anc[0, l], anc[1, l], metas[l], ko, vo)
+
+        out = {}
+        for name, fn, per_elem in (("encode", enc, 2 + 1 + 0.0625), ("merge", merge, 2.0),
+                                   ("dequant_anchor", deq, A / 8 + 2 + 0.0625)):
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = ev(), ev()
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / n_layers
+            out[f"{name}_us_per_layer"] = round(us, 2)
+            out[f"{name}_GBps"] = round(elems * per_elem / (us * 1e-6) / 1e9, 1)
+        r[f"split_{A}_{R}"] = out
+        del anc, res, codes, metas
+    return {"split_widths": r}
+
+
 def cpu_baseline(w, layer_inputs, n_layers):
     """The CPU oracle, untuned, timed on this host on a bounded sample: the
     anchor decode of the first n_layers layers (all kv heads)."""
@@ -889,6 +947,7 @@ def main():
     ovl = overlap_70b_stage(dev) if args.overlap_70b else None
     serdes = serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side) if args.serdes else None
     hier = hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers) if args.hier else None
+    split = split_widths_stage(dev, T, Hkv, K, V, n_layers) if args.split_widths else None
 
     # The speculative decoder's own pieces, timed alone: decode over the
     # anchors plus the 8 BF16 tokens it generated (32 layers), and greedy
@@ -995,6 +1054,7 @@ def main():
             **(ovl or {}),
             **(serdes or {}),
             **(hier or {}),
+            **(split or {}),
             **spec,
             "decode_hidden_behind_h2d": round(overlap, 3),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
