@@ -176,6 +176,8 @@ def lynx_kv_encode(L: Layout, b: int, T: int, block_table, k, v, k_anc, v_anc, k
 
 def lynx_kv_merge(anc, res, codes, n_packed_bytes: int | None = None, stream=None) -> None:
     n = anc.numel() if n_packed_bytes is None else n_packed_bytes
+    if n > anc.numel() or n > res.numel() or 2 * n > codes.numel():
+        raise ValueError("lynx_kv_merge: the planes hold fewer bytes than asked for")
     _check("lynx_kv_merge", load().lynx_kv_merge(_ptr(anc), _ptr(res), _ptr(codes), n,
                                                  _stream(stream)))
 
@@ -309,6 +311,9 @@ def lynx_kv_encode_split(L: Layout, anchor_bits: int, b: int, T: int, block_tabl
 def lynx_kv_merge_split(anchor_bits: int, anc, res, codes, stream=None) -> None:
     """Rows of A-bit anchors and (8 - A)-bit residuals -> rows of 128 codes."""
     n_rows = anc.numel() // (16 * anchor_bits)
+    if (anc.numel() != n_rows * 16 * anchor_bits or res.numel() != n_rows * 16 * (8 - anchor_bits)
+            or codes.numel() < n_rows * 128):
+        raise ValueError("lynx_kv_merge_split: plane sizes do not match one another")
     _check("lynx_kv_merge_split", load().lynx_kv_merge_split(
         anchor_bits, n_rows, _ptr(anc), _ptr(res), _ptr(codes), _stream(stream)))
 
