@@ -618,7 +618,9 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
 // Anchor phase for other split widths: K and V of one sequence from the A-bit
 // anchors as BF16 [T][Hkv][128]; the anchor stands for code
 // 2^R a + (2^R - 1) / 2, x = fmaf(code, scale, zero) rounded to BF16.
-// Thread per (token, head, 8 dims), grid-stride.
+// Thread per (8 tokens, head, 8 dims), the dims fastest: the K scales and
+// zeros of its dims are loaded once for its 8 tokens (which share a K
+// group), grid-stride.
 template <int A, int LAYOUT>
 __global__ __launch_bounds__(kMergeThreads) void dequant_anchor_split_kernel(
     Geometry geo, int b, int T, int bt_shift, const int32_t *__restrict__ block_table,
@@ -627,57 +629,75 @@ __global__ __launch_bounds__(kMergeThreads) void dequant_anchor_split_kernel(
     constexpr int R = 8 - A;
     constexpr float kHalf = (float)((1 << R) - 1) / 2.0f;
     const int Hkv = geo.Hkv;
-    const size_t per = (size_t)T * Hkv * 16;
+    const int n_oct = (T + 7) / 8;
+    const size_t per = (size_t)n_oct * Hkv * 16;
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     const int32_t *bt_row = block_table + (size_t)b * geo.max_blocks;
     for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * per; e += stride) {
         const int which = e >= per ? 1 : 0;
         const size_t r = e - (size_t)which * per;
         const int m = (int)(r & 15);
-        const size_t th = r >> 4;
-        const int h = (int)(th % Hkv);
-        const int t = (int)(th / Hkv);
-        int blk, tb;
-        if (LAYOUT == 0) {
-            blk = bt_row[0];
-            tb = t;
-        } else {
-            const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
-            blk = bt_row[bi];
-            tb = t - bi * geo.bt;
-        }
-        if (blk < 0 || blk >= geo.num_blocks) continue;
-        const size_t row = ((size_t)blk * Hkv + h) * geo.bt + tb;
-        const uint16_t *ap = reinterpret_cast<const uint16_t *>((which == 0 ? k_anc : v_anc) + row * (16 * A) + A * m);
-        uint64_t an = 0;
-#pragma unroll
-        for (int k = 0; k < A / 2; ++k) an |= (uint64_t)ap[k] << (16 * k);
+        const size_t oh = r >> 4;
+        const int h = (int)(oh % Hkv);
+        const int t0 = 8 * (int)(oh / Hkv);
         float sc[8], zr[8];
         if (which == 0) {
-            const size_t km = (((size_t)b * Hkv + h) * geo.n_groups + t / kKGroup) * kHeadDim + 8 * m;
+            const size_t km = (((size_t)b * Hkv + h) * geo.n_groups + t0 / kKGroup) * kHeadDim + 8 * m;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 sc[j] = meta.k_scale[km + j];
                 zr[j] = meta.k_zero[km + j];
             }
-        } else {
-            const size_t vm = ((size_t)b * Hkv + h) * geo.max_tokens + t;
-            const float s0 = meta.v_scale[vm], z0 = meta.v_zero[vm];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                sc[j] = s0;
-                zr[j] = z0;
-            }
         }
-        uint32_t o[4];
-#pragma unroll
-        for (int j = 0; j < 8; j += 2) {
-            const float q0 = (float)(((an >> (A * j)) & ((1u << A) - 1u)) << R) + kHalf;
-            const float q1 = (float)(((an >> (A * (j + 1))) & ((1u << A) - 1u)) << R) + kHalf;
-            o[j / 2] = f32_to_bf16_bits(fmaf(q0, sc[j], zr[j])) | (f32_to_bf16_bits(fmaf(q1, sc[j + 1], zr[j + 1])) << 16);
-        }
+        const uint8_t *plane = which == 0 ? k_anc : v_anc;
         uint16_t *out = which == 0 ? k_out : v_out;
-        *reinterpret_cast<uint4 *>(out + ((size_t)t * Hkv + h) * kHeadDim + 8 * m) = make_uint4(o[0], o[1], o[2], o[3]);
+        const int nt = min(8, T - t0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            if (k >= nt) break;
+            const int t = t0 + k;
+            int blk, tb;
+            if (LAYOUT == 0) {
+                blk = bt_row[0];
+                tb = t;
+            } else {
+                const int bi = bt_shift >= 0 ? (t >> bt_shift) : t / geo.bt;
+                blk = bt_row[bi];
+                tb = t - bi * geo.bt;
+            }
+            if (blk < 0 || blk >= geo.num_blocks) continue;
+            const size_t row = ((size_t)blk * Hkv + h) * geo.bt + tb;
+            const uint16_t *ap = reinterpret_cast<const uint16_t *>(plane + row * (16 * A) + A * m);
+            uint64_t an = 0;
+#pragma unroll
+            for (int i = 0; i < A / 2; ++i) an |= (uint64_t)ap[i] << (16 * i);
+            float s1[8], z1[8];
+            if (which == 0) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    s1[j] = sc[j];
+                    z1[j] = zr[j];
+                }
+            } else {
+                const size_t vm = ((size_t)b * Hkv + h) * geo.max_tokens + t;
+                const float s0 = meta.v_scale[vm], z0 = meta.v_zero[vm];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    s1[j] = s0;
+                    z1[j] = z0;
+                }
+            }
+            uint32_t o[4];
+#pragma unroll
+            for (int j = 0; j < 8; j += 2) {
+                const float q0 = (float)(((an >> (A * j)) & ((1u << A) - 1u)) << R) + kHalf;
+                const float q1 = (float)(((an >> (A * (j + 1))) & ((1u << A) - 1u)) << R) + kHalf;
+                o[j / 2] = f32_to_bf16_bits(fmaf(q0, s1[j], z1[j])) |
+                           (f32_to_bf16_bits(fmaf(q1, s1[j + 1], z1[j + 1])) << 16);
+            }
+            *reinterpret_cast<uint4 *>(out + ((size_t)t * Hkv + h) * kHeadDim + 8 * m) =
+                make_uint4(o[0], o[1], o[2], o[3]);
+        }
     }
 }
 
@@ -720,7 +740,7 @@ hipError_t launch_dequant_anchor_split(int anchor_bits, const Geometry &g, int b
                                        const uint8_t *v_anc, MetaPtrs meta, uint16_t *k_out,
                                        uint16_t *v_out, hipStream_t stream) {
     if (T <= 0) return hipSuccess;
-    size_t blocks = ((size_t)2 * T * g.Hkv * 16 + kMergeThreads - 1) / kMergeThreads;
+    size_t blocks = ((size_t)2 * ((T + 7) / 8) * g.Hkv * 16 + kMergeThreads - 1) / kMergeThreads;
     if (blocks > 256 * 32) blocks = 256 * 32;
     const dim3 grid((unsigned)blocks);
     int sh = -1;
