@@ -345,7 +345,7 @@ int lynx_kv_deserialize_residual(const lynx_layout *L, int32_t b, int32_t t0, in
 
 /*
  * Split widths other than 4 + 4 (the paper leaves them to future work,
- * Sec. 7): the same 8-bit codes as lynx_kv_encode, split into an anchor of
+ * Sec. 8): the same 8-bit codes as lynx_kv_encode, split into an anchor of
  * A = anchor_bits bits (code >> (8 - A)) and a residual of R = 8 - A bits
  * (code & (2^R - 1)), A in {2, 4, 6}.  A plane row (one token of one kv
  * head) holds the 128 fields as a little-endian bit string: element e at

@@ -523,7 +523,7 @@ def hdequant(mode: str, L: Layout, b: int, T: int, block_table: np.ndarray,
 
 
 # --------------------------------------------------------------------------
-# Split widths other than 4 + 4 (Sec. 7): an A-bit anchor c >> (8 - A) and an
+# Split widths other than 4 + 4 (Sec. 8): an A-bit anchor c >> (8 - A) and an
 # (8 - A)-bit residual, rows of 128 elements as little-endian bit strings
 # (16 W bytes a row); the readings are stated in lynx_oracle.c.
 # --------------------------------------------------------------------------

@@ -877,7 +877,7 @@ int oracle_accept_sample(int B, int k, int V, const float *p, const float *q,
 }
 
 /* ------------------------------------------------------------------------ */
-/* Split widths other than 4 + 4 (the paper's future work, Sec. 7)           */
+/* Split widths other than 4 + 4 (the paper's future work, Sec. 8)           */
 /* ------------------------------------------------------------------------ */
 /*
  * The uniform codec's 8-bit code c split into an anchor of A bits, c >> R,

@@ -1,6 +1,6 @@
 """Pins for the oracle's split widths other than 4 + 4 (an A-bit anchor and an
 (8 - A)-bit residual of the uniform 8-bit code, A in {2, 4, 6}; the paper
-leaves other widths to future work, Sec. 7), CPU only.  What the pins rest on,
+leaves other widths to future work, Sec. 8), CPU only.  What the pins rest on,
 other than the oracle itself:
 
   - the codes do not depend on the split: merging the A / (8 - A) planes gives
