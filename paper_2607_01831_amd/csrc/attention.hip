@@ -1,25 +1,10 @@
-// Attention over the split-stream KV cache for gfx950: anchor-only decode
-// (Sec. 4.2 Anchor phase) and the verification pass over the merged 8-bit
-// cache with a causal BF16 draft tail (Sec. 4.3).  Both compute
-// O = softmax(q K^T / sqrt(128)) V (Sec. 2) with K and V reconstructed in
-// registers from the packed cache.
-//
-// Split-context ("flash-decoding") structure: grid = (context split, kv head
-// x row chunk, sequence).  A workgroup holds up to R query rows that share one
-// kv head (the G query heads of a GQA group, times the draft queries in
-// verification), walks its split's tokens with four wavefronts, keeps an
-// online softmax per row, reduces the four wavefronts through LDS and writes
-// one partial (max, sum, unnormalised output) per row.  A combine kernel
-// merges the partials of all splits.
-//
-// Dequantization is folded into the operands instead of being applied per
-// element.  With a K group's per-channel scale s_d and zero z_d,
-//   q . k_hat = sum_d (c q_d s_d) a_d + sum_d q_d (z_d + o s_d)
-// (anchor: c = 16, o = 7.5; codes: c = 1, o = 0), so one fold per 128-token
-// group turns the score into a dot product with the raw 4- or 8-bit integers.
-// With V's per-token scale s_t and zero z_t,
-//   sum_t p_t v_hat_t = sum_t (c p_t s_t) a_t + [sum_t p_t (z_t + o s_t)] 1,
-// the bracket being one scalar per row.
+// Attention over the split-stream KV cache for gfx950: planning and launch of
+// the anchor-only decode (Sec. 4.2 Anchor phase; anchor_decode.hip) and of
+// the verification pass over the merged 8-bit cache (Sec. 4.3; verify.hip),
+// both O = softmax(q K^T / sqrt(128)) V (Sec. 2) split along the context,
+// and the combine kernel that merges their per-split partials (max, sum,
+// unnormalised output) and attends the BF16 tail: the drafts, causal among
+// themselves, in verification, and the generated tokens in decode.
 #include "lynx_internal.h"
 
 #include <float.h>
@@ -28,8 +13,7 @@
 namespace lynx {
 namespace {
 
-constexpr int kAttnThreads = 256;
-constexpr int kWaves = kAttnThreads / 64;
+constexpr int kWaves = 4;  // wavefronts per decode / verification workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -64,321 +48,12 @@ __device__ __forceinline__ void unpack8_bf16(const uint4 &u, float *x) {
 }
 
 // Eight 4-bit values (nibble j = element j) -> floats.
-__device__ __forceinline__ void unpack8_nibbles(uint32_t w, float *x) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] = (float)((w >> (4 * j)) & 15u);
-}
-
 // Eight bytes -> floats.
-__device__ __forceinline__ void unpack8_bytes(uint2 w, float *x) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        x[j] = (float)((w.x >> (8 * j)) & 255u);
-        x[4 + j] = (float)((w.y >> (8 * j)) & 255u);
-    }
-}
-
-__device__ __forceinline__ float sum16(float v) {
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 4);
-    v += __shfl_xor(v, 8);
-    return v;
-}
-
-__device__ __forceinline__ float sum_tq(float v) {  // over lanes m, m+16, m+32, m+48
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
-    return v;
-}
-
-__device__ __forceinline__ float max_tq(float v) {
-    v = fmaxf(v, __shfl_xor(v, 16));
-    v = fmaxf(v, __shfl_xor(v, 32));
-    return v;
-}
-
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
     if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN
     u += 0x7fffu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
-}
-
-// Lane layout inside a wavefront: lane = 16 * tq + m.  Lane (m, tq) owns dims
-// 8m..8m+7 of token slot tq; four tokens are in flight per wave step, each
-// read as 16 lanes x 4 bytes (nibbles) or 16 lanes x 8 bytes (codes) of one
-// contiguous token row.
-template <KvMode MODE, int R>
-__global__ __launch_bounds__(kAttnThreads) void attn_split_kernel(AttnArgs a) {
-    constexpr float kC = MODE == KvMode::kAnchor ? 16.0f : 1.0f;
-    constexpr float kO = MODE == KvMode::kAnchor ? 7.5f : 0.0f;
-    constexpr int kRowBytes = MODE == KvMode::kAnchor ? kNibbleRow : kCodeRow;
-
-    const int Hkv = a.geo.Hkv;
-    const int split = blockIdx.x + a.split_base;
-    const int h = blockIdx.y % Hkv;
-    const int chunk = blockIdx.y / Hkv;
-    const int b = blockIdx.z;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int w = tid >> 6;
-    const int m = lane & 15;
-    const int tq = lane >> 4;
-    const int T = min(a.seq_lens[b], a.max_seq_len);
-
-    __shared__ float s_o[kWaves][R][kHeadDim];
-    __shared__ float s_m[kWaves][R];
-    __shared__ float s_l[kWaves][R];
-
-    // ---- the chunk's query rows: row gr <-> (draft i = gr / G, head g = gr % G)
-    float q[R][8];
-    int row_i[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int gr = chunk * R + r;
-        row_i[r] = gr / a.G;
-        if (gr < a.rows_total) {
-            const size_t qo =
-                (((size_t)b * a.nq + row_i[r]) * a.Hq + (size_t)h * a.G + gr % a.G) * kHeadDim +
-                8 * m;
-            unpack8_bf16(*reinterpret_cast<const uint4 *>(a.q + qo), q[r]);
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) q[r][j] = 0.0f;
-            row_i[r] = -1;
-        }
-    }
-
-    float mrow[R], lrow[R], obias[R], acc[R][8];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        mrow[r] = -INFINITY;
-        lrow[r] = 0.0f;
-        obias[r] = 0.0f;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[r][j] = 0.0f;
-    }
-    bool bad = false;
-    const float sm = kLog2e * rsqrtf((float)kHeadDim);  // 1/sqrt(128) in log2 units
-    const int32_t *bt_row = a.block_table + (size_t)b * a.geo.max_blocks;
-
-    // Online-softmax update for one 16-token block whose scores s[it][r]
-    // belong to token slot tq of step it; returns p in s.
-    auto softmax_block = [&](float (&s)[4][R]) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            float bm = fmaxf(fmaxf(s[0][r], s[1][r]), fmaxf(s[2][r], s[3][r]));
-            bm = max_tq(bm);
-            const float mn = fmaxf(mrow[r], bm);
-            if (mn == -INFINITY) {
-#pragma unroll
-                for (int it = 0; it < 4; ++it) s[it][r] = 0.0f;
-                continue;
-            }
-            if (mn > mrow[r]) {
-                const float alpha = exp2f(mrow[r] - mn);
-                lrow[r] *= alpha;
-                obias[r] *= alpha;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) acc[r][j] *= alpha;
-                mrow[r] = mn;
-            }
-#pragma unroll
-            for (int it = 0; it < 4; ++it) {
-                s[it][r] = exp2f(s[it][r] - mn);
-                lrow[r] += s[it][r];
-            }
-        }
-    };
-
-    if (split < a.n_ctx_splits) {
-        // ---------------- context tokens from the packed cache ----------------
-        const int groups_per_split = a.split_tokens / kKGroup;
-        for (int gi = w; gi < groups_per_split; gi += kWaves) {
-            const int g = split * groups_per_split + gi;
-            const int tg0 = g * kKGroup;
-            if (tg0 >= T) break;
-            const int tg1 = min(T, tg0 + kKGroup);
-            // fold the group's K scale/zero into the query rows
-            const size_t km = (((size_t)b * Hkv + h) * a.geo.n_groups + g) * kHeadDim + 8 * m;
-            float ks[8], kz[8];
-            {
-                const float4 s0 = *reinterpret_cast<const float4 *>(a.meta.k_scale + km);
-                const float4 s1 = *reinterpret_cast<const float4 *>(a.meta.k_scale + km + 4);
-                const float4 z0 = *reinterpret_cast<const float4 *>(a.meta.k_zero + km);
-                const float4 z1 = *reinterpret_cast<const float4 *>(a.meta.k_zero + km + 4);
-                ks[0] = s0.x; ks[1] = s0.y; ks[2] = s0.z; ks[3] = s0.w;
-                ks[4] = s1.x; ks[5] = s1.y; ks[6] = s1.z; ks[7] = s1.w;
-                kz[0] = z0.x; kz[1] = z0.y; kz[2] = z0.z; kz[3] = z0.w;
-                kz[4] = z1.x; kz[5] = z1.y; kz[6] = z1.z; kz[7] = z1.w;
-            }
-            float qs[R][8], kb[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                float bsum = 0.0f;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    qs[r][j] = kC * q[r][j] * ks[j];
-                    bsum += q[r][j] * (kz[j] + kO * ks[j]);
-                }
-                kb[r] = sum16(bsum);
-            }
-            for (int t16 = tg0; t16 < tg1; t16 += 16) {
-                float s[4][R];
-                uint32_t vw[4][kRowBytes / 64];
-                float vsc[4], vzr[4];
-#pragma unroll
-                for (int it = 0; it < 4; ++it) {
-                    const int t = t16 + 4 * it + tq;
-                    float kv[8];
-                    bool ok = t < tg1;
-                    size_t row = 0;
-                    if (ok) {
-                        const int blk = bt_row[t / a.geo.bt];
-                        if (blk < 0 || blk >= a.geo.num_blocks) {
-                            bad = true;
-                            ok = false;
-                        } else {
-                            row = (((size_t)blk * Hkv + h) * a.geo.bt + (t % a.geo.bt)) *
-                                  kRowBytes;
-                        }
-                    }
-                    if (MODE == KvMode::kAnchor) {
-                        uint32_t kw = 0;
-                        vw[it][0] = 0;
-                        if (ok) {
-                            kw = *reinterpret_cast<const uint32_t *>(a.k_plane + row + 4 * m);
-                            vw[it][0] = *reinterpret_cast<const uint32_t *>(a.v_plane + row + 4 * m);
-                        }
-                        unpack8_nibbles(kw, kv);
-                    } else {
-                        uint2 kw = make_uint2(0, 0);
-                        vw[it][0] = 0;
-                        vw[it][1] = 0;
-                        if (ok) {
-                            kw = *reinterpret_cast<const uint2 *>(a.k_plane + row + 8 * m);
-                            const uint2 vv = *reinterpret_cast<const uint2 *>(a.v_plane + row + 8 * m);
-                            vw[it][0] = vv.x;
-                            vw[it][1] = vv.y;
-                        }
-                        unpack8_bytes(kw, kv);
-                    }
-                    vsc[it] = 0.0f;
-                    vzr[it] = 0.0f;
-                    if (ok) {
-                        const size_t vm = ((size_t)b * Hkv + h) * a.geo.max_tokens + t;
-                        vsc[it] = a.meta.v_scale[vm];
-                        vzr[it] = a.meta.v_zero[vm];
-                    }
-#pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        float d = 0.0f;
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) d += qs[r][j] * kv[j];
-                        d = sum16(d);
-                        s[it][r] = ok ? (d + kb[r]) * sm : -INFINITY;
-                    }
-                }
-                softmax_block(s);
-#pragma unroll
-                for (int it = 0; it < 4; ++it) {
-                    float vv[8];
-                    if (MODE == KvMode::kAnchor) {
-                        unpack8_nibbles(vw[it][0], vv);
-                    } else {
-                        unpack8_bytes(make_uint2(vw[it][0], vw[it][kRowBytes / 64 - 1]), vv);
-                    }
-#pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        const float p = s[it][r];
-                        const float pp = kC * p * vsc[it];
-                        obias[r] += p * (vzr[it] + kO * vsc[it]);
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) acc[r][j] += pp * vv[j];
-                    }
-                }
-            }
-        }
-    } else if (w == 0) {
-        // ---------------- BF16 draft tail, causal among drafts ----------------
-        for (int t16 = 0; t16 < a.nq; t16 += 16) {
-            float s[4][R];
-            float vt[4][8];
-#pragma unroll
-            for (int it = 0; it < 4; ++it) {
-                const int j = t16 + 4 * it + tq;
-                float kv[8];
-                if (j < a.nq) {
-                    const size_t o = (((size_t)b * a.nq + j) * Hkv + h) * kHeadDim + 8 * m;
-                    unpack8_bf16(*reinterpret_cast<const uint4 *>(a.k_new + o), kv);
-                    unpack8_bf16(*reinterpret_cast<const uint4 *>(a.v_new + o), vt[it]);
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) kv[e] = vt[it][e] = 0.0f;
-                }
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    float d = 0.0f;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) d += q[r][e] * kv[e];
-                    d = sum16(d);
-                    s[it][r] = (j < a.nq && j <= row_i[r]) ? d * sm : -INFINITY;
-                }
-            }
-            softmax_block(s);
-#pragma unroll
-            for (int it = 0; it < 4; ++it)
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) acc[r][e] += s[it][r] * vt[it][e];
-        }
-    }
-
-    // ---- reduce token slots, then wavefronts, then write the partials ----
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        lrow[r] = sum_tq(lrow[r]);
-        obias[r] = sum_tq(obias[r]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[r][j] = sum_tq(acc[r][j]);
-        if (tq == 0) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) s_o[w][r][8 * m + j] = acc[r][j] + obias[r];
-        }
-        if (lane == 0) {
-            s_m[w][r] = mrow[r];
-            s_l[w][r] = lrow[r];
-        }
-    }
-    const bool any_bad = __syncthreads_or(bad);
-    for (int idx = tid; idx < R * kHeadDim; idx += kAttnThreads) {
-        const int r = idx / kHeadDim;
-        const int d = idx % kHeadDim;
-        const int gr = chunk * R + r;
-        if (gr >= a.rows_total) continue;
-        float M = -INFINITY;
-#pragma unroll
-        for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, s_m[ww][r]);
-        float O = 0.0f, Lsum = 0.0f;
-        if (M != -INFINITY) {
-#pragma unroll
-            for (int ww = 0; ww < kWaves; ++ww) {
-                if (s_m[ww][r] == -INFINITY) continue;
-                const float f = exp2f(s_m[ww][r] - M);
-                O += s_o[ww][r][d] * f;
-                Lsum += s_l[ww][r] * f;
-            }
-        }
-        if (any_bad) {
-            O = NAN;
-            Lsum = NAN;
-        }
-        const size_t pi = (((size_t)b * Hkv + h) * a.rows_total + gr) * a.n_splits + split;
-        a.ws_o[pi * kHeadDim + d] = O;
-        if (d == 0) a.ws_ml[pi] = make_float2(M, Lsum);
-    }
 }
 
 constexpr int kCombineThreads = 256;
@@ -559,27 +234,12 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     }
 }
 
-template <KvMode MODE>
-hipError_t launch_split(int R, dim3 grid, const AttnArgs &args, hipStream_t stream) {
-    switch (R) {
-    case 1: hipLaunchKernelGGL((attn_split_kernel<MODE, 1>), grid, dim3(kAttnThreads), 0, stream, args); break;
-    case 2: hipLaunchKernelGGL((attn_split_kernel<MODE, 2>), grid, dim3(kAttnThreads), 0, stream, args); break;
-    case 4: hipLaunchKernelGGL((attn_split_kernel<MODE, 4>), grid, dim3(kAttnThreads), 0, stream, args); break;
-    default: hipLaunchKernelGGL((attn_split_kernel<MODE, 8>), grid, dim3(kAttnThreads), 0, stream, args); break;
-    }
-    return hipGetLastError();
-}
-
 }  // namespace
 
 AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_len, bool tail) {
     AttnPlan p{};
     const int G = Hq / g.Hkv;
     p.rows_total = nq * G;
-    // smallest power of two >= min(rows_total, 8)
-    p.rows_chunk = 1;
-    while (p.rows_chunk < 8 && p.rows_chunk < p.rows_total) p.rows_chunk *= 2;
-    p.n_chunks = (p.rows_total + p.rows_chunk - 1) / p.rows_chunk;
     // Context tokens per split: 512, doubled while the launch still fills
     // the chip (>= 1024 decode workgroups, two per CU; >= 512 verification
     // workgroups, also two per CU), so long contexts write fewer partials
@@ -693,9 +353,7 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
         if (e != hipSuccess) return e;
         // the BF16 draft tail is attended by the combine kernel below
     } else {
-        dim3 grid(plan.n_splits, g.Hkv * plan.n_chunks, B);
-        hipError_t e = launch_split<KvMode::kAnchor>(plan.rows_chunk, grid, a, stream);
-        if (e != hipSuccess) return e;
+        return hipErrorInvalidValue;  // anchor attention with several queries: no entry point asks for it
     }
     hipLaunchKernelGGL(attn_combine_kernel, dim3(plan.rows_total, g.Hkv, B), dim3(kCombineThreads),
                        0, stream, a, out, lse);

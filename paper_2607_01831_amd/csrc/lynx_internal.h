@@ -99,8 +99,6 @@ enum class KvMode : int { kAnchor = 0, kCodes = 1 };
 
 struct AttnPlan {
     int rows_total;   // nq * G query rows per (sequence, kv head)
-    int rows_chunk;   // rows handled by one workgroup (1, 2, 4 or 8)
-    int n_chunks;     // ceil(rows_total / rows_chunk)
     int split_tokens; // context tokens per split
     int n_ctx_splits; // ceil(max_seq_len / split_tokens)
     int n_splits;     // n_ctx_splits (+1 when a BF16 draft tail is attended)
