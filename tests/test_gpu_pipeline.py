@@ -116,3 +116,69 @@ def test_split_stream_pipeline(paged):
         np.testing.assert_allclose(dec_lse[l].cpu().numpy(), ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
         vref, _ = oracle.verify(OL, Hq, np.array(lens), table.numpy(), kc, vc, meta, bits(qk), None, None)
         assert_close(ver_out[l].float().cpu().numpy(), vref, what=f"pipeline verify layer {l}")
+
+
+@pytest.mark.parametrize("variant", ["biased", "centred"])
+def test_hier_split_stream_pipeline(variant):
+    """The hierarchical codec of Alg. 1 on the same split-stream schedule: the
+    anchor-only BF16 reconstruction runs on the main stream while the
+    correction planes are copied from pinned host memory on a side stream;
+    the merge and the full reconstruction wait on the copy event.  Every
+    plane and output is checked bit for bit against the oracle."""
+    T, Hkv, bt, alpha = 1500, 2, 16, 20.0
+    vid = oracle.H_VARIANTS[variant]
+    k, v = random_kv(T, Hkv, seed=7500 + vid)
+    table, n_blocks = inputs.paged_block_table(torch.tensor([T]), bt, 17)
+    L = lynx.Layout(num_kv_heads=Hkv, block_tokens=bt, max_blocks_per_seq=table.shape[1],
+                    num_blocks=n_blocks, max_tokens=T)
+    OL = oracle.Layout(Hkv=Hkv, bt=bt, max_blocks=table.shape[1], max_tokens=T)
+    pool = lynx.KVPool.allocate(L, 1)
+    hm = lynx.HMeta.empty(L, 1)
+    tdev = table.cuda()
+    note(f"hier pipeline variant={variant} encode T={T}")
+    lynx.lynx_hkv_encode(L, 0, T, tdev, k.cuda(), v.cuda(), alpha, vid, pool.k_anc, pool.v_anc,
+                         pool.k_res, pool.v_res, hm)
+    torch.cuda.synchronize()
+    host = {}
+    for name in ("k_res", "v_res"):
+        host[name] = torch.empty(getattr(pool, name).numel(), dtype=torch.uint8, pin_memory=True)
+        host[name].copy_(getattr(pool, name))
+        getattr(pool, name).zero_()
+    pool.k_codes.fill_(0xA5)
+    pool.v_codes.fill_(0xA5)
+    outs = {m: (torch.empty(T, Hkv, 128, dtype=torch.bfloat16, device="cuda"),
+                torch.empty(T, Hkv, 128, dtype=torch.bfloat16, device="cuda")) for m in ("anchor", "full")}
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    arrived = torch.cuda.Event()
+    side.wait_stream(main)
+    torch.cuda.synchronize()
+
+    note(f"hier pipeline variant={variant} correction copies on the side stream, anchor dequant on main")
+    with torch.cuda.stream(side):
+        pool.k_res.copy_(host["k_res"], non_blocking=True)
+        pool.v_res.copy_(host["v_res"], non_blocking=True)
+        arrived.record(side)
+    lynx.lynx_hkv_dequant(L, 0, T, tdev, False, pool.k_anc, pool.v_anc, alpha, vid, hm, *outs["anchor"],
+                          stream=main)
+    main.wait_event(arrived)
+    pool.merge(stream=main)
+    lynx.lynx_hkv_dequant(L, 0, T, tdev, True, pool.k_codes, pool.v_codes, alpha, vid, hm, *outs["full"],
+                          stream=main)
+    torch.cuda.synchronize()
+
+    nbytes = oracle.plane_bytes(OL, n_blocks, 64)
+    planes = {name: np.zeros(nbytes, np.uint8) for name in ("k_anc", "v_anc", "k_res", "v_res")}
+    ohm = oracle.HMeta.empty(OL, 1)
+    oracle.hencode(OL, 0, T, table.numpy(), bits(k), bits(v), alpha, planes, ohm, variant)
+    codes = {p: oracle.merge(planes[p + "_anc"], planes[p + "_res"]) for p in ("k", "v")}
+    assert np.array_equal(pool.k_codes.cpu().numpy(), codes["k"]), "K codes differ"
+    assert np.array_equal(pool.v_codes.cpu().numpy(), codes["v"]), "V codes differ"
+    ref = {"anchor": oracle.hdequant("anchor", OL, 0, T, table.numpy(), planes["k_anc"], planes["v_anc"],
+                                     alpha, ohm, variant),
+           "full": oracle.hdequant("full", OL, 0, T, table.numpy(), codes["k"], codes["v"], alpha, ohm,
+                                   variant)}
+    for mode in ("anchor", "full"):
+        for i, name in enumerate(("K", "V")):
+            got, want = bits(outs[mode][i]), ref[mode][i]
+            assert np.array_equal(got, want), f"{mode} {name}: {np.count_nonzero(got != want)} values differ"
