@@ -129,9 +129,16 @@ int lynx_kv_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes,
  * its split-context partial results, for `num_queries` query tokens per
  * sequence (1 for anchor decode, k for verify) and sequences of at most
  * max_seq_len tokens.  Returns 0 on invalid arguments.
- * Calls that share a workspace must not run concurrently; its contents need
- * no initialisation.
+ * Layout: LYNX_ATTN_COUNTER_BYTES of uint32 arrival counters, then the
+ * partials.  The counters let the last workgroup of each (sequence, kv head)
+ * merge the split partials itself, so a decode call is one launch.
+ * Zero the first LYNX_ATTN_COUNTER_BYTES once, before the workspace's first
+ * use (e.g. hipMemsetAsync(workspace, 0, LYNX_ATTN_COUNTER_BYTES, stream));
+ * every call leaves them zero again, so calls of any shape can share one
+ * workspace afterwards.  The rest needs no initialisation.  Calls that share
+ * a workspace must not run concurrently.
  */
+#define LYNX_ATTN_COUNTER_BYTES 262144
 size_t lynx_attn_workspace_bytes(const lynx_layout *L, int32_t B, int32_t Hq,
                                  int32_t num_queries, int32_t max_seq_len);
 

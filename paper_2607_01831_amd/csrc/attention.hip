@@ -259,6 +259,8 @@ AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_le
     const size_t parts = (size_t)B * g.Hkv * p.rows_total * p.n_splits;
     p.o_bytes = parts * kHeadDim * sizeof(float);
     p.ml_bytes = parts * sizeof(float2);
+    p.row_chunks = (p.rows_total + 15) / 16;
+    p.counters_fit = (long long)B * g.Hkv * p.row_chunks <= kCounters;
     return p;
 }
 
@@ -296,8 +298,9 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
     a.q = q;
     a.k_new = k_new;
     a.v_new = v_new;
-    a.ws_o = reinterpret_cast<float *>(workspace);
-    a.ws_ml = reinterpret_cast<float2 *>(reinterpret_cast<char *>(workspace) + plan.o_bytes);
+    a.ws_o = reinterpret_cast<float *>(reinterpret_cast<char *>(workspace) + kCounterBytes);
+    a.ws_ml = reinterpret_cast<float2 *>(reinterpret_cast<char *>(workspace) + kCounterBytes +
+                                         plan.o_bytes);
     if (mode == KvMode::kAnchor && nq == 1) {
         // matrix-core decode over the anchor nibbles
         DecodeArgs d;
@@ -323,9 +326,20 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
         d.ws_ml = a.ws_ml;
         d.rows_total = plan.rows_total;
         d.ws_splits = plan.n_splits;
+        // without a tail the last workgroup of each (sequence, kv head, head
+        // chunk) merges the splits itself: no second launch
+        // (the merge holds up to two splits' (max, sum) per thread: 256 / GP
+        // threads per row, GP = 4, 8 or 16 rows padded)
+        const int gp = d.chunk_heads <= 4 ? 4 : d.chunk_heads <= 8 ? 8 : 16;
+        d.fused = (k_new == nullptr && plan.counters_fit && plan.n_ctx_splits <= 2 * (256 / gp)) ? 1 : 0;
+        d.row_chunks = plan.row_chunks;
+        d.counters = reinterpret_cast<unsigned *>(workspace);
+        d.out = out;
+        d.lse = lse;
         const int chunks = (a.G + d.chunk_heads - 1) / d.chunk_heads;
         hipError_t e = launch_anchor_decode_mfma(d, chunks, stream);
         if (e != hipSuccess) return e;
+        if (d.fused) return hipSuccess;
     } else if (mode == KvMode::kCodes) {
         // matrix-core verification over the context splits ...
         VerifyArgs v;

@@ -55,6 +55,29 @@ __device__ __forceinline__ float max_kg(float v) {
     return fmax2(__int_as_float(r[0]), __int_as_float(r[1]));
 }
 
+// ---- Buffer accesses with a cache policy ----
+// A buffer resource over [base, base + bytes): an access at an offset past the
+// end reads 0 and writes nothing.  `base` and `bytes` must be uniform.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, 0x00020000);
+}
+// Cache-policy bits of the buffer builtins: sc1 makes an access coherent
+// across the XCDs' L2 caches (agent scope): stores write through, loads do
+// not return another XCD's stale copy.
+constexpr int kAgentCoherent = 16;
+__device__ __forceinline__ void store16_agent(__amdgpu_buffer_rsrc_t r, uint32_t off, float4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, (int)off, 0, kAgentCoherent);
+}
+__device__ __forceinline__ void store8_agent(__amdgpu_buffer_rsrc_t r, uint32_t off, float2 v) {
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(intx2_t, v), r, (int)off, 0, kAgentCoherent);
+}
+__device__ __forceinline__ float4 load16_agent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kAgentCoherent));
+}
+__device__ __forceinline__ float2 load8_agent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, kAgentCoherent));
+}
+
 // ---- Global-to-LDS copies (global_load_lds), issued as inline assembly ----
 // The 16-byte copies carry the nontemporal hint: the attention kernels read
 // each K/V byte once (32K decode 16.9 -> 15.8-16.2 us, 128K verification

@@ -95,6 +95,14 @@ hipError_t launch_deserialize_residual(const Geometry &g, int b, int t0, int n,
                                        uint8_t *k_codes, uint8_t *v_codes, hipStream_t stream);
 
 // ---- attention (attention.hip) ----------------------------------------------
+// Arrival counters at the head of every attention workspace (the value of
+// lynx.h's LYNX_ATTN_COUNTER_BYTES): zero before a workspace's first use,
+// left zero by every call.
+// One counter per 256 bytes: arrivals on one cache line serialise (512
+// workgroups counting in on one line took 5 us, 64 per line 0.4 us).
+constexpr size_t kCounterBytes = 262144;
+constexpr int kCounterStride = 64;  // uint32 slots between counters
+constexpr int kCounters = (int)(kCounterBytes / (kCounterStride * sizeof(unsigned)));
 enum class KvMode : int { kAnchor = 0, kCodes = 1 };
 
 struct AttnPlan {
@@ -102,9 +110,14 @@ struct AttnPlan {
     int split_tokens; // context tokens per split
     int n_ctx_splits; // ceil(max_seq_len / split_tokens)
     int n_splits;     // n_ctx_splits (+1 when a BF16 draft tail is attended)
+    int row_chunks;   // ceil(rows_total / 16): arrival counters per (sequence, kv head)
+    bool counters_fit;  // B * Hkv * row_chunks <= kCounters
     size_t o_bytes;   // workspace bytes for the partial outputs
     size_t ml_bytes;  // workspace bytes for the partial (max, sum) pairs
-    size_t workspace_bytes() const { return o_bytes + ml_bytes; }  // [outputs][(max, sum)]
+    // [arrival counters, kCounterBytes][outputs][(max, sum)]: the counters sit
+    // at the same place for every call shape, so calls of different shapes
+    // can share a workspace without one's partials landing on the counters
+    size_t workspace_bytes() const { return kCounterBytes + o_bytes + ml_bytes; }
 };
 
 // Arguments of the matrix-core anchor decode kernel (anchor_decode.hip).
@@ -123,6 +136,14 @@ struct DecodeArgs {
     float *ws_o;    // split partials, same layout as the attention workspace
     float2 *ws_ml;
     int rows_total, ws_splits;
+    // Fused split merge: the last workgroup of a (sequence, kv head, head
+    // chunk) to finish merges its splits' partials and writes out / lse.
+    // Arrival counters uint32 [B][Hkv][row_chunks], zero on entry, left zero.
+    int fused;
+    int row_chunks;
+    unsigned *counters;
+    uint16_t *out;  // BF16 [B][Hq][128]
+    float *lse;     // fp32 [B][Hq] or nullptr
 };
 
 hipError_t launch_anchor_decode_mfma(const DecodeArgs &args, int chunks, hipStream_t stream);

@@ -189,11 +189,16 @@ def lynx_attn_workspace_bytes(L: Layout, B: int, Hq: int, num_queries: int,
                                                  max_seq_len))
 
 
+# Arrival counters at the head of every attention workspace (lynx.h).
+ATTN_COUNTER_BYTES = 262144
+
+
 def workspace(L: Layout, B: int, Hq: int, num_queries: int, max_seq_len: int,
               device="cuda") -> torch.Tensor:
-    """A device buffer of lynx_attn_workspace_bytes() bytes (allocated by torch)."""
+    """A device buffer of lynx_attn_workspace_bytes() bytes (allocated by
+    torch), zero-filled: the arrival counters at its head must start at zero."""
     n = lynx_attn_workspace_bytes(L, B, Hq, num_queries, max_seq_len)
-    return torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, ATTN_COUNTER_BYTES), dtype=torch.uint8, device=device)
 
 
 def lynx_attn_anchor_decode(L: Layout, B: int, Hq: int, max_seq_len: int, seq_lens,

@@ -301,8 +301,10 @@ def test_anchor_decode_ragged_batch_stale_workspace():
     B, Hq = len(lens), Hkv * G
     q = random_bf16((B, Hq, 128), seed=13)
     n = lynx.lynx_attn_workspace_bytes(c.L, B, Hq, 1, max(lens))
-    # filled with plausible-looking values (0x3F3F3F3F ~ 0.75)
+    # partials filled with plausible-looking values (0x3F3F3F3F ~ 0.75); the
+    # arrival counters at the head zeroed, as the header requires
     ws = torch.full((n,), 0x3F, dtype=torch.uint8, device="cuda")
+    ws[:lynx.ATTN_COUNTER_BYTES].zero_()
     out = torch.empty(B, Hq, 128, dtype=torch.bfloat16, device="cuda")
     lse = torch.empty(B, Hq, dtype=torch.float32, device="cuda")
     note(f"ragged stale workspace lens={lens}")
@@ -312,6 +314,47 @@ def test_anchor_decode_ragged_batch_stale_workspace():
     ref, ref_lse = oracle_decode(c, q)
     assert_close(out.float().cpu().numpy(), ref, what="ragged batch, stale workspace")
     np.testing.assert_allclose(lse.cpu().numpy(), ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
+
+
+def test_attention_calls_share_one_workspace():
+    """Decode calls of different batch shapes, a decode with a BF16 tail (the
+    combine kernel) and a verification pass take turns on one workspace: each
+    call leaves the arrival counters at its head zero for the next."""
+    Hkv, G = 4, 4
+    Hq = Hkv * G
+    lens = [3000, 700, 5000]
+    kv = [random_kv(T, Hkv, seed=900 + i) for i, T in enumerate(lens)]
+    c = build_cache([a for a, _ in kv], [b for _, b in kv], Hkv, merge=True)
+    B = len(lens)
+    nq = 3
+    ws = lynx.workspace(c.L, B, Hq, nq, max(lens))
+    q = random_bf16((B, Hq, 128), seed=21)
+    qv = random_bf16((B, nq, Hq, 128), seed=22)
+    kn = random_bf16((B, nq, Hkv, 128), seed=23)
+    vn = random_bf16((B, nq, Hkv, 128), seed=24)
+    ref, ref_lse = oracle_decode(c, q)
+    ref_v, _ = oracle_verify(c, qv, kn, vn)
+    for rep in range(3):
+        note(f"shared workspace rep {rep}")
+        out = torch.empty(B, Hq, 128, dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty(B, Hq, dtype=torch.float32, device="cuda")
+        lynx.lynx_attn_anchor_decode(c.L, B, Hq, max(lens), c.lens_dev(), c.table_dev(),
+                                     c.pool.k_anc, c.pool.v_anc, c.pool.meta, q.cuda(), out, lse, ws)
+        # the first sequence alone (a smaller batch over the same counters)
+        out1 = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device="cuda")
+        lynx.lynx_attn_anchor_decode(c.L, 1, Hq, lens[0], c.lens_dev()[:1], c.table_dev()[:1],
+                                     c.pool.k_anc, c.pool.v_anc, c.pool.meta, q[:1].cuda(), out1,
+                                     None, ws)
+        outv = torch.empty(B, nq, Hq, 128, dtype=torch.bfloat16, device="cuda")
+        lynx.lynx_attn_verify(c.L, B, Hq, nq, max(lens), c.lens_dev(), c.table_dev(),
+                              c.pool.k_codes, c.pool.v_codes, c.pool.meta, qv.cuda(), kn.cuda(),
+                              vn.cuda(), outv, ws)
+        torch.cuda.synchronize()
+        assert_close(out.float().cpu().numpy(), ref, what=f"decode rep {rep}")
+        np.testing.assert_allclose(lse.cpu().numpy(), ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
+        assert_close(out1.float().cpu().numpy(), ref[:1], what=f"decode b=0 rep {rep}")
+        assert_close(outv.float().cpu().numpy(), ref_v, what=f"verify rep {rep}")
+    assert int(ws[:lynx.ATTN_COUNTER_BYTES].count_nonzero().item()) == 0
 
 
 def _dominant(k, q, t, h, G, boost):
