@@ -168,6 +168,28 @@ int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t
                             size_t workspace_bytes, void *stream);
 
 /*
+ * lynx_attn_anchor_decode_noalloc -- lynx_attn_anchor_decode for callers that
+ * cannot allocate device memory or pass a workspace (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).  Same
+ * arguments and results, minus the workspace: the split partials and arrival
+ * counters live in a static array of LYNX_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends.  The call
+ * allocates nothing (no hipMalloc, no allocating library routine).
+ *   LYNX_EWORKSPACE  the call needs more than LYNX_NOALLOC_SCRATCH_BYTES
+ *                    (lynx_attn_workspace_bytes(L, B, Hq, 1, max_seq_len)
+ *                    bounds what it needs), checked before anything runs
+ *   LYNX_EHIP        the array's device address could not be obtained
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (other streams, other threads) race and give wrong results.
+ */
+#define LYNX_NOALLOC_SCRATCH_BYTES (16u << 20)
+int lynx_attn_anchor_decode_noalloc(const lynx_layout *L, int32_t B, int32_t Hq,
+                                    int32_t max_seq_len, const int32_t *seq_lens,
+                                    const int32_t *block_table, const uint8_t *k_anc,
+                                    const uint8_t *v_anc, const lynx_meta *meta,
+                                    const void *q_bf16, void *out_bf16, float *lse, void *stream);
+
+/*
  * lynx_attn_verify -- the verification pass (Sec. 4.3): the k speculative
  * query tokens of every sequence attend, in one parallel pass, over the
  * merged 8-bit cache (reconstructed as zero + code * scale) and over the

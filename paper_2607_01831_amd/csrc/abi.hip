@@ -4,6 +4,8 @@
 #include "../../include/lynx.h"
 #include "lynx_internal.h"
 
+#include <mutex>
+
 namespace {
 
 using lynx::Geometry;
@@ -202,6 +204,61 @@ int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t
         lynx::KvMode::kAnchor, g, p, B, Hq, 1, max_seq_len, seq_lens, block_table, k_anc, v_anc,
         mp, static_cast<const uint16_t *>(q_bf16), nullptr, nullptr, 0,
         static_cast<uint16_t *>(out_bf16), lse, workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
+}  // extern "C"
+
+// ---- scratch of lynx_attn_anchor_decode_noalloc ----
+// The split partials and arrival counters of a decode call live in this
+// file-scope device array instead of a caller workspace.  In host code its
+// name is only a stand-in: the device address comes from hipGetSymbolAddress,
+// once per device (each GPU holds its own copy).  It is zero when the library
+// is loaded, and every call leaves its counters zero again.
+namespace {
+constexpr size_t kScratchBytes = 16u << 20;  // the value of LYNX_NOALLOC_SCRATCH_BYTES
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+static_assert(kScratchBytes == LYNX_NOALLOC_SCRATCH_BYTES, "header and library disagree");
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void *g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// Device address of this device's scratch array (nullptr on failure).
+void *scratch_on_current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::call_once(g_scratch_once[dev], [dev]() {
+        void *ptr = nullptr;
+        g_scratch_err[dev] = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? ptr : nullptr;
+    });
+    return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" {
+
+int lynx_attn_anchor_decode_noalloc(const lynx_layout *L, int32_t B, int32_t Hq,
+                                    int32_t max_seq_len, const int32_t *seq_lens,
+                                    const int32_t *block_table, const uint8_t *k_anc,
+                                    const uint8_t *v_anc, const lynx_meta *meta,
+                                    const void *q_bf16, void *out_bf16, float *lse, void *stream) {
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_attention_common(L, B, Hq, max_seq_len, seq_lens, block_table, k_anc, v_anc,
+                                    meta, q_bf16, out_bf16, &g, &mp);
+    if (rc != LYNX_OK) return rc;
+    if (B == 0) return LYNX_OK;
+    if (lse && !aligned16(lse)) return LYNX_EINVAL;
+    const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, 1, max_seq_len, false);
+    if (p.workspace_bytes() > kScratchBytes) return LYNX_EWORKSPACE;
+    void *ws = scratch_on_current_device();
+    if (!ws) return LYNX_EHIP;
+    hipError_t e = lynx::launch_attention(
+        lynx::KvMode::kAnchor, g, p, B, Hq, 1, max_seq_len, seq_lens, block_table, k_anc, v_anc,
+        mp, static_cast<const uint16_t *>(q_bf16), nullptr, nullptr, 0,
+        static_cast<uint16_t *>(out_bf16), lse, ws, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
 

@@ -64,6 +64,8 @@ def load():
         "lynx_attn_workspace_bytes": ([LP, I32, I32, I32, I32], SZ),
         "lynx_attn_anchor_decode": ([LP, I32, I32, I32, P, P, P, P, MP, P, P, P, P, SZ, P],
                                     ctypes.c_int),
+        "lynx_attn_anchor_decode_noalloc": ([LP, I32, I32, I32, P, P, P, P, MP, P, P, P, P],
+                                            ctypes.c_int),
         "lynx_attn_verify": ([LP, I32, I32, I32, I32, P, P, P, P, MP, P, P, P, P, P, SZ, P],
                              ctypes.c_int),
         "lynx_attn_anchor_decode_tail": ([LP, I32, I32, I32, P, P, P, P, MP, P, I32, P, P, P, P, P,
@@ -210,6 +212,21 @@ def lynx_attn_anchor_decode(L: Layout, B: int, Hq: int, max_seq_len: int, seq_le
         ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table), _ptr(k_anc),
         _ptr(v_anc), ctypes.byref(met), _ptr(q), _ptr(out), _ptr(lse), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+# Scratch held by the library for lynx_attn_anchor_decode_noalloc (lynx.h).
+NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def lynx_attn_anchor_decode_noalloc(L: Layout, B: int, Hq: int, max_seq_len: int, seq_lens,
+                                    block_table, k_anc, v_anc, meta: Meta, q, out, lse=None,
+                                    stream=None) -> None:
+    """lynx_attn_anchor_decode without a workspace: the library's own static
+    scratch (calls that overlap on one GPU race)."""
+    lay, met = L.c(), meta.c()
+    _check("lynx_attn_anchor_decode_noalloc", load().lynx_attn_anchor_decode_noalloc(
+        ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table), _ptr(k_anc),
+        _ptr(v_anc), ctypes.byref(met), _ptr(q), _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def lynx_attn_anchor_decode_tail(L: Layout, B: int, Hq: int, max_seq_len: int, seq_lens,

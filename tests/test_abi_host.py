@@ -112,6 +112,14 @@ def test_validation_rejects_before_launch(lib):
                                 1 << 20, None) == E.LYNX_EINVAL
     assert lib.lynx_attn_verify(ctypes.byref(lay), 1, 32, 4, 64, *vargs, 16, None, 16, 16,
                                 1 << 20, None) == E.LYNX_EINVAL
+    # the no-allocation decode rejects a call that needs more than its static
+    # scratch before touching the device: 64 sequences x 8 kv heads x 16
+    # heads x 512 splits of partials
+    big = _layout(max_tokens=1 << 18, block_tokens=1 << 18, max_blocks_per_seq=1).c()
+    assert lib.lynx_attn_anchor_decode_noalloc(ctypes.byref(big), 64, 128, 1 << 18, *args, None,
+                                               None) == E.LYNX_EWORKSPACE
+    assert lib.lynx_attn_anchor_decode_noalloc(ctypes.byref(lay), 1, 12, 64, *args, None,
+                                               None) == E.LYNX_EINVAL
     # B == 0 is a valid empty call
     assert lib.lynx_attn_anchor_decode(ctypes.byref(lay), 0, 32, 64, None, None, None, None,
                                        ctypes.byref(meta), None, None, None, None, 0,
