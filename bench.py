@@ -378,7 +378,8 @@ def overlap_70b_stage(dev):
     out = torch.empty(B, Hq, 128, dtype=torch.bfloat16, device=dev)
     outv = torch.empty(B, nq, Hq, 128, dtype=torch.bfloat16, device=dev)
     nws = max(lynx.lynx_attn_workspace_bytes(L, B, Hq, 1, T), lynx.lynx_attn_workspace_bytes(L, B, Hq, nq, T))
-    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    # zero-filled: the arrival counters at the workspace's head start at zero
+    ws = torch.zeros(nws, dtype=torch.uint8, device=dev)
     main_s, side = torch.cuda.current_stream(), torch.cuda.Stream()
     ev = lambda: torch.cuda.Event(enable_timing=True)
 
