@@ -28,9 +28,14 @@ tokens in 16-token blocks; and the 70B-shaped overlap run (4 x 128K tokens,
 64 q / 8 kv heads: 16 decode steps against the residual H2D, then merge and
 verification of 4 drafts, with the overlap fraction and end-to-end time).
 
+Every stage is timed with a pair of HIP events around each call (or block of
+per-layer calls) after untimed warm-ups and reported as the median, with min,
+max and count where the spread matters: 50 samples unless stated (50 steps by
+default; ten runs for the millisecond-long transport pipelines).
+
 Printed: one JSON line.  `value` is the anchor-decode attention throughput in
-GB/s of algorithmic KV bytes (144 bytes per token per kv head) over the timed
-steps, from HIP events on the stream the kernels run on.
+GB/s of algorithmic KV bytes (144 bytes per token per kv head) over all the
+timed steps, from HIP events on the stream the kernels run on.
 
 Offline helpers (no GPU) turn rocprofv3 output of this script into the text
 summaries kept under profiles/:
@@ -67,12 +72,41 @@ MERGE_BYTES_PER_ELEM = 2.0                      # read 0.5 + 0.5, write 1
 DECODE_BYTES_PER_TOKEN_HEAD = 64 + 64 + 8 + 8   # K, V nibble rows + V meta + K meta (amortised)
 VERIFY_BYTES_PER_TOKEN_HEAD = 128 + 128 + 8 + 8  # K, V code rows + metadata
 
+# timed samples per stage, after untimed warm-ups
+REPS, WARM = 50, 5
+
+
+def summary(samples):
+    """Median, min, max and count of a list of timings (us)."""
+    s = sorted(samples)
+    n = len(s)
+    med = s[n // 2] if n % 2 else 0.5 * (s[n // 2 - 1] + s[n // 2])
+    return {"median": round(med, 3), "min": round(s[0], 3), "max": round(s[-1], 3), "n": n}
+
+
+def call_samples(fn, n=REPS, warm=WARM, per=1):
+    """us per unit of `fn` (which covers `per` units), one pair of HIP events
+    on the current stream around each of n timed calls after `warm` untimed ones."""
+    import torch
+
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)]
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) * 1e3 / per for a, b in evs]
+
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=10)
-    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--layers", type=int, default=None, help="override layer count (testing only)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=8)
@@ -86,7 +120,7 @@ def parse():
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     p.add_argument("--no-spec-stages", dest="spec_stages", action="store_false",
                    help="skip the decode-with-tail and draft-acceptance stages")
-    p.add_argument("--paged-calls", type=int, default=20,
+    p.add_argument("--paged-calls", type=int, default=REPS,
                    help="timed paged batch-decode calls (paged-b16-16k-64k; 0 skips the stage)")
     p.add_argument("--no-hier", dest="hier", action="store_false",
                    help="skip the hierarchical-codec stage")
@@ -96,7 +130,7 @@ def parse():
                    help="skip the serializer / deserializer pipeline stage")
     p.add_argument("--no-overlap-70b", dest="overlap_70b", action="store_false",
                    help="skip the 70B-shaped overlap run (70b-overlap-b4-128k)")
-    p.add_argument("--verify-128k-calls", type=int, default=20,
+    p.add_argument("--verify-128k-calls", type=int, default=REPS,
                    help="timed verification calls at 128K context (0 skips the stage)")
     return p.parse_args()
 
@@ -247,7 +281,11 @@ def verify_128k(calls, dev):
     """Verification at 128K context (32 q / 8 kv heads, k = 8 drafts with
     their causal BF16 tail) over merged codes: two encoded layers, used in
     turn so that no call finds the previous one's bytes in the 256 MB
-    last-level cache; HIP events around the timed calls."""
+    last-level cache; a pair of HIP events around each call.  Then, on the
+    same layer, the anchor-only decode of draft 0 against the verification of
+    draft 0 over the merged codes without the tail: the deviation the
+    residual removes (vNMSE = E ||o_anchor - o_full||^2 / ||o_full||^2 over
+    the query heads, and the largest absolute difference)."""
     import torch
 
     from paper_2607_01831_amd import inputs, lynx
@@ -272,26 +310,36 @@ def verify_128k(calls, dev):
         vns.append(vn)
     out = torch.empty(1, nq, Hq, 128, dtype=torch.bfloat16, device=dev)
     ws = lynx.workspace(L3, 1, Hq, nq, T3)
+    turn = [0]
 
-    def call(i):
+    def call():
+        i = turn[0]
+        turn[0] += 1
         p = pools[i % 2]
         lynx.lynx_attn_verify(L3, 1, Hq, nq, T3, lens, table, p.k_codes, p.v_codes, p.meta,
                               qs[i % 2], kns[i % 2], vns[i % 2], out, ws)
 
-    for i in range(4):
-        call(i)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in range(calls):
-        call(i)
-    e1.record()
-    torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) * 1e3 / calls
+    st = summary(call_samples(call, n=calls))
+    us = st["median"]
     gbps = T3 * Hkv * VERIFY_BYTES_PER_TOKEN_HEAD / (us * 1e-6) / 1e9
+    # anchor-only decode vs the merged-code verification, draft 0, no tail
+    p = pools[0]
+    q0 = qs[0][:, 0].contiguous()                      # [1][Hq][128]
+    o_anc = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device=dev)
+    o_full = torch.empty(1, 1, Hq, 128, dtype=torch.bfloat16, device=dev)
+    lynx.lynx_attn_anchor_decode(L3, 1, Hq, T3, lens, table, p.k_anc, p.v_anc, p.meta, q0, o_anc,
+                                 None, ws)
+    lynx.lynx_attn_verify(L3, 1, Hq, 1, T3, lens, table, p.k_codes, p.v_codes, p.meta,
+                          q0.view(1, 1, Hq, 128), None, None, o_full, ws)
+    torch.cuda.synchronize()
+    oa, of = o_anc[0].float(), o_full[0, 0].float()
+    vn = float(((oa - of).pow(2).sum(dim=-1) / of.pow(2).sum(dim=-1)).mean())
     del pools
-    return {"verify_128k_us": round(us, 2), "verify_128k_GBps": round(gbps, 2),
-            "verify_128k_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+    return {"verify_128k_us": round(us, 2), "verify_128k_us_min": st["min"],
+            "verify_128k_us_max": st["max"], "verify_128k_calls": st["n"],
+            "verify_128k_GBps": round(gbps, 2), "verify_128k_frac": round(gbps / HBM_PEAK_GBPS, 4),
+            "anchor_vs_full_128k": {"query": "draft 0, no tail", "vnmse": float(f"{vn:.3g}"),
+                                    "max_abs_diff": round(float((oa - of).abs().max()), 5)}}
 
 
 def paged_decode_stage(calls, dev):
@@ -327,28 +375,22 @@ def paged_decode_stage(calls, dev):
         lynx.lynx_attn_anchor_decode(L, w.batch, w.Hq, max_len, ldev, tdev, pool.k_anc, pool.v_anc,
                                      pool.meta, q, out, None, ws)
 
-    for _ in range(3):
-        call()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(calls):
-        call()
-    e1.record()
-    torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) * 1e3 / calls
+    st = summary(call_samples(call, n=calls))
+    us = st["median"]
     nbytes = int(lens.sum()) * w.Hkv * DECODE_BYTES_PER_TOKEN_HEAD
     gbps = nbytes / (us * 1e-6) / 1e9
     del pool
-    return {"paged_b16_decode_us": round(us, 2), "paged_b16_decode_MB": round(nbytes / 1e6, 1),
+    return {"paged_b16_decode_us": round(us, 2), "paged_b16_decode_us_min": st["min"],
+            "paged_b16_decode_us_max": st["max"], "paged_b16_decode_calls": st["n"],
+            "paged_b16_decode_MB": round(nbytes / 1e6, 1),
             "paged_b16_decode_GBps": round(gbps, 2),
             "paged_b16_decode_frac": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
 def overlap_70b_stage(dev):
     """The 70B-shaped overlap run (70b-overlap-b4-128k): 4 sequences x 131072
-    tokens, 64 q / 8 kv heads.  Timed with HIP events, each part alone and
-    then overlapped: 16 anchor-decode steps (a fresh query per step); the
+    tokens, 64 q / 8 kv heads.  Timed with HIP events over ten runs (medians;
+    every decode step also alone), each part alone and then overlapped: 16 anchor-decode steps (a fresh query per step); the
     H2D of the residual planes (512 MiB) from pinned host memory on a side
     stream; both at once; then merge of both planes and verification of
     k = 4 drafts with their causal BF16 tail.  overlap = (t_dec + t_h2d -
@@ -383,10 +425,14 @@ def overlap_70b_stage(dev):
     main_s, side = torch.cuda.current_stream(), torch.cuda.Stream()
     ev = lambda: torch.cuda.Event(enable_timing=True)
 
-    def decode_steps():
+    def decode_steps(step_evs=None):
         for s in range(steps):
+            if step_evs is not None:
+                step_evs[s][0].record(main_s)
             lynx.lynx_attn_anchor_decode(L, B, Hq, T, lens, table, pool.k_anc, pool.v_anc, pool.meta,
                                          qs[s], out, None, ws)
+            if step_evs is not None:
+                step_evs[s][1].record(main_s)
 
     def transport(after):
         side.wait_event(after)
@@ -409,12 +455,14 @@ def overlap_70b_stage(dev):
     decode_steps()
     merge_verify()
     torch.cuda.synchronize()
-    best = None
-    for _ in range(3):
-        # decode alone
+    runs, step_us = [], []
+    for _ in range(10):
+        # decode alone (a pair of events around each step too)
         a0, a1 = ev(), ev()
-        a0.record(main_s); decode_steps(); a1.record(main_s)
+        sev = [(ev(), ev()) for _ in range(steps)]
+        a0.record(main_s); decode_steps(sev); a1.record(main_s)
         torch.cuda.synchronize()
+        step_us += [x.elapsed_time(y) * 1e3 for x, y in sev]
         # transport alone
         h0 = ev(); h0.record(main_s)
         h1 = transport(h0)
@@ -428,18 +476,24 @@ def overlap_70b_stage(dev):
         m1 = merge_verify()
         v1 = ev(); v1.record(main_s)
         torch.cuda.synchronize()
-        r = {"t_dec": a0.elapsed_time(a1), "t_h2d": h0.elapsed_time(h1), "t_both": b0.elapsed_time(b1),
-             "merge": b1.elapsed_time(m1), "verify": m1.elapsed_time(v1), "e2e": b0.elapsed_time(v1)}
-        if best is None or r["e2e"] < best["e2e"]:
-            best = r
+        runs.append({"t_dec": a0.elapsed_time(a1), "t_h2d": h0.elapsed_time(h1),
+                     "t_both": b0.elapsed_time(b1), "merge": b1.elapsed_time(m1),
+                     "verify": m1.elapsed_time(v1), "e2e": b0.elapsed_time(v1)})
+    # medians over the runs (ms)
+    best = {k: summary([r_[k] for r_ in runs])["median"] for k in runs[0]}
     t_dec, t_h2d, t_both = best["t_dec"], best["t_h2d"], best["t_both"]
+    st_step = summary(step_us)
     dec_bytes = B * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
     res_bytes = host_k.numel() + host_v.numel()
     merge_bytes = 2 * B * T * Hkv * 128 * MERGE_BYTES_PER_ELEM
     ver_bytes = B * T * Hkv * VERIFY_BYTES_PER_TOKEN_HEAD
-    us_step = t_dec * 1e3 / steps
+    us_step = st_step["median"]
     r = {
+        "runs": len(runs),
         "decode_us_per_step": round(us_step, 2),
+        "decode_us_per_step_min": st_step["min"],
+        "decode_us_per_step_max": st_step["max"],
+        "decode_steps_timed": st_step["n"],
         "decode_GBps": round(dec_bytes / (us_step * 1e-6) / 1e9, 2),
         "decode_frac": round(dec_bytes / (us_step * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
         "decode_16_steps_us": round(t_dec * 1e3, 1),
@@ -478,7 +532,7 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
     m, so neither waits behind the other), the sends on the side stream, the
     receives on a third.  The send and receive of this loopback share one PCIe link, which
     carries both directions at once (≈56 GB/s each).  HIP events give the
-    times, relative to the first serialize; the same pipeline without its
+    times, relative to the first serialize, medians over ten runs; the same pipeline without its
     kernels gives the wire alone.  The received pool is checked against the
     direct encode + merge of the same layers."""
     import torch
@@ -555,24 +609,18 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
                 "residuals_sent": ms(sent[-1]), "full_ready": ms(des[-1])}
 
     run()
-    best = wire = None
-    for _ in range(3):
-        r = run()
-        if best is None or r["full_ready"] < best["full_ready"]:
-            best = r
-        r = run(kernels=False)
-        if wire is None or r["full_ready"] < wire["full_ready"]:
-            wire = r
+    piped, wires = [], []
+    for _ in range(10):
+        piped.append(run())
+        wires.append(run(kernels=False))
+    # medians over the runs (the pinned-host copy rate varies run to run)
+    best = {k: summary([r_[k] for r_ in piped])["median"] for k in piped[0]}
+    wire = {k: summary([r_[k] for r_ in wires])["median"] for k in wires[0]}
+    full_spread = summary([r_["full_ready"] for r_ in piped])
     run()
-    # each kernel alone
+    # each kernel alone: median over blocks of all layers (ms per block)
     def alone(fn):
-        torch.cuda.synchronize()
-        a, b = ev(), ev()
-        a.record()
-        fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b)
+        return summary(call_samples(fn, n=20, warm=2))["median"] * 1e-3
     t_ser = alone(lambda: [lynx.lynx_kv_serialize(Hkv, T, K[l], V[l], tx_anc[l % n_tx], tx_res[l])
                            for l in range(n_layers)])
     t_da = alone(lambda: [lynx.lynx_kv_deserialize_anchor(L, 0, 0, T, table, rx["a"][l % 2], recv[l].k_anc,
@@ -594,7 +642,9 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
         "deserialize_anchor_GBps": round(2 * na * n_layers / (t_da * 1e-3) / 1e9, 1),
         "deserialize_residual_us_per_object": round(us_l(t_dr), 2),
         "deserialize_residual_GBps": round(T * Hkv * 512 * n_layers / (t_dr * 1e-3) / 1e9, 1),
+        "runs": len(piped),
         "pipelined_ms": {k: round(v, 3) for k, v in best.items()},
+        "pipelined_full_ready_ms_min_max": [full_spread["min"], full_spread["max"]],
         "wire_only_ms": {k: round(v, 3) for k, v in wire.items()},
         "wire_GBps_per_direction": round((na + nr) * n_layers / (wire["full_ready"] * 1e-3) / 1e9, 2),
         "anchor_ready_over_full": round(best["anchor_ready"] / best["full_ready"], 3),
@@ -647,16 +697,9 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
     a0 = alphas[0]
     variants = {"biased": lynx.LYNX_HQ_BIASED, "centred": lynx.LYNX_HQ_CENTRED, "int4": lynx.LYNX_HQ_INT4}
 
-    def timed(fn, reps=2):
-        fn()
-        torch.cuda.synchronize()
-        e0, e1 = ev(), ev()
-        e0.record()
-        for _ in range(reps):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / (reps * n_layers)
+    def timed(fn):
+        """Median us per layer over REPS blocks of all layers."""
+        return summary(call_samples(fn, n=REPS, warm=2, per=n_layers))["median"]
 
     def encode(l, a, vid, into=None):
         res = vid != lynx.LYNX_HQ_INT4
@@ -771,14 +814,8 @@ def split_widths_stage(dev, T, Hkv, K, V, n_layers):
         out = {}
         for name, fn, per_elem in (("encode", enc, 2 + 1 + 0.0625), ("merge", merge, 2.0),
                                    ("dequant_anchor", deq, A / 8 + 2 + 0.0625)):
-            fn()
-            torch.cuda.synchronize()
-            e0, e1 = ev(), ev()
-            e0.record()
-            fn()
-            e1.record()
-            torch.cuda.synchronize()
-            us = e0.elapsed_time(e1) * 1e3 / n_layers
+            # median us per layer over REPS blocks of all layers
+            us = summary(call_samples(fn, n=REPS, warm=2, per=n_layers))["median"]
             out[f"{name}_us_per_layer"] = round(us, 2)
             out[f"{name}_GBps"] = round(elems * per_elem / (us * 1e-6) / 1e9, 1)
         r[f"split_{A}_{R}"] = out
@@ -786,9 +823,26 @@ def split_widths_stage(dev, T, Hkv, K, V, n_layers):
     return {"split_widths": r}
 
 
-def cpu_baseline(w, layer_inputs, n_layers):
-    """The CPU oracle, untuned, timed on this host on a bounded sample: the
-    anchor decode of the first n_layers layers (all kv heads)."""
+def host_cpu():
+    """The host CPU's model name and logical core count."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.lower().startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu": model, "nproc": os.cpu_count()}
+
+
+def cpu_baseline(w, layer_inputs, n_dec=8, n_enc=4, n_ver=2):
+    """The CPU oracle, untuned, timed on this host on bounded samples of the
+    workload's step: its encode (single-threaded) and merge (single-threaded)
+    of n_enc layers, its anchor decode of n_dec layers and its verification
+    (k drafts with the causal BF16 tail) of n_ver layers, both threaded over
+    the kv heads on every core this process may use.  GB/s with the GPU's
+    algorithmic bytes; `value` is the anchor decode's (the metric's step)."""
     import numpy as np
     import torch
 
@@ -801,20 +855,48 @@ def cpu_baseline(w, layer_inputs, n_layers):
     T, Hkv = w.context, w.Hkv
     OL = oracle.Layout(Hkv=Hkv, bt=T, max_blocks=1, max_tokens=T)
     table = np.zeros((1, 1), np.int32)
-    t_dec = 0.0
-    for l in range(n_layers):
-        k, v, q = layer_inputs(l)
-        planes, meta = oracle.encode_batch(OL, [T], table, [bits(k)], [bits(v)], 1)
+    t = {"encode": 0.0, "merge": 0.0, "decode": 0.0, "verify": 0.0}
+    for l in range(max(n_dec, n_enc, n_ver)):
+        k, v, q, qv, kn, vn = layer_inputs(l)
         t0 = time.perf_counter()
-        oracle.anchor_decode(OL, w.Hq, np.array([T]), table, planes["k_anc"], planes["v_anc"],
-                             meta, bits(q), nthreads=threads)
-        t_dec += time.perf_counter() - t0
-    nbytes = n_layers * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD
-    return {"value": round(nbytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": threads,
+        planes, meta = oracle.encode_batch(OL, [T], table, [bits(k)], [bits(v)], 1)
+        t1 = time.perf_counter()
+        kc = oracle.merge(planes["k_anc"], planes["k_res"])
+        vc = oracle.merge(planes["v_anc"], planes["v_res"])
+        t2 = time.perf_counter()
+        if l < n_enc:
+            t["encode"] += t1 - t0
+            t["merge"] += t2 - t1
+        if l < n_dec:
+            t0 = time.perf_counter()
+            oracle.anchor_decode(OL, w.Hq, np.array([T]), table, planes["k_anc"], planes["v_anc"],
+                                 meta, bits(q), nthreads=threads)
+            t["decode"] += time.perf_counter() - t0
+        if l < n_ver:
+            t0 = time.perf_counter()
+            oracle.verify(OL, w.Hq, np.array([T]), table, kc, vc, meta, bits(qv), bits(kn), bits(vn),
+                          nthreads=threads)
+            t["verify"] += time.perf_counter() - t0
+    elems = T * Hkv * 128 * 2
+    gb = lambda nbytes, secs: round(nbytes / secs / 1e9, 4)
+    steps = {
+        "encode": {"GBps": gb(n_enc * elems * ENC_BYTES_PER_ELEM, t["encode"]), "cores": 1,
+                   "layers": n_enc, "s": round(t["encode"], 2)},
+        "merge": {"GBps": gb(n_enc * elems * MERGE_BYTES_PER_ELEM, t["merge"]), "cores": 1,
+                  "layers": n_enc, "s": round(t["merge"], 2)},
+        "anchor_decode": {"GBps": gb(n_dec * T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD, t["decode"]),
+                          "cores": threads, "layers": n_dec, "s": round(t["decode"], 2)},
+        "verify": {"GBps": gb(n_ver * T * Hkv * VERIFY_BYTES_PER_TOKEN_HEAD, t["verify"]),
+                   "us_per_layer": round(t["verify"] * 1e6 / n_ver, 1), "cores": threads,
+                   "layers": n_ver, "s": round(t["verify"], 2)},
+    }
+    return {"value": steps["anchor_decode"]["GBps"], "unit": "GB/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"anchor decode (fp64 oracle, on its own encode of the same seeded inputs) "
-                      f"of {n_layers} of {w.layers} layers, all {Hkv} kv heads, {T} tokens; "
-                      f"{t_dec:.2f} s of decode"}
+            "sample": f"fp64 oracle on the same seeded inputs, {T} tokens, all {Hkv} kv heads: "
+                      f"anchor decode of {n_dec} of {w.layers} layers on {threads} threads "
+                      f"({t['decode']:.2f} s); also encode and merge of {n_enc} layers (one "
+                      f"thread) and verification of k={w.drafts} drafts of {n_ver} layers",
+            "steps": steps, "host": host_cpu()}
 
 
 # ----------------------------------------------------------------------- main --
@@ -932,16 +1014,13 @@ def main():
 
     # The same decode calls once more with no residual transport running
     # (reported beside the step's figure, which overlaps the transport).
-    e0, e1 = ev(), ev()
-    e0.record(main_s)
-    for _ in range(args.steps):
+    def decode_layers():
         for l in range(n_layers):
             p = pools[l]
             lynx.lynx_attn_anchor_decode(L, 1, Hq, T, lens, table, p.k_anc, p.v_anc, p.meta,
                                          Q[l], out, None, ws)
-    e1.record(main_s)
-    torch.cuda.synchronize()
-    t_dec_alone = e0.elapsed_time(e1) / args.steps
+
+    st_dec_alone = summary(call_samples(decode_layers, n=max(args.steps, 1), warm=1, per=n_layers))
 
     ver128 = verify_128k(args.verify_128k_calls, dev) if args.verify_128k_calls > 0 else None
     paged = paged_decode_stage(args.paged_calls, dev) if args.paged_calls > 0 else None
@@ -955,16 +1034,14 @@ def main():
     # acceptance of 8 drafts over a 128256-entry vocabulary.
     spec = {}
     if args.spec_stages:
-        e0, e1 = ev(), ev()
-        e0.record(main_s)
-        for _ in range(args.steps):
+        def decode_tail_layers():
             for l in range(n_layers):
                 p = pools[l]
                 lynx.lynx_attn_anchor_decode_tail(L, 1, Hq, T, lens, table, p.k_anc, p.v_anc, p.meta,
                                                   Q[l], KN[l], VN[l], out, None, ws)
-        e1.record(main_s)
-        torch.cuda.synchronize()
-        spec["anchor_decode_tail8_us_per_layer"] = round(e0.elapsed_time(e1) * 1e3 / (args.steps * n_layers), 3)
+
+        spec["anchor_decode_tail8_us_per_layer"] = summary(
+            call_samples(decode_tail_layers, n=max(args.steps, 1), warm=1, per=n_layers))["median"]
         vocab = 128256
         g = torch.Generator().manual_seed(7)
         logits = torch.randn(1, nq + 1, vocab, generator=g).to(dev)
@@ -973,14 +1050,8 @@ def main():
         nxt = torch.empty(1, dtype=torch.int32, device=dev)
         aws = torch.empty(max(lynx.lynx_spec_accept_workspace_bytes(1, nq, vocab), 16),
                           dtype=torch.uint8, device=dev)
-        for _ in range(3):
-            lynx.lynx_spec_accept_greedy(logits, drafts, acc, nxt, aws)
-        e0.record(main_s)
-        for _ in range(20):
-            lynx.lynx_spec_accept_greedy(logits, drafts, acc, nxt, aws)
-        e1.record(main_s)
-        torch.cuda.synchronize()
-        spec["accept_greedy_k8_vocab128256_us"] = round(e0.elapsed_time(e1) * 1e3 / 20, 2)
+        spec["accept_greedy_k8_vocab128256_us"] = summary(call_samples(
+            lambda: lynx.lynx_spec_accept_greedy(logits, drafts, acc, nxt, aws)))["median"]
         spec["accept_greedy_all_kept"] = int(acc.item()) == nq
         # acceptance of sampled drafts over the same vocabulary: target and
         # draft distributions (softmax of the scores and of perturbed ones)
@@ -988,17 +1059,15 @@ def main():
         qprobs = torch.softmax(logits[:, :nq] + 0.5 * torch.randn(1, nq, vocab, generator=g).to(dev),
                                dim=2).contiguous()
         uni = torch.rand(1, nq + 1, generator=g).to(dev)
-        for _ in range(3):
-            lynx.lynx_spec_accept_sample(probs, qprobs, drafts, uni, acc, nxt, aws)
-        e0.record(main_s)
-        for _ in range(20):
-            lynx.lynx_spec_accept_sample(probs, qprobs, drafts, uni, acc, nxt, aws)
-        e1.record(main_s)
-        torch.cuda.synchronize()
-        spec["accept_sample_k8_vocab128256_us"] = round(e0.elapsed_time(e1) * 1e3 / 20, 2)
+        spec["accept_sample_k8_vocab128256_us"] = summary(call_samples(
+            lambda: lynx.lynx_spec_accept_sample(probs, qprobs, drafts, uni, acc, nxt, aws)))["median"]
 
     def ms(a, b):
         return sum(r[a].elapsed_time(r[b]) for r in recs) / len(recs)
+
+    def per_layer(a, b):
+        """median, min, max over the timed steps of one stage, us per layer"""
+        return summary([r[a].elapsed_time(r[b]) * 1e3 / n_layers for r in recs])
 
     t_step = ms("start", "ver")
     t_enc = ms("start", "enc")
@@ -1043,8 +1112,14 @@ def main():
             "encode_us_per_layer": round(t_enc * 1e3 / n_layers, 2),
             "anchor_decode_GBps": round(dec_gbps, 2),
             "anchor_decode_us_per_layer": round(t_dec * 1e3 / n_layers, 3),
-            "anchor_decode_GBps_without_transport": round(dec_bytes / (t_dec_alone * 1e-3) / 1e9, 2),
-            "anchor_decode_us_per_layer_without_transport": round(t_dec_alone * 1e3 / n_layers, 3),
+            "anchor_decode_GBps_without_transport": round(
+                T * Hkv * DECODE_BYTES_PER_TOKEN_HEAD / (st_dec_alone["median"] * 1e-6) / 1e9, 2),
+            "anchor_decode_us_per_layer_without_transport": st_dec_alone["median"],
+            "per_layer_us": {"encode": per_layer("start", "enc"),
+                             "anchor_decode": per_layer("dec0", "dec"),
+                             "anchor_decode_without_transport": st_dec_alone,
+                             "merge": per_layer("merge0", "merge"),
+                             "verify": per_layer("merge", "ver")},
             "merge_GBps": round(merge_gbps, 2), "merge_frac": round(merge_gbps / HBM_PEAK_GBPS, 4),
             "merge_us_per_layer": round(t_merge * 1e3 / n_layers, 2),
             "verify_us_per_layer": round(ver_us, 2),
@@ -1075,9 +1150,12 @@ def main():
     }
     if not args.no_cpu_baseline:
         def layer_inputs(l):
+            kn, vn = inputs.drafts_kv(w, layer=l)
             return (inputs.kv(w, "k", layer=l), inputs.kv(w, "v", layer=l),
-                    inputs.queries(w, layer=l))
-        result["cpu_baseline"] = cpu_baseline(w, layer_inputs, min(args.cpu_layers, n_layers))
+                    inputs.queries(w, layer=l), inputs.queries(w, layer=l, step=1, nq=nq), kn, vn)
+        nl = min(args.cpu_layers, n_layers)
+        result["cpu_baseline"] = cpu_baseline(w, layer_inputs, n_dec=nl, n_enc=min(4, nl),
+                                              n_ver=min(2, nl))
     print(json.dumps(result), flush=True)
 
 

@@ -10,6 +10,8 @@
 #include <float.h>
 #include <math.h>
 
+#include <mutex>
+
 namespace lynx {
 namespace {
 
@@ -234,6 +236,20 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     }
 }
 
+// Compute units of the current device (0 if unknown), queried once per device.
+int compute_units() {
+    constexpr int kMaxDevices = 64;
+    static std::once_flag once[kMaxDevices];
+    static int cus[kMaxDevices];
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+    std::call_once(once[dev], [dev]() {
+        int n = 0;
+        cus[dev] = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess ? n : 0;
+    });
+    return cus[dev];
+}
+
 }  // namespace
 
 AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_len, bool tail) {
@@ -328,10 +344,20 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
         d.ws_splits = plan.n_splits;
         // without a tail the last workgroup of each (sequence, kv head, head
         // chunk) merges the splits itself: no second launch
-        // (the merge holds up to two splits' (max, sum) per thread: 256 / GP
-        // threads per row, GP = 4, 8 or 16 rows padded)
+        // The in-kernel merge costs every workgroup a wait for its partial's
+        // stores and an atomic (about 1.2 us), during which it holds its CU
+        // slot: a win when the whole grid runs in one round (two workgroups
+        // per CU), a loss over several rounds, where the combine kernel
+        // merges instead (70B batch: 126 us per step with the combine, 133
+        // fused; 32K layer: 17.7 us with the combine, 15.9 fused).  The merge
+        // holds up to two splits' (max, sum) per thread: 256 / GP threads per
+        // row, GP = 4, 8 or 16 rows padded.
         const int gp = d.chunk_heads <= 4 ? 4 : d.chunk_heads <= 8 ? 8 : 16;
-        d.fused = (k_new == nullptr && plan.counters_fit && plan.n_ctx_splits <= 2 * (256 / gp)) ? 1 : 0;
+        const int chunks_ = (a.G + d.chunk_heads - 1) / d.chunk_heads;
+        const long long wgs = (long long)plan.n_ctx_splits * g.Hkv * chunks_ * B;
+        const bool one_round = wgs <= 2LL * compute_units();
+        d.fused = (k_new == nullptr && plan.counters_fit && plan.n_ctx_splits <= 2 * (256 / gp) &&
+                   one_round) ? 1 : 0;
         d.row_chunks = plan.row_chunks;
         d.counters = reinterpret_cast<unsigned *>(workspace);
         d.out = out;

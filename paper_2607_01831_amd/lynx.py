@@ -123,6 +123,38 @@ def _check(fn: str, status: int):
         raise LynxError(fn, status)
 
 
+# Size checks of the tensors a call reads or writes.  The C ABI sees only
+# pointers, so a short tensor would become an out-of-bounds device access:
+# the binding rejects it first.
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def _need(fn: str, what: str, t, nbytes: int) -> None:
+    if isinstance(t, torch.Tensor) and _nbytes(t) < nbytes:
+        raise ValueError(f"{fn}: {what} holds {_nbytes(t)} bytes; the call uses {nbytes}")
+
+
+def _need_meta(fn: str, L: "Layout", meta: "Meta", rows: int) -> None:
+    """fp32 metadata rows 0 .. rows - 1 (sequences) of the layout."""
+    k = rows * L.num_kv_heads * L.n_groups * HEAD_DIM * 4
+    v = rows * L.num_kv_heads * L.max_tokens * 4
+    for name, nbytes in (("k_scale", k), ("k_zero", k), ("v_scale", v), ("v_zero", v)):
+        _need(fn, f"meta.{name}", getattr(meta, name), nbytes)
+
+
+def _need_attn(fn: str, L: "Layout", B: int, seq_lens, block_table, planes, row_bytes: int,
+               meta: "Meta") -> None:
+    """The per-batch arguments every attention call reads."""
+    if B <= 0:
+        return
+    _need(fn, "seq_lens", seq_lens, B * 4)
+    _need(fn, "block_table", block_table, B * L.max_blocks_per_seq * 4)
+    for i, t in enumerate(planes):
+        _need(fn, f"plane {i}", t, L.plane_bytes(row_bytes))
+    _need_meta(fn, L, meta, B)
+
+
 @dataclass
 class Layout:
     """Cache geometry (see lynx_layout in include/lynx.h)."""
@@ -170,6 +202,13 @@ class Meta:
 
 def lynx_kv_encode(L: Layout, b: int, T: int, block_table, k, v, k_anc, v_anc, k_res, v_res,
                    meta: Meta, stream=None) -> None:
+    fn = "lynx_kv_encode"
+    _need(fn, "k", k, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "v", v, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "block_table", block_table, (b + 1) * L.max_blocks_per_seq * 4)
+    for name, t in (("k_anc", k_anc), ("v_anc", v_anc), ("k_res", k_res), ("v_res", v_res)):
+        _need(fn, name, t, L.plane_bytes(64))
+    _need_meta(fn, L, meta, b + 1)
     lay, met = L.c(), meta.c()
     _check("lynx_kv_encode", load().lynx_kv_encode(
         ctypes.byref(lay), b, T, _ptr(block_table), _ptr(k), _ptr(v), _ptr(k_anc), _ptr(v_anc),
@@ -206,6 +245,11 @@ def workspace(L: Layout, B: int, Hq: int, num_queries: int, max_seq_len: int,
 def lynx_attn_anchor_decode(L: Layout, B: int, Hq: int, max_seq_len: int, seq_lens,
                             block_table, k_anc, v_anc, meta: Meta, q, out, lse=None,
                             workspace_buf=None, stream=None) -> None:
+    fn = "lynx_attn_anchor_decode"
+    _need_attn(fn, L, B, seq_lens, block_table, (k_anc, v_anc), 64, meta)
+    _need(fn, "q", q, B * Hq * HEAD_DIM * 2)
+    _need(fn, "out", out, B * Hq * HEAD_DIM * 2)
+    _need(fn, "lse", lse, B * Hq * 4)
     lay, met = L.c(), meta.c()
     ws = workspace_buf
     _check("lynx_attn_anchor_decode", load().lynx_attn_anchor_decode(
@@ -223,6 +267,11 @@ def lynx_attn_anchor_decode_noalloc(L: Layout, B: int, Hq: int, max_seq_len: int
                                     stream=None) -> None:
     """lynx_attn_anchor_decode without a workspace: the library's own static
     scratch (calls that overlap on one GPU race)."""
+    fn = "lynx_attn_anchor_decode_noalloc"
+    _need_attn(fn, L, B, seq_lens, block_table, (k_anc, v_anc), 64, meta)
+    _need(fn, "q", q, B * Hq * HEAD_DIM * 2)
+    _need(fn, "out", out, B * Hq * HEAD_DIM * 2)
+    _need(fn, "lse", lse, B * Hq * 4)
     lay, met = L.c(), meta.c()
     _check("lynx_attn_anchor_decode_noalloc", load().lynx_attn_anchor_decode_noalloc(
         ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table), _ptr(k_anc),
@@ -234,6 +283,15 @@ def lynx_attn_anchor_decode_tail(L: Layout, B: int, Hq: int, max_seq_len: int, s
                                  lse=None, workspace_buf=None, stream=None) -> None:
     """Anchor decode that also attends the BF16 tail k_tail / v_tail
     ([B][n_tail][Hkv][128], or None for n_tail = 0)."""
+    fn = "lynx_attn_anchor_decode_tail"
+    _need_attn(fn, L, B, seq_lens, block_table, (k_anc, v_anc), 64, meta)
+    _need(fn, "q", q, B * Hq * HEAD_DIM * 2)
+    _need(fn, "out", out, B * Hq * HEAD_DIM * 2)
+    _need(fn, "lse", lse, B * Hq * 4)
+    if k_tail is not None:
+        nt = int(k_tail.shape[1])
+        _need(fn, "k_tail", k_tail, B * nt * L.num_kv_heads * HEAD_DIM * 2)
+        _need(fn, "v_tail", v_tail, B * nt * L.num_kv_heads * HEAD_DIM * 2)
     lay, met = L.c(), meta.c()
     ws = workspace_buf
     n_tail = 0 if k_tail is None else int(k_tail.shape[1])
@@ -282,6 +340,12 @@ def lynx_spec_accept_sample(target_probs, draft_probs, draft_tokens, uniforms, a
 def lynx_attn_verify(L: Layout, B: int, Hq: int, k: int, max_seq_len: int, seq_lens,
                      block_table, k_codes, v_codes, meta: Meta, q, k_new, v_new, out,
                      workspace_buf=None, stream=None) -> None:
+    fn = "lynx_attn_verify"
+    _need_attn(fn, L, B, seq_lens, block_table, (k_codes, v_codes), 128, meta)
+    _need(fn, "q", q, B * k * Hq * HEAD_DIM * 2)
+    _need(fn, "out", out, B * k * Hq * HEAD_DIM * 2)
+    _need(fn, "k_new", k_new, B * k * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "v_new", v_new, B * k * L.num_kv_heads * HEAD_DIM * 2)
     lay, met = L.c(), meta.c()
     ws = workspace_buf
     _check("lynx_attn_verify", load().lynx_attn_verify(
@@ -324,6 +388,15 @@ def lynx_kv_encode_split(L: Layout, anchor_bits: int, b: int, T: int, block_tabl
                          k_res, v_res, meta: Meta, stream=None) -> None:
     """k, v: BF16 [T][Hkv][128]; planes: uint8 device tensors of rows of
     16 anchor_bits (anchor) and 16 (8 - anchor_bits) (residual) bytes."""
+    fn = "lynx_kv_encode_split"
+    _need(fn, "k", k, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "v", v, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "block_table", block_table, (b + 1) * L.max_blocks_per_seq * 4)
+    if 0 < anchor_bits < 8:
+        for name, t, w in (("k_anc", k_anc, anchor_bits), ("v_anc", v_anc, anchor_bits),
+                           ("k_res", k_res, 8 - anchor_bits), ("v_res", v_res, 8 - anchor_bits)):
+            _need(fn, name, t, L.plane_bytes(16 * w))
+    _need_meta(fn, L, meta, b + 1)
     lay, met = L.c(), meta.c()
     _check("lynx_kv_encode_split", load().lynx_kv_encode_split(
         ctypes.byref(lay), anchor_bits, b, T, _ptr(block_table), _ptr(k), _ptr(v), _ptr(k_anc),
@@ -343,6 +416,14 @@ def lynx_kv_merge_split(anchor_bits: int, anc, res, codes, stream=None) -> None:
 def lynx_kv_dequant_anchor_split(L: Layout, anchor_bits: int, b: int, T: int, block_table, k_anc, v_anc,
                                  meta: Meta, k_out, v_out, stream=None) -> None:
     """k_out, v_out: BF16 [T][Hkv][128] (device, written)."""
+    fn = "lynx_kv_dequant_anchor_split"
+    _need(fn, "block_table", block_table, (b + 1) * L.max_blocks_per_seq * 4)
+    if 0 < anchor_bits < 8:
+        _need(fn, "k_anc", k_anc, L.plane_bytes(16 * anchor_bits))
+        _need(fn, "v_anc", v_anc, L.plane_bytes(16 * anchor_bits))
+    _need_meta(fn, L, meta, b + 1)
+    _need(fn, "k_out", k_out, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "v_out", v_out, T * L.num_kv_heads * HEAD_DIM * 2)
     lay, met = L.c(), meta.c()
     _check("lynx_kv_dequant_anchor_split", load().lynx_kv_dequant_anchor_split(
         ctypes.byref(lay), anchor_bits, b, T, _ptr(block_table), _ptr(k_anc), _ptr(v_anc),
@@ -356,6 +437,19 @@ LYNX_HQ_BIASED, LYNX_HQ_CENTRED, LYNX_HQ_INT4 = 0, 1, 2
 def lynx_hkv_encode(L: Layout, b: int, T: int, block_table, k, v, alpha: float, variant: int,
                     k_anc, v_anc, k_res, v_res, hmeta: HMeta, stream=None) -> None:
     """k_res, v_res may be None for LYNX_HQ_INT4."""
+    fn = "lynx_hkv_encode"
+    _need(fn, "k", k, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "v", v, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "block_table", block_table, (b + 1) * L.max_blocks_per_seq * 4)
+    for name, t in (("k_anc", k_anc), ("v_anc", v_anc), ("k_res", k_res), ("v_res", v_res)):
+        _need(fn, name, t, L.plane_bytes(64))
+    pg = (b + 1) * L.num_kv_heads * -(-L.max_tokens // 256) * HEAD_DIM * 4
+    ch = (b + 1) * L.num_kv_heads * -(-L.max_tokens // 32) * HEAD_DIM * 4
+    for t in ("k", "v"):
+        _need(fn, f"hmeta.{t}_gmin", getattr(hmeta, f"{t}_gmin"), pg)
+        _need(fn, f"hmeta.{t}_gscale", getattr(hmeta, f"{t}_gscale"), pg)
+        _need(fn, f"hmeta.{t}_mu", getattr(hmeta, f"{t}_mu"), ch)
+        _need(fn, f"hmeta.{t}_sigma", getattr(hmeta, f"{t}_sigma"), ch)
     lay, met = L.c(), hmeta.c()
     _check("lynx_hkv_encode", load().lynx_hkv_encode(
         ctypes.byref(lay), b, T, _ptr(block_table), _ptr(k), _ptr(v), alpha, variant, _ptr(k_anc),
@@ -365,6 +459,19 @@ def lynx_hkv_encode(L: Layout, b: int, T: int, block_table, k, v, alpha: float, 
 def lynx_hkv_dequant(L: Layout, b: int, T: int, block_table, full: bool, k_plane, v_plane,
                      alpha: float, variant: int, hmeta: HMeta, k_out, v_out, stream=None) -> None:
     """k_out, v_out: BF16 [T][Hkv][128] (device, written)."""
+    fn = "lynx_hkv_dequant"
+    _need(fn, "block_table", block_table, (b + 1) * L.max_blocks_per_seq * 4)
+    _need(fn, "k_plane", k_plane, L.plane_bytes(128 if full else 64))
+    _need(fn, "v_plane", v_plane, L.plane_bytes(128 if full else 64))
+    _need(fn, "k_out", k_out, T * L.num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "v_out", v_out, T * L.num_kv_heads * HEAD_DIM * 2)
+    pg = (b + 1) * L.num_kv_heads * -(-L.max_tokens // 256) * HEAD_DIM * 4
+    ch = (b + 1) * L.num_kv_heads * -(-L.max_tokens // 32) * HEAD_DIM * 4
+    for t in ("k", "v"):
+        _need(fn, f"hmeta.{t}_gmin", getattr(hmeta, f"{t}_gmin"), pg)
+        _need(fn, f"hmeta.{t}_gscale", getattr(hmeta, f"{t}_gscale"), pg)
+        _need(fn, f"hmeta.{t}_mu", getattr(hmeta, f"{t}_mu"), ch)
+        _need(fn, f"hmeta.{t}_sigma", getattr(hmeta, f"{t}_sigma"), ch)
     lay, met = L.c(), hmeta.c()
     _check("lynx_hkv_dequant", load().lynx_hkv_dequant(
         ctypes.byref(lay), b, T, _ptr(block_table), 1 if full else 0, _ptr(k_plane), _ptr(v_plane),
@@ -383,6 +490,13 @@ def lynx_kv_serialize(num_kv_heads: int, n_tokens: int, k, v, anchor_buf, residu
                       stream=None) -> None:
     """k, v: BF16 [n_tokens][Hkv][128] (an object's tokens); the buffers are
     uint8 device tensors of lynx_serialized_bytes() bytes."""
+    fn = "lynx_kv_serialize"
+    _need(fn, "k", k, n_tokens * num_kv_heads * HEAD_DIM * 2)
+    _need(fn, "v", v, n_tokens * num_kv_heads * HEAD_DIM * 2)
+    if num_kv_heads > 0 and n_tokens > 0:
+        na, nr = lynx_serialized_bytes(num_kv_heads, n_tokens)
+        _need(fn, "anchor_buf", anchor_buf, na)
+        _need(fn, "residual_buf", residual_buf, nr)
     _check("lynx_kv_serialize", load().lynx_kv_serialize(
         num_kv_heads, n_tokens, _ptr(k), _ptr(v), _ptr(anchor_buf), _ptr(residual_buf),
         _stream(stream)))
@@ -390,6 +504,13 @@ def lynx_kv_serialize(num_kv_heads: int, n_tokens: int, k, v, anchor_buf, residu
 
 def lynx_kv_deserialize_anchor(L: Layout, b: int, t0: int, n_tokens: int, block_table, anchor_buf,
                                k_anc, v_anc, meta: Meta, stream=None) -> None:
+    fn = "lynx_kv_deserialize_anchor"
+    _need(fn, "block_table", block_table, (b + 1) * L.max_blocks_per_seq * 4)
+    if n_tokens > 0:
+        _need(fn, "anchor_buf", anchor_buf, lynx_serialized_bytes(L.num_kv_heads, n_tokens)[0])
+    _need(fn, "k_anc", k_anc, L.plane_bytes(64))
+    _need(fn, "v_anc", v_anc, L.plane_bytes(64))
+    _need_meta(fn, L, meta, b + 1)
     lay, met = L.c(), meta.c()
     _check("lynx_kv_deserialize_anchor", load().lynx_kv_deserialize_anchor(
         ctypes.byref(lay), b, t0, n_tokens, _ptr(block_table), _ptr(anchor_buf), _ptr(k_anc),
@@ -399,6 +520,13 @@ def lynx_kv_deserialize_anchor(L: Layout, b: int, t0: int, n_tokens: int, block_
 def lynx_kv_deserialize_residual(L: Layout, b: int, t0: int, n_tokens: int, block_table,
                                  residual_buf, k_anc, v_anc, k_codes, v_codes,
                                  stream=None) -> None:
+    fn = "lynx_kv_deserialize_residual"
+    _need(fn, "block_table", block_table, (b + 1) * L.max_blocks_per_seq * 4)
+    if n_tokens > 0:
+        _need(fn, "residual_buf", residual_buf, lynx_serialized_bytes(L.num_kv_heads, n_tokens)[1])
+    for name, t, rb in (("k_anc", k_anc, 64), ("v_anc", v_anc, 64), ("k_codes", k_codes, 128),
+                        ("v_codes", v_codes, 128)):
+        _need(fn, name, t, L.plane_bytes(rb))
     lay = L.c()
     _check("lynx_kv_deserialize_residual", load().lynx_kv_deserialize_residual(
         ctypes.byref(lay), b, t0, n_tokens, _ptr(block_table), _ptr(residual_buf), _ptr(k_anc),

@@ -256,3 +256,56 @@ def test_hierarchical_codec_validation(lib):
     assert deq(alpha=0.0) == E.LYNX_EINVAL
     assert deq(T=300) == E.LYNX_EINVAL
     assert deq(T=0) == E.LYNX_OK
+
+
+def test_binding_rejects_short_tensors(lib):
+    """The Python binding checks the tensors a call reads or writes against
+    the sizes the layout implies and raises ValueError before the C ABI sees
+    a pointer (host tensors suffice: the check comes first)."""
+    import torch
+
+    from paper_2607_01831_amd import lynx
+    L = _layout(num_kv_heads=2, block_tokens=64, max_blocks_per_seq=1, num_blocks=2, max_tokens=64)
+    B, Hq, T = 2, 4, 64
+    u8 = lambda n: torch.zeros(n, dtype=torch.uint8)
+    planes = [u8(L.plane_bytes(64)) for _ in range(4)]
+    meta = lynx.Meta.empty(L, B, device="cpu")
+    table = torch.arange(B, dtype=torch.int32).view(B, 1)
+    lens = torch.full((B,), T, dtype=torch.int32)
+    k = torch.zeros(T, 2, 128, dtype=torch.bfloat16)
+    bad = [
+        # encode: short K, a sequence past the metadata rows, short planes
+        lambda: lynx.lynx_kv_encode(L, 0, T, table, k[:T - 1], k, *planes, meta),
+        lambda: lynx.lynx_kv_encode(L, 2, T, table, k, k, *planes, meta),
+        lambda: lynx.lynx_kv_encode(L, 0, T, table, k, k, planes[0][:100], *planes[1:], meta),
+        # decode: seq_lens / block_table / q / out / lse shorter than the batch
+        lambda: lynx.lynx_attn_anchor_decode(L, B, Hq, T, lens[:1], table, planes[0], planes[1],
+                                             meta, torch.zeros(B, Hq, 128, dtype=torch.bfloat16),
+                                             torch.zeros(B, Hq, 128, dtype=torch.bfloat16)),
+        lambda: lynx.lynx_attn_anchor_decode(L, B, Hq, T, lens, table[:1], planes[0], planes[1],
+                                             meta, torch.zeros(B, Hq, 128, dtype=torch.bfloat16),
+                                             torch.zeros(B, Hq, 128, dtype=torch.bfloat16)),
+        lambda: lynx.lynx_attn_anchor_decode_noalloc(L, B, Hq, T, lens, table, planes[0], planes[1],
+                                                     meta, torch.zeros(1, Hq, 128, dtype=torch.bfloat16),
+                                                     torch.zeros(B, Hq, 128, dtype=torch.bfloat16)),
+        lambda: lynx.lynx_attn_anchor_decode(L, B, Hq, T, lens, table, planes[0], planes[1], meta,
+                                             torch.zeros(B, Hq, 128, dtype=torch.bfloat16),
+                                             torch.zeros(B, Hq, 128, dtype=torch.bfloat16),
+                                             torch.zeros(B * Hq - 1)),
+        # verify: code planes sized for nibbles, a short draft tail
+        lambda: lynx.lynx_attn_verify(L, B, Hq, 2, T, lens, table, planes[0], planes[1], meta,
+                                      torch.zeros(B, 2, Hq, 128, dtype=torch.bfloat16), None, None,
+                                      torch.zeros(B, 2, Hq, 128, dtype=torch.bfloat16)),
+        lambda: lynx.lynx_attn_verify(L, B, Hq, 2, T, lens, table, u8(L.plane_bytes(128)),
+                                      u8(L.plane_bytes(128)), meta,
+                                      torch.zeros(B, 2, Hq, 128, dtype=torch.bfloat16),
+                                      torch.zeros(B, 1, 2, 128, dtype=torch.bfloat16),
+                                      torch.zeros(B, 2, 2, 128, dtype=torch.bfloat16),
+                                      torch.zeros(B, 2, Hq, 128, dtype=torch.bfloat16)),
+        # split widths: a 2-bit anchor plane sized for nibbles is too short for 6 bits
+        lambda: lynx.lynx_kv_encode_split(L, 6, 0, T, table, k, k, planes[0], planes[1],
+                                          planes[2], planes[3], meta),
+    ]
+    for i, call in enumerate(bad):
+        with pytest.raises(ValueError):
+            call()

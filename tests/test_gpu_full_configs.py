@@ -73,7 +73,8 @@ def run_verify(c, q, kn, vn):
     ws = lynx.workspace(c.L, B, Hq, nq, max_len)
     note(f"full-size verify B={B} k={nq} Hq={Hq} max_len={max_len}")
     lynx.lynx_attn_verify(c.L, B, Hq, nq, max_len, c.lens_dev(), c.table_dev(), c.pool.k_codes,
-                          c.pool.v_codes, c.pool.meta, q.cuda(), kn.cuda(), vn.cuda(), out, ws)
+                          c.pool.v_codes, c.pool.meta, q.cuda(),
+                          None if kn is None else kn.cuda(), None if vn is None else vn.cuda(), out, ws)
     torch.cuda.synchronize()
     return out.float().cpu().numpy()
 
@@ -87,8 +88,16 @@ def oracle_verify(c, q, kn, vn, mask):
     kc = oracle.merge(c.planes["k_anc"], c.planes["k_res"])
     vc = oracle.merge(c.planes["v_anc"], c.planes["v_res"])
     out, _ = oracle.verify(c.OL, q.shape[2], np.array(c.lens), c.table.numpy(), kc, vc, c.meta,
-                           bits(q), bits(kn), bits(vn), unit_mask=mask)
+                           bits(q), None if kn is None else bits(kn), None if vn is None else bits(vn),
+                           unit_mask=mask)
     return out
+
+
+def vnmse(o_hat, o):
+    """E ||o_hat - o||^2 / ||o||^2 over the rows of [..][128] arrays."""
+    o_hat = np.asarray(o_hat, np.float64).reshape(-1, 128)
+    o = np.asarray(o, np.float64).reshape(-1, 128)
+    return float((((o_hat - o) ** 2).sum(axis=1) / (o ** 2).sum(axis=1)).mean())
 
 
 def test_llama3_8b_32k_layer():
@@ -130,6 +139,24 @@ def test_verify_128k():
     outv = run_verify(c, qv, kn, vn)
     refv = oracle_verify(c, qv, kn, vn, mask)
     check_units(outv, refv, mask, w.G, "128K verify k=8")
+    # the anchor-only decode of draft 0 and the verification of draft 0 over
+    # the merged codes (no tail), each against the oracle; then how far the
+    # anchor-only output is from the full one (what the residual removes),
+    # on the GPU and in the oracle
+    q0 = qv[:, 0].contiguous()
+    out_a, _ = run_decode(c, q0, with_lse=False)
+    ref_a, _ = oracle_decode(c, q0, mask)
+    check_units(out_a, ref_a, mask, w.G, "128K anchor decode of draft 0")
+    q0v = q0.view(1, 1, w.Hq, 128)
+    out_f = run_verify(c, q0v, None, None)[:, 0]
+    ref_f = oracle_verify(c, q0v, None, None, mask)[:, 0]
+    check_units(out_f, ref_f, mask, w.G, "128K verify of draft 0, no tail")
+    heads = [hh for h in np.nonzero(mask[0])[0] for hh in range(h * w.G, (h + 1) * w.G)]
+    dev_gpu = vnmse(out_a[0, heads], out_f[0, heads])
+    dev_ref = vnmse(ref_a[0, heads], ref_f[0, heads])
+    note(f"128K anchor-only vs full, draft 0: vNMSE {dev_gpu:.4g} (oracle {dev_ref:.4g})")
+    assert dev_ref > 0
+    assert abs(dev_gpu - dev_ref) <= 0.1 * dev_ref
 
 
 def test_paged_b16_decode():
