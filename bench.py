@@ -113,11 +113,9 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="run one plain device copy of 640 MiB before the steps (counter calibration)")
     p.add_argument("--summarize-trace", metavar="DIR")
-    p.add_argument("--trace-split", type=int, default=0,
-                   help="with --summarize-trace: report the first N decode calls apart from the rest")
-    p.add_argument("--trace-verify-tail", type=int, default=0,
-                   help="with --summarize-trace: report the last N verify calls apart from the rest")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    p.add_argument("--summarize-copies", metavar="DIR",
+                   help="kernel + memory-copy trace CSVs -> kernels inside each H2D copy")
     p.add_argument("--no-spec-stages", dest="spec_stages", action="store_false",
                    help="skip the decode-with-tail and draft-acceptance stages")
     p.add_argument("--paged-calls", type=int, default=REPS,
@@ -132,6 +130,8 @@ def parse():
                    help="skip the 70B-shaped overlap run (70b-overlap-b4-128k)")
     p.add_argument("--verify-128k-calls", type=int, default=REPS,
                    help="timed verification calls at 128K context (0 skips the stage)")
+    p.add_argument("--no-ceilings", dest="ceilings", action="store_false",
+                   help="skip the plain copy / add stream-rate stage")
     return p.parse_args()
 
 
@@ -174,80 +174,102 @@ def _csv(dirname, suffix):
 
 
 def _short(name: str) -> str:
-    for key in ("anchor_decode_kernel", "attn_combine_kernel", "attn_split_kernel", "verify_kernel",
-                "encode_kernel", "merge_kernel", "copyBuffer"):
+    for key in ("anchor_decode_kernel", "attn_combine_kernel", "verify_kernel", "encode_kernel",
+                "merge_kernel", "copyBuffer", "hencode_kernel", "hdequant_kernel",
+                "deserialize_anchor_kernel", "deserialize_residual_kernel", "merge_split_kernel",
+                "dequant_anchor_split_kernel", "argmax_chunk_kernel", "accept_kernel",
+                "sample_chunk_kernel", "sample_pick_kernel"):
         if key in name:
-            if key == "attn_split_kernel":
-                return "attn_split_kernel<codes>" if "(lynx::KvMode)1" in name else "attn_split_kernel<anchor>"
             return key
+    if "vectorized_elementwise_kernel" in name and "CUDAFunctor_add" in name:
+        return "torch add (uint8)"
     return name.split("(")[0][:60]
 
 
+def _us(r):
+    return (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+
+
+def _grid(r):
+    """Work-items of a dispatch (counter CSVs give Grid_Size, trace CSVs X/Y/Z)."""
+    if r.get("Grid_Size"):
+        return int(r["Grid_Size"])
+    return int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+
+
 def _calls(rows, first):
-    """Pair every `first` dispatch (anchor_decode_kernel or verify_kernel)
-    with the attn_combine_kernel dispatch that follows it: one
-    lynx_attn_anchor_decode or lynx_attn_verify call."""
+    """Every `first` dispatch (anchor_decode_kernel or verify_kernel) with the
+    attn_combine_kernel dispatch right after it on the same queue, if there
+    is one (a fused decode has none): one lynx_attn_* call each."""
     rows = sorted(rows, key=lambda r: int(r["Dispatch_Id"]))
-    calls, pending = [], None
+    nxt = {}
+    for i, r in enumerate(rows):
+        for r2 in rows[i + 1:]:
+            if r2["Queue_Id"] == r["Queue_Id"]:
+                nxt[id(r)] = r2
+                break
+    calls = []
     for r in rows:
-        n = _short(r["Kernel_Name"])
-        if n == first:
-            pending = r
-        elif n == "attn_combine_kernel" and pending is not None:
-            calls.append((pending, r))
-            pending = None
+        if _short(r["Kernel_Name"]) == first:
+            n = nxt.get(id(r))
+            calls.append((r, n if n is not None and _short(n["Kernel_Name"]) == "attn_combine_kernel"
+                          else None))
     return calls
 
 
-def _decode_calls(rows):
-    return _calls(rows, "anchor_decode_kernel")
+def _stats(xs):
+    xs = sorted(xs)
+    n = len(xs)
+    med = xs[n // 2] if n % 2 else 0.5 * (xs[n // 2 - 1] + xs[n // 2])
+    return med, xs[0], xs[-1], sum(xs) / n
 
 
-def _print_calls(what, label, cs):
-    first = "anchor_decode_kernel" if what == "anchor-decode" else "verify_kernel"
-    sk = [(int(a["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, _ in cs]
-    comb = [(int(b["End_Timestamp"]) - int(b["Start_Timestamp"])) / 1e3 for _, b in cs]
-    span = [(int(b["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3 for a, b in cs]
-    n = len(cs)
-    print(f"{what} calls ({label}): {n}; per call: {first} {sum(sk) / n:.2f} us + "
-          f"attn_combine_kernel {sum(comb) / n:.2f} us = {(sum(sk) + sum(comb)) / n:.2f} us of "
-          f"kernel time; first start to last end {sum(span) / n:.2f} us")
-
-
-def summarize_trace(dirname, split=0, verify_tail=0):
+def summarize_trace(dirname):
+    """Kernel durations of a rocprofv3 --kernel-trace run, per kernel and grid
+    size (work-items), and per API call (decode or verify kernel plus its
+    combine kernel, when there is one)."""
     rows = _csv(dirname, "kernel_trace.csv")
     by = {}
     for r in rows:
-        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-        by.setdefault(_short(r["Kernel_Name"]), []).append(d)
-    print("| kernel | calls | avg us | min us | max us |\n|---|---|---|---|---|")
-    for n, ds in sorted(by.items(), key=lambda kv: -sum(kv[1])):
-        print(f"| {n} | {len(ds)} | {sum(ds) / len(ds):.2f} | {min(ds):.2f} | {max(ds):.2f} |")
-    calls = _decode_calls(rows)
-    parts = [("all", calls)] if not split else [(f"calls 1..{split}", calls[:split]),
-                                                 (f"calls {split + 1}..{len(calls)}", calls[split:])]
+        by.setdefault((_short(r["Kernel_Name"]), _grid(r)), []).append(_us(r))
+    print("| kernel | grid (work-items) | dispatches | median us | min us | max us | mean us |")
+    print("|---|---|---|---|---|---|---|")
+    for (n, g), ds in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        med, lo, hi, mean = _stats(ds)
+        print(f"| {n} | {g} | {len(ds)} | {med:.2f} | {lo:.2f} | {hi:.2f} | {mean:.2f} |")
     print()
-    for label, cs in parts:
-        if cs:
-            _print_calls("anchor-decode", label, cs)
-    vcalls = _calls(rows, "verify_kernel")
-    if verify_tail and len(vcalls) > verify_tail:
-        _print_calls("verify", f"calls 1..{len(vcalls) - verify_tail}", vcalls[:-verify_tail])
-        _print_calls("verify", f"last {verify_tail}", vcalls[-verify_tail:])
-    elif vcalls:
-        _print_calls("verify", "all", vcalls)
+    print("| call | grid of the first kernel | calls | first kernel median us | combine median us | "
+          "call (first start to last end) median us |")
+    print("|---|---|---|---|---|---|")
+    for first in ("anchor_decode_kernel", "verify_kernel"):
+        groups = {}
+        for a, b in _calls(rows, first):
+            groups.setdefault(_grid(a), []).append((a, b))
+        for g, cs in sorted(groups.items()):
+            k = _stats([_us(a) for a, _ in cs])[0]
+            comb = [_us(b) for _, b in cs if b is not None]
+            c = f"{_stats(comb)[0]:.2f}" if comb else "(fused)"
+            span = _stats([(int((b or a)["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3
+                           for a, b in cs])[0]
+            print(f"| {first.replace('_kernel', '')} | {g} | {len(cs)} | {k:.2f} | {c} | {span:.2f} |")
 
 
 def summarize_pmc(fetch_dir, write_dir):
+    """HBM bytes per dispatch from two rocprofv3 --pmc runs (FETCH_SIZE, then
+    WRITE_SIZE, KiB per dispatch) of a run with --copy-calibration: each
+    counter scaled by what it reads for the plain copy of known size.  Per
+    kernel and grid size, and per 32K-layer anchor-decode call (the
+    roofline's kernel: 8 kv heads x 32768 tokens, one round of 512
+    workgroups)."""
     def per_dispatch(dirname, counter):
-        return [(r, float(r["Counter_Value"])) for r in _csv(dirname, "counter_collection.csv")
-                if r["Counter_Name"] == counter]
+        return {int(r["Dispatch_Id"]): (r, float(r["Counter_Value"]))
+                for r in _csv(dirname, "counter_collection.csv") if r["Counter_Name"] == counter}
 
     fetch = per_dispatch(fetch_dir, "FETCH_SIZE")
     write = per_dispatch(write_dir, "WRITE_SIZE")
 
     def copy_kib(table):
-        cands = [v for r, v in table if _short(r["Kernel_Name"]) == "copyBuffer"]
+        cands = [v for r, v in table.values() if _short(r["Kernel_Name"]) == "copyBuffer"]
         if not cands:
             raise SystemExit("no copy kernel in the counter run (use --copy-calibration)")
         return max(cands)
@@ -255,24 +277,86 @@ def summarize_pmc(fetch_dir, write_dir):
     known_kib = COPY_CALIBRATION_BYTES / 1024
     f_fetch = known_kib / copy_kib(fetch)
     f_write = known_kib / copy_kib(write)
-
-    def decode_kib(table):
-        vals = {int(r["Dispatch_Id"]): v for r, v in table}
-        calls = _decode_calls([r for r, _ in table])
-        per = [vals[int(a["Dispatch_Id"])] + vals[int(b["Dispatch_Id"])] for a, b in calls]
-        return sum(per) / len(per), len(per)
-
-    fk, nf = decode_kib(fetch)
-    wk, nw = decode_kib(write)
-    traffic = fk * 1024 * f_fetch + wk * 1024 * f_write
     print(f"copy calibration: a plain copy of {COPY_CALIBRATION_BYTES} bytes reads FETCH_SIZE "
           f"{copy_kib(fetch):.0f} KiB and WRITE_SIZE {copy_kib(write):.0f} KiB; scale factors "
           f"fetch {f_fetch:.4f}, write {f_write:.4f}")
-    print(f"anchor-decode calls measured: {nf} (FETCH), {nw} (WRITE)")
-    print(f"per call (anchor_decode_kernel + attn_combine_kernel): FETCH_SIZE {fk:.0f} KiB, "
-          f"WRITE_SIZE {wk:.0f} KiB")
-    print(f"kernel_sources_sha256: {decode_sources_hash()}")
-    print(f"traffic_bytes_per_call: {int(round(traffic))}")
+    print()
+
+    def grouped(table, f):
+        g = {}
+        for r, v in table.values():
+            g.setdefault((_short(r["Kernel_Name"]), _grid(r)), []).append(v * 1024 * f)
+        return g
+
+    gf, gw = grouped(fetch, f_fetch), grouped(write, f_write)
+    print("| kernel | grid (work-items) | dispatches | read MB per dispatch | written MB per dispatch |")
+    print("|---|---|---|---|---|")
+    for key in sorted(gf, key=lambda k: -sum(gf[k])):
+        if key[0] == "copyBuffer" or key not in gw:
+            continue
+        rd = sum(gf[key]) / len(gf[key]) / 1e6
+        wr = sum(gw[key]) / len(gw[key]) / 1e6
+        print(f"| {key[0]} | {key[1]} | {len(gf[key])} | {rd:.2f} | {wr:.2f} |")
+    # one 32K-layer decode call: the decode kernel with the 32K layer's grid
+    # (and its combine, when the call has one)
+    rows_f = [r for r, _ in fetch.values()]
+    grid_32k = 512 * 256
+    per = []
+    for a, b in _calls(rows_f, "anchor_decode_kernel"):
+        if _grid(a) != grid_32k:
+            continue
+        ids = [int(a["Dispatch_Id"])] + ([int(b["Dispatch_Id"])] if b is not None else [])
+        if all(i in write for i in ids):
+            per.append(sum(fetch[i][1] * 1024 * f_fetch + write[i][1] * 1024 * f_write for i in ids))
+    print()
+    if per:
+        print(f"32K-layer anchor-decode calls measured: {len(per)}")
+        print(f"kernel_sources_sha256: {decode_sources_hash()}")
+        print(f"traffic_bytes_per_call: {int(round(sum(per) / len(per)))}")
+
+
+def summarize_copies(dirname):
+    """For every host-to-device copy longer than 1 ms in a rocprofv3
+    --kernel-trace --memory-copy-trace run: the kernels that ran while it
+    was in flight (count, and time inside the copy's window)."""
+    kt = _csv(dirname, "kernel_trace.csv")
+    mc = _csv(dirname, "memory_copy_trace.csv")
+    big = [r for r in mc if r["Direction"].endswith("HOST_TO_DEVICE")
+           and int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) > 1_000_000]
+    print("| H2D copy | duration us | kernels inside its window (kernel [grid] x dispatches: us inside) |")
+    print("|---|---|---|")
+    for i, r in enumerate(big):
+        s0, e0 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        inside = {}
+        for k in kt:
+            ov = min(int(k["End_Timestamp"]), e0) - max(int(k["Start_Timestamp"]), s0)
+            if ov > 0:
+                c = inside.setdefault((_short(k["Kernel_Name"]), _grid(k)), [0, 0.0])
+                c[0] += 1
+                c[1] += ov / 1e3
+        desc = "; ".join(f"{n} [{g}] x{c}: {t:.1f}" for (n, g), (c, t) in
+                         sorted(inside.items(), key=lambda kv: -kv[1][1])) or "none"
+        print(f"| {i + 1} | {(e0 - s0) / 1e3:.1f} | {desc} |")
+
+
+def stream_ceilings(dev):
+    """Practical HBM stream rates on this part, with torch's own kernels over
+    buffers larger than the 256 MB last-level cache: a device-to-device copy
+    (reads and writes one byte per byte, as the merge does) and a uint8 add
+    c = a + b (reads two bytes per byte written, as the encode does); median
+    over REPS calls, bytes read + written per second."""
+    import torch
+
+    n = 512 << 20
+    a = torch.ones(n, dtype=torch.uint8, device=dev)
+    b = torch.ones(n, dtype=torch.uint8, device=dev)
+    c = torch.empty(n, dtype=torch.uint8, device=dev)
+    copy = summary(call_samples(lambda: c.copy_(a)))
+    add = summary(call_samples(lambda: torch.add(a, b, out=c)))
+    del a, b, c
+    return {"stream_ceilings": {
+        "copy_512MiB_us": copy["median"], "copy_GBps": round(2 * n / (copy["median"] * 1e-6) / 1e9, 1),
+        "add_u8_512MiB_us": add["median"], "add_u8_GBps": round(3 * n / (add["median"] * 1e-6) / 1e9, 1)}}
 
 
 # --------------------------------------------------------------- CPU baseline --
@@ -904,10 +988,13 @@ def cpu_baseline(w, layer_inputs, n_dec=8, n_enc=4, n_ver=2):
 def main():
     args = parse()
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.trace_split, args.trace_verify_tail)
+        summarize_trace(args.summarize_trace)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
+        return
+    if args.summarize_copies:
+        summarize_copies(args.summarize_copies)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no "
@@ -1022,6 +1109,7 @@ def main():
 
     st_dec_alone = summary(call_samples(decode_layers, n=max(args.steps, 1), warm=1, per=n_layers))
 
+    ceil = stream_ceilings(dev) if args.ceilings else None
     ver128 = verify_128k(args.verify_128k_calls, dev) if args.verify_128k_calls > 0 else None
     paged = paged_decode_stage(args.paged_calls, dev) if args.paged_calls > 0 else None
     ovl = overlap_70b_stage(dev) if args.overlap_70b else None
@@ -1125,6 +1213,7 @@ def main():
             "verify_us_per_layer": round(ver_us, 2),
             "verify_GBps": round(ver_gbps, 2),
             "residual_h2d_GBps": round(h2d_gbps, 2),
+            **(ceil or {}),
             **(ver128 or {}),
             **(paged or {}),
             **(ovl or {}),
@@ -1137,7 +1226,8 @@ def main():
             "setup_s": round(t_setup, 1),
         },
         "roofline": {
-            "kernel": "one lynx_attn_anchor_decode call (anchor_decode_kernel + attn_combine_kernel)",
+            "kernel": "anchor_decode_kernel: one launch per lynx_attn_anchor_decode call on a 32K layer "
+                      "(the split merge runs in the same launch)",
             "bound": "hbm",
             "achieved": round(per_call_bytes / per_call_s / 1e9, 2),
             "peak": HBM_PEAK_GBPS,

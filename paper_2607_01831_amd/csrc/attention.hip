@@ -49,8 +49,7 @@ __device__ __forceinline__ void unpack8_bf16(const uint4 &u, float *x) {
     x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
 }
 
-// Eight 4-bit values (nibble j = element j) -> floats.
-// Eight bytes -> floats.
+// fp32 -> BF16 bits, round to nearest even (NaN -> a quiet NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
     if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN

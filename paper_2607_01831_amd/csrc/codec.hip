@@ -11,6 +11,7 @@
 // The fp32 arithmetic that decides a code is spelled out operation by
 // operation (sub, mul, round-half-even, clamp; one IEEE division per group)
 // so that every code is the one the definition gives.
+#include "lane_ops.h"
 #include "lynx_internal.h"
 
 #include <float.h>
@@ -48,58 +49,8 @@ __device__ __forceinline__ void group_params(float mn, float mx, float &zero, fl
     zero = mn;
 }
 
-// Min / max without the NaN canonicalisation the compiler adds around
-// fminf / fmaxf (non-finite inputs give unspecified codes).
-__device__ __forceinline__ float vmin3(float a, float b, float c) {
-    float r;
-    asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-    return r;
-}
-__device__ __forceinline__ float vmax3(float a, float b, float c) {
-    float r;
-    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-    return r;
-}
-__device__ __forceinline__ float vmin(float a, float b) {
-    float r;
-    asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
-__device__ __forceinline__ float vmax(float a, float b) {
-    float r;
-    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-// over the 16 lanes of a row
-__device__ __forceinline__ float row16_min(float v) {
-    v = vmin(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
-    v = vmin(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
-    v = vmin(v, dpp<0x141>(v));  // row_half_mirror
-    return vmin(v, dpp<0x140>(v));  // row_mirror
-}
-__device__ __forceinline__ float row16_max(float v) {
-    v = vmax(v, dpp<0xB1>(v));
-    v = vmax(v, dpp<0x4E>(v));
-    v = vmax(v, dpp<0x141>(v));
-    return vmax(v, dpp<0x140>(v));
-}
-// over lanes l, l^16, l^32, l^48
-__device__ __forceinline__ float rows_min(float v) {
-    auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
-    v = vmin(__int_as_float(r[0]), __int_as_float(r[1]));
-    r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
-    return vmin(__int_as_float(r[0]), __int_as_float(r[1]));
-}
-__device__ __forceinline__ float rows_max(float v) {
-    auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
-    v = vmax(__int_as_float(r[0]), __int_as_float(r[1]));
-    r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
-    return vmax(__int_as_float(r[0]), __int_as_float(r[1]));
-}
+// (Min / max and the cross-lane reductions come from lane_ops.h; non-finite
+// inputs give unspecified codes.)
 
 // Eight values -> eight codes clamp(rint((x - zero) * inv), 0, 255), then
 // the anchor word (nibble j = code_j >> 4) and the residual word (nibble j =
@@ -237,8 +188,8 @@ __global__ __launch_bounds__(kEncodeThreads, 4) void encode_kernel(
         for (int i = 0; i < 8; ++i) {
             float x[8];
             unpack8(raw[i], x);
-            float mn = vmin3(vmin3(x[0], x[1], x[2]), vmin3(x[3], x[4], x[5]), vmin(x[6], x[7]));
-            float mx = vmax3(vmax3(x[0], x[1], x[2]), vmax3(x[3], x[4], x[5]), vmax(x[6], x[7]));
+            float mn = fmin3(fmin3(x[0], x[1], x[2]), fmin3(x[3], x[4], x[5]), fmin2(x[6], x[7]));
+            float mx = fmax3(fmax3(x[0], x[1], x[2]), fmax3(x[3], x[4], x[5]), fmax2(x[6], x[7]));
             mn = row16_min(mn);
             mx = row16_max(mx);
             float scale;
@@ -279,17 +230,17 @@ __global__ __launch_bounds__(kEncodeThreads, 4) void encode_kernel(
         for (int i = 0; i < 8; ++i) unpack8(raw[i], x[i]);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            kmin[j] = vmin3(vmin3(x[0][j], x[1][j], x[2][j]), vmin3(x[3][j], x[4][j], x[5][j]),
-                            vmin(x[6][j], x[7][j]));
-            kmax[j] = vmax3(vmax3(x[0][j], x[1][j], x[2][j]), vmax3(x[3][j], x[4][j], x[5][j]),
-                            vmax(x[6][j], x[7][j]));
+            kmin[j] = fmin3(fmin3(x[0][j], x[1][j], x[2][j]), fmin3(x[3][j], x[4][j], x[5][j]),
+                            fmin2(x[6][j], x[7][j]));
+            kmax[j] = fmax3(fmax3(x[0][j], x[1][j], x[2][j]), fmax3(x[3][j], x[4][j], x[5][j]),
+                            fmax2(x[6][j], x[7][j]));
         }
     }
     // lanes m, m+16, m+32, m+48 of a wave hold the same channels
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        kmin[j] = rows_min(kmin[j]);
-        kmax[j] = rows_max(kmax[j]);
+        kmin[j] = min_kg(kmin[j]);
+        kmax[j] = max_kg(kmax[j]);
     }
     if ((tid & 63) < 16) {
 #pragma unroll
@@ -301,8 +252,8 @@ __global__ __launch_bounds__(kEncodeThreads, 4) void encode_kernel(
     __syncthreads();
     if (tid < kHeadDim) {
         const int d = tid;
-        const float mn = vmin(vmin(s_min[0][d], s_min[1][d]), vmin(s_min[2][d], s_min[3][d]));
-        const float mx = vmax(vmax(s_max[0][d], s_max[1][d]), vmax(s_max[2][d], s_max[3][d]));
+        const float mn = fmin2(fmin2(s_min[0][d], s_min[1][d]), fmin2(s_min[2][d], s_min[3][d]));
+        const float mx = fmax2(fmax2(s_max[0][d], s_max[1][d]), fmax2(s_max[2][d], s_max[3][d]));
         float zero, scale, inv;
         group_params(mn, mx, zero, scale, inv);
         s_zero[d] = zero;

@@ -30,8 +30,9 @@ __device__ __forceinline__ float sum_kg(float v) {
     r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
     return __int_as_float(r[0]) + __int_as_float(r[1]);
 }
-// Maximum of values that are finite or -inf (never NaN), without the NaN
-// canonicalisation the compiler adds around fmaxf.
+// Minimum / maximum without the NaN canonicalisation the compiler adds around
+// fminf / fmaxf (for values that are never NaN, or where a NaN's result does
+// not matter).
 __device__ __forceinline__ float fmax2(float a, float b) {
     float r;
     asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
@@ -41,6 +42,28 @@ __device__ __forceinline__ float fmax3(float a, float b, float c) {
     float r;
     asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
     return r;
+}
+__device__ __forceinline__ float fmin2(float a, float b) {
+    float r;
+    asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ float fmin3(float a, float b, float c) {
+    float r;
+    asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+__device__ __forceinline__ float row16_min(float v) {  // over the 16 lanes of a row
+    v = fmin2(v, dpp<0xB1>(v));
+    v = fmin2(v, dpp<0x4E>(v));
+    v = fmin2(v, dpp<0x141>(v));
+    return fmin2(v, dpp<0x140>(v));
+}
+__device__ __forceinline__ float min_kg(float v) {  // over lanes l, l^16, l^32, l^48
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
+    v = fmin2(__int_as_float(r[0]), __int_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
+    return fmin2(__int_as_float(r[0]), __int_as_float(r[1]));
 }
 __device__ __forceinline__ float row16_max(float v) {  // over the 16 lanes of a row
     v = fmax2(v, dpp<0xB1>(v));

@@ -3,9 +3,8 @@
 // What it computes (Sec. 4.3; attention of Sec. 2): the k draft queries of a
 // sequence attend, in one pass, over the merged 8-bit cache, with K and V
 // reconstructed as zero + code * scale.  This kernel covers the context
-// tokens.  The drafts' own BF16 K/V (the causal tail) form one more split,
-// handled by the vector kernel of attention.hip, and the combine kernel
-// merges all splits.
+// tokens; the combine kernel of attention.hip merges its splits and attends
+// the drafts' own BF16 K/V (the causal tail) as one more partial.
 //
 // Why matrix cores: with k * G query rows per kv head (32 for 8 drafts and
 // G = 4) every context token costs 2 x 128 x 32 multiply-adds against 272
