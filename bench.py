@@ -114,6 +114,10 @@ def parse():
                    help="run one plain device copy of 640 MiB before the steps (counter calibration)")
     p.add_argument("--summarize-trace", metavar="DIR")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    p.add_argument("--summarize-conditions", nargs="+", metavar="DIR",
+                   help="per-condition counters of the transport-interference stage from --pmc runs")
+    p.add_argument("--transport-trials", type=int, default=8,
+                   help="trials per condition of the transport-interference stage (0: skip it)")
     p.add_argument("--summarize-copies", metavar="DIR",
                    help="kernel + memory-copy trace CSVs -> kernels inside each H2D copy")
     p.add_argument("--no-spec-stages", dest="spec_stages", action="store_false",
@@ -337,6 +341,81 @@ def summarize_copies(dirname):
         desc = "; ".join(f"{n} [{g}] x{c}: {t:.1f}" for (n, g), (c, t) in
                          sorted(inside.items(), key=lambda kv: -kv[1][1])) or "none"
         print(f"| {i + 1} | {(e0 - s0) / 1e3:.1f} | {desc} |")
+
+
+TRANSPORT_CONDITIONS = ("alone", "h2d running", "after encode", "after encode, h2d running")
+
+
+def transport_interference(encode_all, decode_all, start_h2d, trials):
+    """The 32 decode calls in four conditions, interleaved trial by trial:
+    alone; with the residual H2D running on the side stream; right after the
+    encode of every layer; right after the encode with the H2D running (the
+    step's own order).  Before each decode run a marker kernel (a fill of
+    (c + 1) << 16 int16 values) names condition c for a counter run.  Returns
+    us per call (median, min, max) per condition."""
+    import torch
+
+    main_s = torch.cuda.current_stream()
+    res = {c: [] for c in TRANSPORT_CONDITIONS}
+    for t in range(trials + 1):
+        for c, name in enumerate(TRANSPORT_CONDITIONS):
+            torch.cuda.synchronize()
+            if c >= 2:
+                encode_all()
+            if c in (1, 3):
+                done = torch.cuda.Event()
+                done.record(main_s)
+                start_h2d(done)
+            torch.full(((c + 1) << 16,), c, dtype=torch.int16, device=main_s.device)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(main_s)
+            n = decode_all()
+            b.record(main_s)
+            torch.cuda.synchronize()
+            if t > 0:  # the first round warms up
+                res[name].append(a.elapsed_time(b) * 1e3 / n)
+    return {name: summary(v) for name, v in res.items()}
+
+
+def summarize_conditions(dirs):
+    """Counters of the anchor-decode dispatches of a --pmc run per condition of
+    the transport-interference stage (the condition is named by the int16 fill
+    before its decode run), mean per dispatch; then the derived latencies."""
+    per = {}
+    for d in dirs:
+        rows = sorted(_csv(d, "counter_collection.csv"), key=lambda r: int(r["Dispatch_Id"]))
+        disp = {}
+        for r in rows:
+            disp.setdefault(int(r["Dispatch_Id"]), []).append(r)
+        markers = sorted({_grid(rs[0]) for rs in disp.values()
+                          if "FillFunctor<short>" in rs[0]["Kernel_Name"]})
+        if len(markers) != len(TRANSPORT_CONDITIONS):
+            raise SystemExit(f"{d}: expected {len(TRANSPORT_CONDITIONS)} marker sizes, found {markers}")
+        cond = None
+        for i in sorted(disp):
+            rs = disp[i]
+            name = rs[0]["Kernel_Name"]
+            if "FillFunctor<short>" in name:
+                cond = markers.index(_grid(rs[0]))
+            elif cond is not None and _short(name) == "anchor_decode_kernel" and _grid(rs[0]) == 131072:
+                for r in rs:
+                    per.setdefault(r["Counter_Name"], {}).setdefault(cond, []).append(
+                        float(r["Counter_Value"]))
+                per.setdefault("duration_us", {}).setdefault(cond, []).append(_us(rs[0]))
+    names = sorted(per)
+    print("| counter (mean per 32K decode dispatch) | " + " | ".join(TRANSPORT_CONDITIONS) + " |")
+    print("|---|" + "---|" * len(TRANSPORT_CONDITIONS))
+    mean = lambda xs: sum(xs) / len(xs) if xs else float("nan")
+    for n in names:
+        print(f"| {n} | " + " | ".join(f"{mean(per[n].get(c, [])):.1f}"
+                                      for c in range(len(TRANSPORT_CONDITIONS))) + " |")
+    for num, den, label in (("TCC_EA0_RDREQ_LEVEL_sum", "TCC_EA0_RDREQ_sum", "L2 -> memory read latency (cycles)"),
+                            ("TCC_EA0_WRREQ_LEVEL_sum", "TCC_EA0_WRREQ_sum", "L2 -> memory write latency (cycles)"),
+                            ("TCP_TCC_READ_REQ_LATENCY_sum", "TCP_TCC_READ_REQ_sum", "L1 -> L2 read latency (cycles)")):
+        if num in per and den in per:
+            print(f"| {label} | " + " | ".join(
+                f"{mean(per[num].get(c, [])) / max(mean(per[den].get(c, [])), 1e-9):.0f}"
+                for c in range(len(TRANSPORT_CONDITIONS))) + " |")
 
 
 def stream_ceilings(dev):
@@ -993,6 +1072,9 @@ def main():
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
         return
+    if args.summarize_conditions:
+        summarize_conditions(args.summarize_conditions)
+        return
     if args.summarize_copies:
         summarize_copies(args.summarize_copies)
         return
@@ -1109,6 +1191,22 @@ def main():
 
     st_dec_alone = summary(call_samples(decode_layers, n=max(args.steps, 1), warm=1, per=n_layers))
 
+    def encode_layers():
+        for l in range(n_layers):
+            pools[l].encode(0, T, table, K[l], V[l])
+
+    def start_h2d(after):
+        side.wait_event(after)
+        with torch.cuda.stream(side):
+            recv_k.copy_(host_k, non_blocking=True)
+            recv_v.copy_(host_v, non_blocking=True)
+
+    def decode_counted():
+        decode_layers()
+        return n_layers
+
+    transport = (transport_interference(encode_layers, decode_counted, start_h2d, args.transport_trials)
+                 if args.transport_trials > 0 else None)
     ceil = stream_ceilings(dev) if args.ceilings else None
     ver128 = verify_128k(args.verify_128k_calls, dev) if args.verify_128k_calls > 0 else None
     paged = paged_decode_stage(args.paged_calls, dev) if args.paged_calls > 0 else None
@@ -1222,6 +1320,7 @@ def main():
             **(split or {}),
             **spec,
             "decode_hidden_behind_h2d": round(overlap, 3),
+            **({"anchor_decode_us_per_layer_by_condition": transport} if transport else {}),
             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
             "setup_s": round(t_setup, 1),
         },
