@@ -29,8 +29,8 @@
 // Wavefront w owns the groups w, w + 4, ... of the split: it folds each
 // group's K scales into its own MFMA operand lanes of the query (registers)
 // and attends the group's four 32-token tiles with its own online softmax,
-// so the loop has no barrier.  Tiles stream into a private 3-slot LDS ring
-// by global-to-LDS copies, two tiles ahead of the one being attended (no
+// so the loop has no barrier.  Tiles stream into a private 2-slot LDS ring
+// by global-to-LDS copies, one tile ahead of the one being attended (no
 // registers held by loads in flight), each with its V metadata; a group's K
 // metadata rides with its first tile.  At the end the wavefronts are merged
 // through LDS into one partial (max, sum, output) per head.
@@ -88,8 +88,11 @@ __device__ __forceinline__ u32x4_t nibbles_to_bf16(uint32_t w) {
 }
 
 // Ring slot of one tile: K rows (32 x 64 B), V rows (32 x 64 B), then the
-// tile's V scales [32] and zeros [32].
-constexpr int kDepth = 3;
+// tile's V scales [32] and zeros [32].  Two slots per wavefront: a third
+// (two tiles ahead) puts more requests in flight at the start, and every
+// wavefront's first tile arrives later (32K layer 15.3 -> 15.8 us per call,
+// paged batch 148 -> 154 us, 70B batch 114.7 -> 115.9 us).
+constexpr int kDepth = 2;
 constexpr int kPlaneTile = kTile * kNibbleRow;           // 2 KB
 constexpr int kVMetaOff = 2 * kPlaneTile;
 constexpr int kSlotBytes = kVMetaOff + 2 * kTile * 4;    // 4.25 KB
@@ -305,7 +308,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
         return;
     }
 
-    // LDS: 56-60 KB, two workgroups per CU; the epilogue reuses the ring
+    // LDS: 39-43 KB, two workgroups per CU; the epilogue reuses the ring
     __shared__ __attribute__((aligned(16))) uint8_t s_ring[kWaves * kDepth * kSlotBytes];
     __shared__ __attribute__((aligned(16))) uint8_t s_km[kWaves][kKMetaBytes];
     __shared__ __attribute__((aligned(16))) uint8_t s_q[GP * kHeadDim * 2];  // BF16 query rows
@@ -579,7 +582,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_decode_kernel(DecodeArgs a
     // wavefront's first tile and stays fixed, so the loop carries no rescale.
     // Weights of later, larger scores exceed 1; if any sum leaves the safe
     // range the wavefront redoes its tiles below with a running maximum.
-    // Two tiles are in flight while one is attended; no barriers.
+    // The next tile is in flight while one is attended; no barriers.
     // copies of a tile at position c of its group: 5, and 6 for a group's first
     auto copies_at = [](int c) { return (c & 3) == 0 ? 6 : 5; };
     static_assert(kDepth - 1 <= 4, "the ring reaches at most into the next group");
