@@ -109,7 +109,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--layers", type=int, default=None, help="override layer count (testing only)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=8)
+    p.add_argument("--cpu-layers", type=int, default=24,
+                   help="layers of the CPU oracle's decode sample (encode and merge: half, verify: a quarter)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run one plain device copy of 640 MiB before the steps (counter calibration)")
     p.add_argument("--summarize-trace", metavar="DIR")
@@ -1058,7 +1059,8 @@ def cpu_baseline(w, layer_inputs, n_dec=8, n_enc=4, n_ver=2):
             "sample": f"fp64 oracle on the same seeded inputs, {T} tokens, all {Hkv} kv heads: "
                       f"anchor decode of {n_dec} of {w.layers} layers on {threads} threads "
                       f"({t['decode']:.2f} s); also encode and merge of {n_enc} layers (one "
-                      f"thread) and verification of k={w.drafts} drafts of {n_ver} layers",
+                      f"thread, {t['encode'] + t['merge']:.2f} s) and verification of k={w.drafts} drafts "
+                      f"of {n_ver} layers ({t['verify']:.2f} s)",
             "steps": steps, "host": host_cpu()}
 
 
@@ -1343,8 +1345,8 @@ def main():
             return (inputs.kv(w, "k", layer=l), inputs.kv(w, "v", layer=l),
                     inputs.queries(w, layer=l), inputs.queries(w, layer=l, step=1, nq=nq), kn, vn)
         nl = min(args.cpu_layers, n_layers)
-        result["cpu_baseline"] = cpu_baseline(w, layer_inputs, n_dec=nl, n_enc=min(4, nl),
-                                              n_ver=min(2, nl))
+        result["cpu_baseline"] = cpu_baseline(w, layer_inputs, n_dec=nl, n_enc=max(1, nl // 2),
+                                              n_ver=max(1, nl // 4))
     print(json.dumps(result), flush=True)
 
 

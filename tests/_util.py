@@ -14,12 +14,16 @@ HEAD_DIM = 128
 ATOL = 2e-2
 RTOL = 1e-2
 
-# Log-sum-exp (natural log) tolerance, an auxiliary output: the matrix-core
-# decode carries the folded query 16 q s as bf16 hi + lo (relative error
-# about 2^-18) against nibble operands 128 + a, so one score term of size
-# 16 |q s| * 143 is off by about 2^-18 of that; over 128 dims and the
-# 1/sqrt(128) factor this stays below 2e-3 in natural-log units for the
-# value ranges of these tests (|q s| <= 0.5).
+# Log-sum-exp (natural log) tolerance, an auxiliary output.  A caller uses the
+# lse to merge this attention with another partial one; an error e in it
+# scales that partial's weight by exp(e), so the outputs' relative tolerance
+# of 1e-2 corresponds to |d lse| <= ln(1.01), about 1e-2.  The matrix-core
+# decode carries the folded query 16 c q s as bf16 hi + lo (relative error at
+# most 2^-18) against operands 128 + a <= 143, so a score term is off by at
+# most 16 c |q s| 143 2^-18 (log2 units, c = log2(e) / sqrt(128)): 5.6e-4 at
+# |q s| = 0.5, about 4.4e-3 in natural-log units over 128 dims of random sign.
+# The inputs here have |q s| near 0.03 (0.3 on outlier channels), and the
+# check below, tighter than the contract's 1e-2, holds with room.
 LSE_ATOL = 2e-3
 LSE_RTOL = 1e-4
 
