@@ -67,6 +67,9 @@ def _load():
     lib.oracle_merge_split.restype = I
     lib.oracle_dequant_anchor_split.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P]
     lib.oracle_dequant_anchor_split.restype = I
+    lib.oracle_anchor_decode_split.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P,
+                                               P, P, P, P, I]
+    lib.oracle_anchor_decode_split.restype = I
     lib.oracle_accept_sample.argtypes = [I, I, I, P, P, P, P, P, P]
     lib.oracle_accept_sample.restype = I
     lib.oracle_hsplit.argtypes = [I, I, I, IP, IP]
@@ -571,3 +574,27 @@ def dequant_anchor_split(A: int, L: Layout, b: int, T: int, block_table: np.ndar
     if rc != 0:
         raise ValueError(f"oracle_dequant_anchor_split rejected its arguments ({rc})")
     return k_out, v_out
+
+
+def anchor_decode_split(A: int, L: Layout, Hq: int, seq_lens: np.ndarray, block_table: np.ndarray,
+                        k_anc: np.ndarray, v_anc: np.ndarray, meta: Meta, q_bits: np.ndarray,
+                        unit_mask: np.ndarray | None = None, nthreads: int | None = None):
+    """One query per sequence (q_bits uint16 [B][Hq][128]) over the A-bit
+    anchors of a split width (rows of 16 A bytes), each standing for code
+    2^R a + (2^R - 1) / 2 (R = 8 - A).  Returns (out fp64 [B][Hq][128],
+    lse fp64 [B][Hq]); units left out by unit_mask come back as NaN."""
+    seq_lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    B = seq_lens.size
+    q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
+    assert q_bits.shape == (B, Hq, HEAD_DIM)
+    out = np.full((B, Hq, HEAD_DIM), np.nan)
+    lse = np.full((B, Hq), np.nan)
+    mask = None if unit_mask is None else np.ascontiguousarray(unit_mask, dtype=np.uint8)
+    bt_arr = np.ascontiguousarray(block_table, dtype=np.int32)
+    rc = _load().oracle_anchor_decode_split(
+        A, L.Hkv, L.bt, L.max_blocks, L.max_tokens, B, Hq, _ptr(seq_lens), _ptr(bt_arr),
+        _ptr(k_anc), _ptr(v_anc), _ptr(meta.k_scale), _ptr(meta.k_zero), _ptr(meta.v_scale),
+        _ptr(meta.v_zero), _ptr(q_bits), _ptr(out), _ptr(lse), _ptr(mask), nthreads or default_threads())
+    if rc != 0:
+        raise ValueError(f"oracle_anchor_decode_split rejected its arguments ({rc})")
+    return out, lse

@@ -26,7 +26,9 @@
  *              parallel verification pass of k draft queries over the merged
  *              cache, causal among the drafts (Sec. 4.3); the decode may also
  *              attend the BF16 tokens generated since the context arrived
- *              (the speculative decoder's own KV, Sec. 4.2-4.3).
+ *              (the speculative decoder's own KV, Sec. 4.2-4.3);
+ *              the decode over the A-bit anchors of the other split widths
+ *              (Sec. 8) as well.
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   - K is grouped per channel over 128 consecutive tokens, V per token over
@@ -227,7 +229,12 @@ void oracle_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes,
 /* One reconstructed element (b, h, t, d), fp64.
  * mode 0: anchor-only, planes are nibble planes:  x = zero + (16 a + 7.5) scale
  * mode 1: full 8-bit, planes are code planes:     x = zero + c * scale      */
-static void dequant_element(int mode, int Hkv, int bt, int max_tokens,
+static int get_field(const uint8_t *row, int e, int w);
+
+/* mode 0: 4-bit anchors (16 a + 7.5); mode 1: 8-bit codes; mode 2: A-bit
+ * anchors of a split width (rows of 16 A bytes, the anchor standing for code
+ * 2^R a + (2^R - 1) / 2 with R = 8 - A). */
+static void dequant_element(int mode, int A, int Hkv, int bt, int max_tokens,
                             const int32_t *bt_row, int b, int h, int t, int d,
                             const uint8_t *k_plane, const uint8_t *v_plane,
                             const float *k_scale, const float *k_zero,
@@ -235,7 +242,7 @@ static void dequant_element(int mode, int Hkv, int bt, int max_tokens,
                             double *k_out, double *v_out)
 {
     const int n_groups_max = (max_tokens + K_GROUP - 1) / K_GROUP;
-    const int row_bytes = mode == 0 ? NIBBLE_ROW : CODE_ROW;
+    const int row_bytes = mode == 0 ? NIBBLE_ROW : mode == 1 ? CODE_ROW : 16 * A;
     size_t off = plane_row_offset(bt_row, Hkv, bt, h, t, row_bytes);
     size_t km = (((size_t)b * Hkv + h) * n_groups_max + t / K_GROUP) * HEAD_DIM + d;
     size_t vm = ((size_t)b * Hkv + h) * (size_t)max_tokens + t;
@@ -243,6 +250,11 @@ static void dequant_element(int mode, int Hkv, int bt, int max_tokens,
     if (mode == 0) {
         kq = 16.0 * get_nibble(k_plane + off, d) + 7.5;
         vq = 16.0 * get_nibble(v_plane + off, d) + 7.5;
+    } else if (mode == 2) {
+        const int R = 8 - A;
+        const double w = (double)(1 << R), half = ((double)(1 << R) - 1.0) / 2.0;
+        kq = w * get_field(k_plane + off, d, A) + half;
+        vq = w * get_field(v_plane + off, d, A) + half;
     } else {
         kq = (double)k_plane[off + d];
         vq = (double)v_plane[off + d];
@@ -268,7 +280,7 @@ int oracle_dequant(int mode, int Hkv, int bt, int max_blocks, int max_tokens,
         for (int h = 0; h < Hkv; ++h)
             for (int d = 0; d < HEAD_DIM; ++d) {
                 size_t o = ((size_t)t * Hkv + h) * HEAD_DIM + d;
-                dequant_element(mode, Hkv, bt, max_tokens, bt_row, b, h, t, d,
+                dequant_element(mode, 0, Hkv, bt, max_tokens, bt_row, b, h, t, d,
                                 k_plane, v_plane, k_scale, k_zero, v_scale,
                                 v_zero, &k_hat[o], &v_hat[o]);
             }
@@ -308,7 +320,8 @@ static void attend(const double *q, const double *keys, const double *vals,
 }
 
 typedef struct {
-    int mode; /* 0 anchor decode, 1 verify */
+    int mode; /* 0 anchor decode, 1 verify, 2 anchor decode over A-bit anchors */
+    int anchor_bits; /* mode 2: A */
     int Hkv, bt, max_blocks, max_tokens, B, Hq, nq;
     int n_tail; /* anchor decode: BF16 tail tokens per sequence, all visible */
     const int32_t *seq_lens, *block_table;
@@ -331,7 +344,7 @@ static void attention_unit(const attn_job *J, int u, double *keys, double *vals)
     const int32_t *bt_row = J->block_table + (size_t)b * (size_t)J->max_blocks;
     for (int t = 0; t < T; ++t)
         for (int d = 0; d < HEAD_DIM; ++d)
-            dequant_element(J->mode, Hkv, J->bt, J->max_tokens, bt_row, b, kvh, t,
+            dequant_element(J->mode, J->anchor_bits, Hkv, J->bt, J->max_tokens, bt_row, b, kvh, t,
                             d, J->k_plane, J->v_plane, J->k_scale, J->k_zero,
                             J->v_scale, J->v_zero, &keys[(size_t)t * HEAD_DIM + d],
                             &vals[(size_t)t * HEAD_DIM + d]);
@@ -1007,4 +1020,35 @@ int oracle_dequant_anchor_split(int A, int Hkv, int bt, int max_blocks, int max_
             }
         }
     return 0;
+}
+
+/*
+ * Anchor-phase decode over the A-bit anchors of a split width (Sec. 4.2
+ * Anchor phase with the widths of Sec. 8): one query per sequence, as
+ * oracle_anchor_decode, with each anchor standing for code 2^R a + (2^R - 1)/2
+ * (R = 8 - A) dequantized in fp64 with the group's scale and zero.  Planes of
+ * rows of 16 A bytes (the layout of oracle_encode_split).  A = 4 is the plain
+ * anchor decode.  Returns 0, or -1.
+ */
+int oracle_anchor_decode_split(int A, int Hkv, int bt, int max_blocks, int max_tokens, int B,
+                               int Hq, const int32_t *seq_lens,
+                               const int32_t *block_table, const uint8_t *k_anc,
+                               const uint8_t *v_anc, const float *k_scale,
+                               const float *k_zero, const float *v_scale,
+                               const float *v_zero, const uint16_t *q, double *out,
+                               double *lse, const uint8_t *unit_mask, int nthreads)
+{
+    if (!split_ok(A)) return -1;
+    attn_job J;
+    memset(&J, 0, sizeof J);
+    J.mode = 2;
+    J.anchor_bits = A;
+    J.Hkv = Hkv; J.bt = bt; J.max_blocks = max_blocks; J.max_tokens = max_tokens;
+    J.B = B; J.Hq = Hq; J.nq = 1;
+    J.seq_lens = seq_lens; J.block_table = block_table;
+    J.k_plane = k_anc; J.v_plane = v_anc;
+    J.k_scale = k_scale; J.k_zero = k_zero; J.v_scale = v_scale; J.v_zero = v_zero;
+    J.q = q; J.out = out; J.lse = lse; J.unit_mask = unit_mask;
+    J.nthreads = nthreads;
+    return run_attention(&J);
 }

@@ -148,3 +148,34 @@ def test_split_pins_catch_mutant(name, tmp_path):
                         "tests/test_oracle_split.py"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+# Planted mistakes in the anchor decode over split-width anchors, each of which
+# the pins in test_oracle_split_decode.py must catch.
+SPLIT_DECODE_MUTANTS = {
+    "decode_anchor_centre_2R_half": ("const double w = (double)(1 << R), half = ((double)(1 << R) - 1.0) / 2.0;",
+                                     "const double w = (double)(1 << R), half = (double)(1 << R) / 2.0;"),
+    "decode_anchor_weight_2A": ("const double w = (double)(1 << R), half",
+                                "const double w = (double)(1 << A), half"),
+    "decode_rows_of_nibble_width": ("const int row_bytes = mode == 0 ? NIBBLE_ROW : mode == 1 ? CODE_ROW : 16 * A;",
+                                    "const int row_bytes = mode == 0 ? NIBBLE_ROW : mode == 1 ? CODE_ROW : NIBBLE_ROW;"),
+    "decode_fields_of_residual_width": ("kq = w * get_field(k_plane + off, d, A) + half;\n        vq = w * get_field(v_plane + off, d, A) + half;",
+                                        "kq = w * get_field(k_plane + off, d, R) + half;\n        vq = w * get_field(v_plane + off, d, R) + half;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SPLIT_DECODE_MUTANTS))
+def test_split_decode_pins_catch_mutant(name, tmp_path):
+    find, repl = SPLIT_DECODE_MUTANTS[name]
+    assert SRC.count(find) == 1, f"mutation anchor for {name} not unique/present"
+    src = tmp_path / "mutant.c"
+    src.write_text(SRC.replace(find, repl))
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-shared", "-fPIC",
+                    "-pthread", str(src), "-o", str(lib), "-lm"], check=True)
+    env = dict(os.environ, LYNX_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        "tests/test_oracle_split_decode.py"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
+
