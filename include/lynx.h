@@ -417,6 +417,31 @@ int lynx_kv_dequant_anchor_split(const lynx_layout *L, int32_t anchor_bits, int3
                                  void *v_out_bf16, void *stream);
 
 /*
+ * lynx_attn_anchor_decode_split -- decode attention over the anchors of a
+ * split width (Sec. 4.2 Anchor phase, with the other widths of Sec. 8), read
+ * straight from the A-bit anchor planes: for every sequence b and query head
+ * hq, O = softmax(q K^T / sqrt(128)) V (Sec. 2) with K, V reconstructed as
+ * zero + (2^R a + (2^R - 1) / 2) scale, R = 8 - anchor_bits (the anchor
+ * alone at the middle of the codes it covers, as lynx_kv_dequant_anchor_split).
+ *
+ *   anchor_bits  A: 2, 4 or 6
+ *   k_anc, v_anc anchor planes of rows of 16 A bytes (device), as written by
+ *                lynx_kv_encode_split; meta: metadata of the batch
+ *   other arguments as lynx_attn_anchor_decode; workspace >=
+ *   lynx_attn_workspace_bytes(L, B, Hq, 1, max_seq_len) (the arrival counters
+ *   at its head are not used by this call).
+ * Errors: LYNX_EINVAL (anchor_bits not 2, 4 or 6, or an argument
+ * lynx_attn_anchor_decode rejects), LYNX_EWORKSPACE, LYNX_EHIP.  A sequence
+ * with no tokens yields zeros and lse = -inf.
+ */
+int lynx_attn_anchor_decode_split(int32_t anchor_bits, const lynx_layout *L, int32_t B, int32_t Hq,
+                                  int32_t max_seq_len, const int32_t *seq_lens,
+                                  const int32_t *block_table, const uint8_t *k_anc,
+                                  const uint8_t *v_anc, const lynx_meta *meta, const void *q_bf16,
+                                  void *out_bf16, float *lse, void *workspace,
+                                  size_t workspace_bytes, void *stream);
+
+/*
  * The hierarchical non-linear codec of Alg. 1 (Sec. 4.1), the paper's own
  * quantizer, as an alternative to the uniform 8-bit one.  Per channel of a
  * kv head (K and V alike), over pages of 256 tokens and chunks of 32:

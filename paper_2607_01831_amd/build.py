@@ -12,7 +12,7 @@ HERE = Path(__file__).resolve().parent
 CSRC = HERE / "csrc"
 ROOT = HERE.parent
 LIBRARY = HERE / "liblynx.so"
-SOURCES = ["codec.hip", "hier.hip", "attention.hip", "anchor_decode.hip", "verify.hip", "spec.hip",
+SOURCES = ["codec.hip", "hier.hip", "attention.hip", "anchor_decode.hip", "anchor_split.hip", "verify.hip", "spec.hip",
            "abi.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

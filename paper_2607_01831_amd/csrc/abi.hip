@@ -207,6 +207,31 @@ int lynx_attn_anchor_decode(const lynx_layout *L, int32_t B, int32_t Hq, int32_t
     return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
 }
 
+int lynx_attn_anchor_decode_split(int32_t anchor_bits, const lynx_layout *L, int32_t B, int32_t Hq,
+                                  int32_t max_seq_len, const int32_t *seq_lens,
+                                  const int32_t *block_table, const uint8_t *k_anc,
+                                  const uint8_t *v_anc, const lynx_meta *meta, const void *q_bf16,
+                                  void *out_bf16, float *lse, void *workspace,
+                                  size_t workspace_bytes, void *stream) {
+    if (anchor_bits != 2 && anchor_bits != 4 && anchor_bits != 6) return LYNX_EINVAL;
+    Geometry g;
+    MetaPtrs mp;
+    int rc = check_attention_common(L, B, Hq, max_seq_len, seq_lens, block_table, k_anc, v_anc,
+                                    meta, q_bf16, out_bf16, &g, &mp);
+    if (rc != LYNX_OK) return rc;
+    if (B == 0) return LYNX_OK;
+    if (lse && !aligned16(lse)) return LYNX_EINVAL;
+    const lynx::AttnPlan p = lynx::plan_attention(g, B, Hq, 1, max_seq_len, false);
+    if (!workspace || !aligned16(workspace) || workspace_bytes < p.workspace_bytes())
+        return LYNX_EWORKSPACE;
+    hipError_t e = lynx::launch_attention(
+        lynx::KvMode::kAnchorSplit, g, p, B, Hq, 1, max_seq_len, seq_lens, block_table, k_anc,
+        v_anc, mp, static_cast<const uint16_t *>(q_bf16), nullptr, nullptr, 0,
+        static_cast<uint16_t *>(out_bf16), lse, workspace, static_cast<hipStream_t>(stream),
+        anchor_bits);
+    return e == hipSuccess ? LYNX_OK : LYNX_EHIP;
+}
+
 }  // extern "C"
 
 // ---- scratch of lynx_attn_anchor_decode_noalloc ----

@@ -285,7 +285,7 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
                             const uint8_t *v_plane, MetaPtrs meta, const uint16_t *q,
                             const uint16_t *k_new, const uint16_t *v_new, int tail_count,
                             uint16_t *out,
-                            float *lse, void *workspace, hipStream_t stream) {
+                            float *lse, void *workspace, hipStream_t stream, int anchor_bits) {
     if (B == 0 || plan.n_splits == 0) return hipSuccess;
     AttnArgs a;
     a.geo = g;
@@ -365,6 +365,30 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
         hipError_t e = launch_anchor_decode_mfma(d, chunks, stream);
         if (e != hipSuccess) return e;
         if (d.fused) return hipSuccess;
+    } else if (mode == KvMode::kAnchorSplit && nq == 1 && k_new == nullptr) {
+        // matrix-core decode over A-bit anchors; the combine kernel below
+        // merges its splits
+        SplitDecodeArgs d;
+        d.geo = g;
+        d.B = B;
+        d.Hq = Hq;
+        d.G = a.G;
+        d.max_seq_len = max_seq_len;
+        d.anchor_bits = anchor_bits;
+        d.n_splits = plan.n_ctx_splits;
+        d.groups_per_split = plan.split_tokens / kKGroup;
+        d.rows_total = plan.rows_total;
+        d.ws_splits = plan.n_splits;
+        d.seq_lens = seq_lens;
+        d.block_table = block_table;
+        d.k_anc = k_plane;
+        d.v_anc = v_plane;
+        d.meta = meta;
+        d.q = q;
+        d.ws_o = a.ws_o;
+        d.ws_ml = a.ws_ml;
+        hipError_t e = launch_anchor_split_decode(d, stream);
+        if (e != hipSuccess) return e;
     } else if (mode == KvMode::kCodes) {
         // matrix-core verification over the context splits ...
         VerifyArgs v;

@@ -103,7 +103,7 @@ hipError_t launch_deserialize_residual(const Geometry &g, int b, int t0, int n,
 constexpr size_t kCounterBytes = 262144;
 constexpr int kCounterStride = 64;  // uint32 slots between counters
 constexpr int kCounters = (int)(kCounterBytes / (kCounterStride * sizeof(unsigned)));
-enum class KvMode : int { kAnchor = 0, kCodes = 1 };
+enum class KvMode : int { kAnchor = 0, kCodes = 1, kAnchorSplit = 2 };
 
 struct AttnPlan {
     int rows_total;   // nq * G query rows per (sequence, kv head)
@@ -169,6 +169,29 @@ struct VerifyArgs {
 
 hipError_t launch_verify_mfma(const VerifyArgs &args, int split_groups, hipStream_t stream);
 
+// Arguments of the anchor decode over split-width anchors (anchor_split.hip):
+// one query per sequence over A-bit anchor planes (rows of 16 A bytes);
+// context splits only, merged by the combine kernel.
+struct SplitDecodeArgs {
+    Geometry geo;
+    int B, Hq, G, max_seq_len;
+    int anchor_bits;      // A: 2, 4 or 6
+    int n_splits;         // grid.x
+    int groups_per_split; // 4, 8 or 16
+    int rows_total;       // G query rows per (sequence, kv head)
+    int ws_splits;        // partial-row stride
+    const int32_t *seq_lens;
+    const int32_t *block_table;
+    const uint8_t *k_anc;
+    const uint8_t *v_anc;
+    MetaPtrs meta;
+    const uint16_t *q;    // BF16 [B][Hq][128]
+    float *ws_o;
+    float2 *ws_ml;
+};
+
+hipError_t launch_anchor_split_decode(const SplitDecodeArgs &args, hipStream_t stream);
+
 AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_len, bool tail);
 
 // k_new / v_new: the BF16 tail, or nullptr.  Verification (kCodes): k drafts
@@ -179,7 +202,8 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
                             const int32_t *block_table, const uint8_t *k_plane,
                             const uint8_t *v_plane, MetaPtrs meta, const uint16_t *q,
                             const uint16_t *k_new, const uint16_t *v_new, int tail_count,
-                            uint16_t *out, float *lse, void *workspace, hipStream_t stream);
+                            uint16_t *out, float *lse, void *workspace, hipStream_t stream,
+                            int anchor_bits = 4);
 
 // ---- acceptance of drafts (spec.hip) ------------------------------------------
 // Sampled acceptance workspace: B * (k + 1) * spec_accept_chunks(vocab) pairs of

@@ -39,6 +39,7 @@
 // group's K metadata rides with its first tile, and the query rows are
 // copied into LDS once.  At the end the four wavefronts merge through LDS
 // into one partial per row and split.
+#include "f16_ops.h"
 #include "lane_ops.h"
 #include "lynx_internal.h"
 
@@ -48,58 +49,10 @@ namespace lynx {
 
 namespace {
 
-typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
-
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kTile = 32;      // tokens per wavefront step
 constexpr float kLog2e = 1.4426950408889634f;
-
-__device__ __forceinline__ f32x4_t mfma(u32x4_t a, u32x4_t b, f32x4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
-                                                 __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
-}
-
-// Eight code bytes (two words, byte e = element e) -> eight fp16 values
-// 1024 + c in element order.
-__device__ __forceinline__ u32x4_t codes_to_f16(uint32_t w0, uint32_t w1) {
-    const uint32_t c = 0x64646464u;
-    u32x4_t r;
-    r[0] = __builtin_amdgcn_perm(c, w0, 0x04010400u);
-    r[1] = __builtin_amdgcn_perm(c, w0, 0x04030402u);
-    r[2] = __builtin_amdgcn_perm(c, w1, 0x04010400u);
-    r[3] = __builtin_amdgcn_perm(c, w1, 0x04030402u);
-    return r;
-}
-
-// Two floats -> two fp16 in one word, a in the low half.  pack_f16 rounds
-// toward zero (the split of bounded query values into hi + lo);
-// pack_f16_rne rounds to nearest and overflows to infinity, so a softmax
-// weight too large for fp16 cannot saturate unnoticed.
-__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
-    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(a, b));
-}
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t pack_f16_rne(float a, float b) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
-}
-__device__ __forceinline__ float f16_lo(uint32_t w) {
-    return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xffffu));
-}
-__device__ __forceinline__ float f16_hi(uint32_t w) {
-    return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
-}
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// Byte offset of 16-byte chunk q of V-tile row t in a wavefront's LDS slot.
-// The XOR swizzle spreads the 8 rows one transposed read touches over all
-// 32 banks.
-__device__ __forceinline__ uint32_t v_slot(int t, int q) {
-    const int sw = (t & 7) ^ ((t >> 4) << 2);
-    return (uint32_t)t * kCodeRow + (uint32_t)((q ^ sw) * 16);
-}
 
 constexpr int kDepth = 2;                          // ring slots per wavefront
 constexpr int kTileBytes = kTile * kCodeRow;       // one plane's 32 rows: 4 KB
@@ -406,8 +359,8 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
                 const u32x4_t av = (kk & 1) ? codes_to_f16(u.z, u.w) : codes_to_f16(u.x, u.y);
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt) {
-                    sc[rt][r] = mfma(av, bq[rt][2 * kk + 0], sc[rt][r]);
-                    sc[rt][r] = mfma(av, bq[rt][2 * kk + 1], sc[rt][r]);
+                    sc[rt][r] = mfma_f16(av, bq[rt][2 * kk + 0], sc[rt][r]);
+                    sc[rt][r] = mfma_f16(av, bq[rt][2 * kk + 1], sc[rt][r]);
                 }
             }
         }
@@ -464,10 +417,10 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
                 (__attribute__((address_space(3))) intx2_t *)(vl + v_slot(tr, c) + 8 * half));
             const u32x4_t bv = codes_to_f16((uint32_t)vt[0], (uint32_t)vt[1]);
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) acc[rt][c] = mfma(pa[rt], bv, acc[rt][c]);
+            for (int rt = 0; rt < RT; ++rt) acc[rt][c] = mfma_f16(pa[rt], bv, acc[rt][c]);
         }
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) acc_off[rt] = mfma(pa[rt], c1024, acc_off[rt]);
+        for (int rt = 0; rt < RT; ++rt) acc_off[rt] = mfma_f16(pa[rt], c1024, acc_off[rt]);
     };
 
     // Fast path: the softmax reference of each row is the maximum of the

@@ -64,6 +64,8 @@ def load():
         "lynx_attn_workspace_bytes": ([LP, I32, I32, I32, I32], SZ),
         "lynx_attn_anchor_decode": ([LP, I32, I32, I32, P, P, P, P, MP, P, P, P, P, SZ, P],
                                     ctypes.c_int),
+        "lynx_attn_anchor_decode_split": ([I32, LP, I32, I32, I32, P, P, P, P, MP, P, P, P, P, SZ, P],
+                                          ctypes.c_int),
         "lynx_attn_anchor_decode_noalloc": ([LP, I32, I32, I32, P, P, P, P, MP, P, P, P, P],
                                             ctypes.c_int),
         "lynx_attn_verify": ([LP, I32, I32, I32, I32, P, P, P, P, MP, P, P, P, P, P, SZ, P],
@@ -255,6 +257,25 @@ def lynx_attn_anchor_decode(L: Layout, B: int, Hq: int, max_seq_len: int, seq_le
     _check("lynx_attn_anchor_decode", load().lynx_attn_anchor_decode(
         ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table), _ptr(k_anc),
         _ptr(v_anc), ctypes.byref(met), _ptr(q), _ptr(out), _ptr(lse), _ptr(ws),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def lynx_attn_anchor_decode_split(anchor_bits: int, L: Layout, B: int, Hq: int, max_seq_len: int,
+                                  seq_lens, block_table, k_anc, v_anc, meta: Meta, q, out, lse=None,
+                                  workspace_buf=None, stream=None) -> None:
+    """Decode over the A-bit anchor planes of a split width (rows of 16 A bytes)."""
+    fn = "lynx_attn_anchor_decode_split"
+    if anchor_bits not in (2, 4, 6):
+        raise LynxError(fn, LYNX_EINVAL)
+    _need_attn(fn, L, B, seq_lens, block_table, (k_anc, v_anc), 16 * anchor_bits, meta)
+    _need(fn, "q", q, B * Hq * HEAD_DIM * 2)
+    _need(fn, "out", out, B * Hq * HEAD_DIM * 2)
+    _need(fn, "lse", lse, B * Hq * 4)
+    lay, met = L.c(), meta.c()
+    ws = workspace_buf
+    _check(fn, load().lynx_attn_anchor_decode_split(
+        anchor_bits, ctypes.byref(lay), B, Hq, max_seq_len, _ptr(seq_lens), _ptr(block_table),
+        _ptr(k_anc), _ptr(v_anc), ctypes.byref(met), _ptr(q), _ptr(out), _ptr(lse), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 

@@ -224,6 +224,18 @@ def test_split_width_validation(lib):
     assert deq(A=1) == E.LYNX_EINVAL
     assert deq(T=-1) == E.LYNX_EINVAL
     assert deq(T=0) == E.LYNX_OK
+    # decode over split-width anchors: bad width, bad heads, workspace, empty batch
+    args = (16, 16, 16, 16, ctypes.byref(m), 16, 16)
+    dec = lambda A=2, B=1, Hq=32, ws=None, wsb=0: lib.lynx_attn_anchor_decode_split(
+        A, ctypes.byref(lay), B, Hq, 64, *args, None, ws, wsb, None)
+    assert dec(A=3) == E.LYNX_EINVAL
+    assert dec(A=8) == E.LYNX_EINVAL
+    assert dec(Hq=12) == E.LYNX_EINVAL
+    assert dec() == E.LYNX_EWORKSPACE
+    assert dec(ws=16, wsb=64) == E.LYNX_EWORKSPACE
+    assert lib.lynx_attn_anchor_decode_split(6, ctypes.byref(lay), 0, 32, 64, None, None, None, None,
+                                             ctypes.byref(m), None, None, None, None, 0,
+                                             None) == E.LYNX_OK
 
 
 def test_hierarchical_codec_validation(lib):

@@ -1,0 +1,152 @@
+"""GPU parity of the anchor decode over split-width anchors (A-bit anchor planes,
+A in 2, 4, 6; Sec. 4.2 Anchor phase with the widths of Sec. 8) through the C
+ABI, against the CPU oracle's anchor decode over the same anchors, on the
+same seeded inputs: contiguous and paged pools, ragged and empty sequences,
+head chunks past 16 query heads, a dominant late token (the running maximum
+rescales), and a 32K-token Llama-3-8B layer; A = 4 also against the nibble
+decode kernel over the plain 4 + 4 planes."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_01831_amd import inputs, lynx
+from tests._util import LSE_ATOL, LSE_RTOL, assert_close
+from tests.gpu_cases import bits, build_cache, gpu_anchor_decode, note, random_bf16, random_kv
+
+pytestmark = pytest.mark.gpu
+
+
+def encode(A, k_list, v_list, Hkv, bt=None, seed=0):
+    """Encode every sequence into A-bit planes on the GPU and with the oracle;
+    the planes and metadata must agree bit for bit."""
+    lens = [int(k.shape[0]) for k in k_list]
+    B = len(lens)
+    max_T = max(max(lens), 1)
+    if bt is None:
+        bt_eff, table, n_blocks = max_T, torch.arange(B, dtype=torch.int32).view(B, 1), B
+    else:
+        bt_eff = bt
+        table, n_blocks = inputs.paged_block_table(torch.tensor(lens), bt, seed)
+        n_blocks = max(n_blocks, 1)
+    L = lynx.Layout(num_kv_heads=Hkv, block_tokens=bt_eff, max_blocks_per_seq=table.shape[1],
+                    num_blocks=n_blocks, max_tokens=max_T)
+    OL = oracle.Layout(Hkv=Hkv, bt=bt_eff, max_blocks=table.shape[1], max_tokens=max_T)
+    n_rows = n_blocks * Hkv * bt_eff
+    R = 8 - A
+    planes = {"k_anc": torch.zeros(n_rows * 16 * A, dtype=torch.uint8, device="cuda"),
+              "v_anc": torch.zeros(n_rows * 16 * A, dtype=torch.uint8, device="cuda"),
+              "k_res": torch.zeros(n_rows * 16 * R, dtype=torch.uint8, device="cuda"),
+              "v_res": torch.zeros(n_rows * 16 * R, dtype=torch.uint8, device="cuda")}
+    meta = lynx.Meta.empty(L, B)
+    tdev = table.cuda()
+    op = {name: np.zeros(t.numel(), np.uint8) for name, t in planes.items()}
+    om = oracle.Meta.empty(OL, B)
+    for b in range(B):
+        note(f"kv_encode_split A={A} b={b} T={lens[b]} Hkv={Hkv} bt={bt_eff}")
+        lynx.lynx_kv_encode_split(L, A, b, lens[b], tdev, k_list[b].cuda(), v_list[b].cuda(),
+                                  planes["k_anc"], planes["v_anc"], planes["k_res"], planes["v_res"], meta)
+        oracle.encode_split(A, OL, b, lens[b], table.numpy(), bits(k_list[b]), bits(v_list[b]), op, om)
+    torch.cuda.synchronize()
+    for name in ("k_anc", "v_anc"):
+        assert np.array_equal(planes[name].cpu().numpy(), op[name]), name
+    return lens, L, OL, table, planes, meta, op, om
+
+
+def decode(A, lens, L, table, planes, meta, q):
+    B, Hq = len(lens), q.shape[1]
+    max_len = max(lens)
+    out = torch.empty(B, Hq, 128, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(B, Hq, dtype=torch.float32, device="cuda")
+    ws = lynx.workspace(L, B, Hq, 1, max_len)
+    note(f"anchor_decode_split A={A} B={B} Hq={Hq} lens={lens[:4]}")
+    lynx.lynx_attn_anchor_decode_split(A, L, B, Hq, max_len, torch.tensor(lens, dtype=torch.int32).cuda(),
+                                       table.cuda(), planes["k_anc"], planes["v_anc"], meta,
+                                       q.cuda().contiguous(), out, lse, ws)
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy(), lse.cpu().numpy()
+
+
+def check(A, lens, OL, table, op, om, q, out, lse, unit_mask=None, what=""):
+    ref, ref_lse = oracle.anchor_decode_split(A, OL, q.shape[1], np.array(lens, np.int32), table.numpy(),
+                                              op["k_anc"], op["v_anc"], om, bits(q), unit_mask=unit_mask)
+    if unit_mask is not None:
+        G = q.shape[1] // OL.Hkv
+        rows = np.repeat(np.asarray(unit_mask, bool), G, axis=1)  # [B][Hq]
+        out, ref, lse, ref_lse = out[rows], ref[rows], lse[rows], ref_lse[rows]
+    assert_close(out, ref, what=what)
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(fin, np.isfinite(lse)), what
+    np.testing.assert_allclose(lse[fin], ref_lse[fin], rtol=LSE_RTOL, atol=LSE_ATOL)
+
+
+CASES = [
+    # (lens, Hkv, G, bt)
+    ([1000], 2, 4, None),
+    ([300, 0, 129], 2, 3, 16),
+    ([513, 1], 1, 8, 32),
+    ([2125], 2, 16, None),
+    ([700, 40], 2, 20, 16),
+    ([1], 1, 1, None),
+]
+
+
+@pytest.mark.parametrize("A", [2, 4, 6])
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_split_decode_against_oracle(A, case):
+    lens, Hkv, G, bt = CASES[case]
+    kv = [random_kv(T, Hkv, seed=4000 + 17 * case + T) for T in lens]
+    lens, L, OL, table, planes, meta, op, om = encode(A, [k for k, _ in kv], [v for _, v in kv], Hkv, bt,
+                                                      seed=case)
+    q = random_bf16((len(lens), Hkv * G, 128), seed=4100 + case)
+    out, lse = decode(A, lens, L, table, planes, meta, q)
+    check(A, lens, OL, table, op, om, q, out, lse, what=f"A={A} case {CASES[case]}")
+
+
+@pytest.mark.parametrize("A", [2, 6])
+@pytest.mark.parametrize("boost", [30.0, 400.0])
+def test_split_decode_dominant_late_token(A, boost):
+    """A late token whose score dwarfs every earlier one: the running maximum
+    rescales the accumulators when the tile that holds it arrives."""
+    T, Hkv, G = 3000, 2, 4
+    g = torch.Generator().manual_seed(int(boost) + A)
+    q = torch.randn(1, G * Hkv, 128, generator=g)
+    k = torch.randn(T, Hkv, 128, generator=g)
+    v = torch.randn(T, Hkv, 128, generator=g)
+    for h in range(Hkv):
+        k[2500, h] = boost * q[0, h * G] / q[0, h * G].norm()
+    lens, L, OL, table, planes, meta, op, om = encode(A, [k.to(torch.bfloat16)], [v.to(torch.bfloat16)], Hkv)
+    qb = q.to(torch.bfloat16)
+    out, lse = decode(A, lens, L, table, planes, meta, qb)
+    check(A, lens, OL, table, op, om, qb, out, lse, what=f"A={A} dominant token x{boost}")
+
+
+def test_split_decode_a4_matches_the_nibble_decode():
+    """A = 4 planes are the 4 + 4 nibble planes: the split-width kernel and the
+    nibble decode kernel attend the same cache, each within the tolerance of
+    the oracle, and within twice that of each other."""
+    T, Hkv, G = 1500, 2, 4
+    k, v = random_kv(T, Hkv, seed=4200)
+    lens, L, OL, table, planes, meta, op, om = encode(4, [k], [v], Hkv)
+    q = random_bf16((1, Hkv * G, 128), seed=4201)
+    out, lse = decode(4, lens, L, table, planes, meta, q)
+    c = build_cache([k], [v], Hkv, merge=False)
+    out_n, lse_n = gpu_anchor_decode(c, q)
+    assert_close(out, out_n, atol=4e-2, rtol=2e-2, what="A=4 split kernel vs nibble kernel")
+    np.testing.assert_allclose(lse, lse_n, rtol=2 * LSE_RTOL, atol=2 * LSE_ATOL)
+    check(4, lens, OL, table, op, om, q, out, lse, what="A=4")
+
+
+@pytest.mark.parametrize("A", [2, 6])
+def test_split_decode_llama3_8b_layer(A):
+    """A 32K-token Llama-3-8B layer (8 kv heads, 32 query heads): every output
+    on the GPU, two kv heads' outputs against the oracle."""
+    w = inputs.WORKLOADS["llama3-8b-32k"]
+    k, v = inputs.kv(w, "k", layer=5), inputs.kv(w, "v", layer=5)
+    lens, L, OL, table, planes, meta, op, om = encode(A, [k], [v], w.Hkv)
+    q = inputs.queries(w, layer=5)
+    out, lse = decode(A, lens, L, table, planes, meta, q)
+    assert np.isfinite(out).all()
+    mask = np.zeros((1, w.Hkv), np.uint8)
+    mask[0, [0, 5]] = 1
+    check(A, lens, OL, table, op, om, q, out, lse, unit_mask=mask, what=f"A={A} 32K layer")
