@@ -179,7 +179,7 @@ def _csv(dirname, suffix):
 
 
 def _short(name: str) -> str:
-    for key in ("anchor_decode_kernel", "attn_combine_kernel", "verify_kernel", "encode_kernel",
+    for key in ("anchor_split_decode_kernel", "anchor_decode_kernel", "attn_combine_kernel", "verify_kernel", "encode_kernel",
                 "merge_kernel", "copyBuffer", "hencode_kernel", "hdequant_kernel",
                 "deserialize_anchor_kernel", "deserialize_residual_kernel", "merge_split_kernel",
                 "dequant_anchor_split_kernel", "argmax_chunk_kernel", "accept_kernel",
@@ -937,12 +937,15 @@ def hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers, alphas=(255.0
     return {"hier_codec": r}
 
 
-def split_widths_stage(dev, T, Hkv, K, V, n_layers):
+def split_widths_stage(dev, T, Hkv, K, V, n_layers, Q=None, Hq=None):
     """The 2 + 6 and 6 + 2 splits on the workload's layers: encode of every
     layer into its own planes (so the merge below reads cold planes), merge of
-    the whole cache (one call per plane kind) and the anchor phase's BF16
-    pages (layers in turn), HIP events; bytes as for the 4 + 4 codec, with
-    A / 8 and (8 - A) / 8 bytes per element for the two planes."""
+    the whole cache (one call per plane kind), the anchor phase's BF16
+    pages and the anchor decode straight from the A-bit planes (layers in
+    turn, one query per layer), HIP events; bytes as for the 4 + 4 codec, with
+    A / 8 and (8 - A) / 8 bytes per element for the two planes, and for the
+    decode 32 A + 16 bytes per token and kv head (K and V anchors, V scale and
+    zero, K scales and zeros over the group's 128 tokens)."""
     import torch
 
     from paper_2607_01831_amd import lynx
@@ -975,6 +978,15 @@ def split_widths_stage(dev, T, Hkv, K, V, n_layers):
             for l in range(n_layers):
                 lynx.lynx_kv_dequant_anchor_split(L, A, 0, T, table, anc[0, l], anc[1, l], metas[l], ko, vo)
 
+        lens = torch.tensor([T], dtype=torch.int32, device=dev)
+        dec_out = torch.empty(1, Hq or 1, 128, dtype=torch.bfloat16, device=dev)
+        ws = lynx.workspace(L, 1, Hq or 1, 1, T)
+
+        def dec():
+            for l in range(n_layers):
+                lynx.lynx_attn_anchor_decode_split(A, L, 1, Hq, T, lens, table, anc[0, l], anc[1, l], metas[l],
+                                                   Q[l], dec_out, None, ws)
+
         out = {}
         for name, fn, per_elem in (("encode", enc, 2 + 1 + 0.0625), ("merge", merge, 2.0),
                                    ("dequant_anchor", deq, A / 8 + 2 + 0.0625)):
@@ -982,6 +994,13 @@ def split_widths_stage(dev, T, Hkv, K, V, n_layers):
             us = summary(call_samples(fn, n=REPS, warm=2, per=n_layers))["median"]
             out[f"{name}_us_per_layer"] = round(us, 2)
             out[f"{name}_GBps"] = round(elems * per_elem / (us * 1e-6) / 1e9, 1)
+        if Q is not None:
+            enc()
+            st = summary(call_samples(dec, n=REPS, warm=2, per=n_layers))
+            out["anchor_decode_us_per_layer"] = st
+            gbps = rows * (32 * A + 16) / (st["median"] * 1e-6) / 1e9
+            out["anchor_decode_GBps"] = round(gbps, 1)
+            out["anchor_decode_frac"] = round(gbps / HBM_PEAK_GBPS, 4)
         r[f"split_{A}_{R}"] = out
         del anc, res, codes, metas
     return {"split_widths": r}
@@ -1215,7 +1234,7 @@ def main():
     ovl = overlap_70b_stage(dev) if args.overlap_70b else None
     serdes = serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side) if args.serdes else None
     hier = hier_codec_stage(dev, T, Hkv, Hq, K, V, Q, pools, L, n_layers) if args.hier else None
-    split = split_widths_stage(dev, T, Hkv, K, V, n_layers) if args.split_widths else None
+    split = split_widths_stage(dev, T, Hkv, K, V, n_layers, Q, Hq) if args.split_widths else None
 
     # The speculative decoder's own pieces, timed alone: decode over the
     # anchors plus the 8 BF16 tokens it generated (32 layers), and greedy

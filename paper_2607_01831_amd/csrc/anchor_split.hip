@@ -202,31 +202,6 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_split_decode_kernel(SplitD
     const int n_tiles = 4 * n_mine;
     auto tile_t0 = [&](int j) { return (g0 + w + kWaves * (j >> 2)) * kKGroup + kTile * (j & 3); };
 
-    // ---- query rows into LDS (rows past the chunk's heads repeat the last) ----
-    {
-        const int r = tid >> 4;  // 16 threads per 256-byte row
-        const int hh = min(row_base + r, a.rows_total - 1);
-        const size_t qrow = (size_t)b * a.Hq + (size_t)h * a.G + hh;
-        reinterpret_cast<uint4 *>(s_q)[tid] = reinterpret_cast<const uint4 *>(a.q + qrow * kHeadDim)[tid & 15];
-    }
-
-    // ---- the largest adjusted V scale s' of the wavefront's tokens ----
-    int Ev = 0;
-    {
-        float vm = 0.0f;
-#pragma unroll
-        for (int u = 0; u < kMaxGroups; ++u) {
-#pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                const int t = (g0 + w + kWaves * u) * kKGroup + 64 * k + lane;
-                if (u < n_mine && t < T) vm = fmax2(vm, a.meta.v_scale[vmeta + t]);
-            }
-        }
-        vm = max_kg(row16_max(vm)) * (float)(1 << R);
-        if (vm > 0.0f) frexpf(vm, &Ev);
-        Ev = max(Ev, -100);
-    }
-
     auto load_tile = [&](int j, TileRegs<A> &rg) {
         const int t0 = tile_t0(j);
 #pragma unroll
@@ -250,6 +225,35 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_split_decode_kernel(SplitD
         }
     };
 
+    // the first tile's loads, the query rows and the V scales go out together:
+    // one round trip before the loop
+    TileRegs<A> cur, nxt;
+    if (n_tiles > 0) load_tile(0, cur);
+    uint4 q4;
+    {
+        const int r = tid >> 4;  // 16 threads per 256-byte row (rows past the chunk's heads repeat the last)
+        const int hh = min(row_base + r, a.rows_total - 1);
+        const size_t qrow = (size_t)b * a.Hq + (size_t)h * a.G + hh;
+        q4 = reinterpret_cast<const uint4 *>(a.q + qrow * kHeadDim)[tid & 15];
+    }
+    // ---- the largest adjusted V scale s' of the wavefront's tokens ----
+    int Ev = 0;
+    {
+        float vm = 0.0f;
+#pragma unroll
+        for (int u = 0; u < kMaxGroups; ++u) {
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int t = (g0 + w + kWaves * u) * kKGroup + 64 * k + lane;
+                if (u < n_mine && t < T) vm = fmax2(vm, a.meta.v_scale[vmeta + t]);
+            }
+        }
+        vm = max_kg(row16_max(vm)) * (float)(1 << R);
+        if (vm > 0.0f) frexpf(vm, &Ev);
+        Ev = max(Ev, -100);
+    }
+
+    reinterpret_cast<uint4 *>(s_q)[tid] = q4;
     __syncthreads();  // the query rows are in
 
     // ---- per-wavefront online-softmax state: lane (col = query row, kg);
@@ -309,8 +313,6 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_split_decode_kernel(SplitD
     const int tr = 16 * ((col >> 1) >> 2) + 4 * kg + ((col >> 1) & 3);
     const int half = col & 1;
 
-    TileRegs<A> cur, nxt;
-    if (n_tiles > 0) load_tile(0, cur);
     for (int j = 0; j < n_tiles; ++j) {
         if (j + 1 < n_tiles) load_tile(j + 1, nxt);  // in flight while tile j is attended
         const int t0 = tile_t0(j);
