@@ -428,8 +428,8 @@ int lynx_kv_dequant_anchor_split(const lynx_layout *L, int32_t anchor_bits, int3
  *   k_anc, v_anc anchor planes of rows of 16 A bytes (device), as written by
  *                lynx_kv_encode_split; meta: metadata of the batch
  *   other arguments as lynx_attn_anchor_decode; workspace >=
- *   lynx_attn_workspace_bytes(L, B, Hq, 1, max_seq_len) (the arrival counters
- *   at its head are not used by this call).
+ *   lynx_attn_workspace_bytes(L, B, Hq, 1, max_seq_len), its arrival counters
+ *   zero on entry as for lynx_attn_anchor_decode (every call leaves them zero).
  * Errors: LYNX_EINVAL (anchor_bits not 2, 4 or 6, or an argument
  * lynx_attn_anchor_decode rejects), LYNX_EWORKSPACE, LYNX_EHIP.  A sequence
  * with no tokens yields zeros and lse = -inf.

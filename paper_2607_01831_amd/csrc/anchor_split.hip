@@ -33,10 +33,13 @@
 // of a per-wavefront LDS tile, read back transposed (ds_read_b64_tr_b8) as
 // the P V operand.  The softmax keeps a running maximum (rescaling when a
 // tile raises it).  The four wavefronts merge through LDS into one partial
-// per split, which the combine kernel merges across splits.
+// per split.  When the grid runs in one round the last workgroup of each
+// (sequence, kv head, row chunk) merges the splits in the same launch (as
+// the 4-bit decode does); otherwise the combine kernel merges them.
 #include "f16_ops.h"
 #include "lane_ops.h"
 #include "lynx_internal.h"
+#include "split_merge.h"
 
 #include <math.h>
 
@@ -158,7 +161,20 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_split_decode_kernel(SplitD
     auto partial_index = [&](int r) {
         return (((size_t)b * Hkv + h) * a.rows_total + r) * a.ws_splits + split;
     };
-    if (n_groups == 0) {  // a split past the context: (max, sum) = (-inf, 0)
+    const int heads = min(kRows, a.rows_total - row_base);  // live query rows of the chunk
+    // splits holding tokens (one for an empty sequence)
+    const int live = max(1, (T + SG * kKGroup - 1) / (SG * kKGroup));
+    if (a.fused && split >= live) return;  // nothing to attend, nothing to merge
+    if (n_groups == 0) {
+        if (a.fused) {  // split 0 of an empty sequence: zero output, lse -inf
+            const size_t orow0 = (size_t)b * a.Hq + (size_t)h * a.G + row_base;
+            for (int idx = tid; idx < heads * (kHeadDim / 4); idx += kThreads)
+                *reinterpret_cast<uint2 *>(a.out + (orow0 + idx / (kHeadDim / 4)) * kHeadDim +
+                                           4 * (idx % (kHeadDim / 4))) = make_uint2(0u, 0u);
+            if (a.lse && tid < heads) a.lse[orow0 + tid] = -INFINITY;
+            return;
+        }
+        // a split past the context: (max, sum) = (-inf, 0)
         for (int r = tid; r < kRows; r += kThreads)
             if (row_base + r < a.rows_total) a.ws_ml[partial_index(row_base + r)] = make_float2(-INFINITY, 0.0f);
         return;
@@ -466,6 +482,11 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_split_decode_kernel(SplitD
         s_ML[tid][1] = any_bad ? NAN : L;
     }
     __syncthreads();
+    // the chunk's partials: rows row_base .. + heads - 1 of (b, h)
+    const size_t prow0 = ((size_t)b * Hkv + h) * a.rows_total + row_base;
+    const __amdgpu_buffer_rsrc_t pair_o =
+        buffer_rsrc(a.ws_o + prow0 * a.ws_splits * kHeadDim, (uint32_t)heads * a.ws_splits * kHeadDim * 4);
+    const __amdgpu_buffer_rsrc_t pair_ml = buffer_rsrc(a.ws_ml + prow0 * a.ws_splits, (uint32_t)heads * a.ws_splits * 8);
     for (int idx = tid; idx < kRows * (kHeadDim / 4); idx += kThreads) {
         const int rr = idx / (kHeadDim / 4);
         const int d4 = idx % (kHeadDim / 4);
@@ -483,10 +504,29 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_split_decode_kernel(SplitD
             O.w = fmaf(o.w + ob, f, O.w);
         }
         if (any_bad) O = make_float4(NAN, NAN, NAN, NAN);
-        const size_t pi = partial_index(row);
-        reinterpret_cast<float4 *>(a.ws_o + pi * kHeadDim)[d4] = O;
-        if (d4 == 0) a.ws_ml[pi] = make_float2(s_ML[rr][0], s_ML[rr][1]);
+        if (a.fused) {
+            const uint32_t sp = (uint32_t)rr * a.ws_splits + split;  // within the chunk's rows
+            store16_agent(pair_o, (sp * kHeadDim + 4 * d4) * 4, O);
+            if (d4 == 0) store8_agent(pair_ml, sp * 8, make_float2(s_ML[rr][0], s_ML[rr][1]));
+        } else {
+            const size_t pi = partial_index(row);
+            reinterpret_cast<float4 *>(a.ws_o + pi * kHeadDim)[d4] = O;
+            if (d4 == 0) a.ws_ml[pi] = make_float2(s_ML[rr][0], s_ML[rr][1]);
+        }
     }
+    if (!a.fused) return;
+
+    // ---- split merge: count in; the chunk's last workgroup merges ----
+    __shared__ int s_last;
+    unsigned *ctr = a.counters + (((size_t)b * Hkv + h) * a.row_chunks + chunk) * kCounterStride;
+    if (!last_to_arrive(ctr, live, &s_last)) return;
+    const size_t orow0 = (size_t)b * a.Hq + (size_t)h * a.G + row_base;
+    if (heads <= 4)
+        merge_pair<4>(a, pair_o, pair_ml, orow0, heads, live, s_buf);
+    else if (heads <= 8)
+        merge_pair<8>(a, pair_o, pair_ml, orow0, heads, live, s_buf);
+    else
+        merge_pair<16>(a, pair_o, pair_ml, orow0, heads, live, s_buf);
 }
 
 template <int A, int LAYOUT>

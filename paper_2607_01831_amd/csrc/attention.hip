@@ -387,8 +387,20 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
         d.q = q;
         d.ws_o = a.ws_o;
         d.ws_ml = a.ws_ml;
+        // the split merge in the same launch, under the rule of the 4-bit
+        // decode: one round of workgroups, and at most 2 * 256 / GP splits
+        // for the merging workgroup (GP: the chunk's rows, padded)
+        const int gp = a.G <= 4 ? 4 : a.G <= 8 ? 8 : 16;
+        const long long wgs = (long long)plan.n_ctx_splits * g.Hkv * plan.row_chunks * B;
+        d.fused = (plan.counters_fit && plan.n_ctx_splits <= 2 * (256 / gp) &&
+                   wgs <= 2LL * compute_units()) ? 1 : 0;
+        d.row_chunks = plan.row_chunks;
+        d.counters = reinterpret_cast<unsigned *>(workspace);
+        d.out = out;
+        d.lse = lse;
         hipError_t e = launch_anchor_split_decode(d, stream);
         if (e != hipSuccess) return e;
+        if (d.fused) return hipSuccess;
     } else if (mode == KvMode::kCodes) {
         // matrix-core verification over the context splits ...
         VerifyArgs v;

@@ -188,6 +188,13 @@ struct SplitDecodeArgs {
     const uint16_t *q;    // BF16 [B][Hq][128]
     float *ws_o;
     float2 *ws_ml;
+    // split merge in the same launch (as DecodeArgs): arrival counters
+    // uint32 [B][Hkv][row_chunks], zero on entry, left zero
+    int fused;
+    int row_chunks;
+    unsigned *counters;
+    uint16_t *out;        // BF16 [B][Hq][128]
+    float *lse;           // fp32 [B][Hq] or nullptr
 };
 
 hipError_t launch_anchor_split_decode(const SplitDecodeArgs &args, hipStream_t stream);

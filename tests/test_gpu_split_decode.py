@@ -150,3 +150,30 @@ def test_split_decode_llama3_8b_layer(A):
     mask = np.zeros((1, w.Hkv), np.uint8)
     mask[0, [0, 5]] = 1
     check(A, lens, OL, table, op, om, q, out, lse, unit_mask=mask, what=f"A={A} 32K layer")
+
+
+def test_split_decode_calls_share_one_workspace():
+    """Back-to-back calls of different widths and shapes on one workspace (its
+    arrival counters zeroed once): each call leaves the counters zero, so
+    every result equals the one from a fresh workspace."""
+    Hkv, G = 2, 4
+    cases = []
+    for A, lens in ((2, [700, 5]), (6, [1500]), (2, [40, 2000, 3])):
+        kv = [random_kv(T, Hkv, seed=4400 + T) for T in lens]
+        cases.append((A, encode(A, [k for k, _ in kv], [v for _, v in kv], Hkv)))
+    nbytes = max(lynx.lynx_attn_workspace_bytes(c[1], len(c[0]), Hkv * G, 1, max(c[0])) for _, c in cases)
+    shared = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    for rep in range(2):
+        for i, (A, (lens, L, OL, table, planes, meta, op, om)) in enumerate(cases):
+            q = random_bf16((len(lens), Hkv * G, 128), seed=4500 + i)
+            fresh, fresh_lse = decode(A, lens, L, table, planes, meta, q)
+            out = torch.empty(len(lens), Hkv * G, 128, dtype=torch.bfloat16, device="cuda")
+            lse = torch.empty(len(lens), Hkv * G, dtype=torch.float32, device="cuda")
+            note(f"anchor_decode_split shared workspace A={A} lens={lens} rep={rep}")
+            lynx.lynx_attn_anchor_decode_split(A, L, len(lens), Hkv * G, max(lens),
+                                               torch.tensor(lens, dtype=torch.int32).cuda(), table.cuda(),
+                                               planes["k_anc"], planes["v_anc"], meta, q.cuda(), out, lse, shared)
+            torch.cuda.synchronize()
+            assert np.array_equal(out.float().cpu().numpy(), fresh), (A, lens, rep)
+            assert np.array_equal(lse.cpu().numpy(), fresh_lse), (A, lens, rep)
+    assert int(shared[:lynx.ATTN_COUNTER_BYTES].count_nonzero()) == 0
