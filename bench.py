@@ -64,7 +64,7 @@ WORKLOAD = "llama3-8b-32k"
 COPY_CALIBRATION_BYTES = 640 << 20
 TRAFFIC_SUMMARY = ROOT / "profiles" / "anchor_decode_llama3-8b-32k_traffic.md"
 # sources whose kernels make up one anchor-decode call
-DECODE_SOURCES = ["anchor_decode.hip", "attention.hip", "lynx_internal.h", "lane_ops.h"]
+DECODE_SOURCES = ["anchor_decode.hip", "split_merge.h", "attention.hip", "lynx_internal.h", "lane_ops.h"]
 
 # algorithmic bytes per unit
 ENC_BYTES_PER_ELEM = 2.0 + 0.5 + 0.5 + 0.0625   # read BF16, write 2 nibbles, metadata
