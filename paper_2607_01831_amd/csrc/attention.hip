@@ -62,12 +62,15 @@ constexpr int kCombineThreads = 256;
 // One workgroup per (row, kv head, sequence): merge the partials of all
 // splits and the BF16 tail tokens, normalise, round to BF16, write lse.
 // Thread (split group sg, float4 column d4) folds every 8th split into a
-// running (max, sum, output), loading 16 splits' partial outputs and (max,
-// sum) pairs together, then every 8th tail token the same way, as a partial
-// of weight 1.  The 8 running triples meet in LDS.  Every load the kernel
-// needs first (the first 16 splits' partials, the tail's values, and the
-// query and tail keys for the tail scores) is issued before any of them is
-// used, so the kernel waits for memory once.
+// running (max, sum, output), loading kBatch splits' partial outputs and
+// (max, sum) pairs together (8 when 64 splits or fewer, so no load is a
+// clamped repeat; 16 above), then every 8th tail token the same way, as a
+// partial of weight 1.  The 8 running triples meet in LDS.  Every load the
+// kernel needs first (the first kBatch splits' partials, the tail's values,
+// and the query and tail keys for the tail scores) is issued before any of
+// them is used, so the kernel waits for memory once for up to 8 kBatch
+// splits.
+template <int kBatch>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs a, uint16_t *out,
                                                                        float *lse) {
     const int gr = blockIdx.x;
@@ -80,7 +83,6 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(AttnArgs 
     // attends the tail itself
     const int n = a.tail_in_combine ? a.n_ctx_splits : a.n_splits;
     constexpr int kGroups = kCombineThreads / (kHeadDim / 4);  // 8 split groups
-    constexpr int kBatch = 16;
     constexpr int kTailMax = 64;                   // tail tokens attended at most
     constexpr int kTailPer = kTailMax / kGroups;   // per split group
     __shared__ float4 s_acc[kGroups][kHeadDim / 4];
@@ -430,8 +432,13 @@ hipError_t launch_attention(KvMode mode, const Geometry &g, const AttnPlan &plan
     } else {
         return hipErrorInvalidValue;  // anchor attention with several queries: no entry point asks for it
     }
-    hipLaunchKernelGGL(attn_combine_kernel, dim3(plan.rows_total, g.Hkv, B), dim3(kCombineThreads),
-                       0, stream, a, out, lse);
+    const int n_merged = a.tail_in_combine ? a.n_ctx_splits : a.n_splits;
+    if (n_merged <= 64)
+        hipLaunchKernelGGL(attn_combine_kernel<8>, dim3(plan.rows_total, g.Hkv, B), dim3(kCombineThreads),
+                           0, stream, a, out, lse);
+    else
+        hipLaunchKernelGGL(attn_combine_kernel<16>, dim3(plan.rows_total, g.Hkv, B), dim3(kCombineThreads),
+                           0, stream, a, out, lse);
     return hipGetLastError();
 }
 

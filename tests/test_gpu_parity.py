@@ -452,6 +452,32 @@ def test_anchor_decode_tail(n_tail, lens, bt):
     np.testing.assert_allclose(lse, ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
 
 
+def test_combine_of_more_than_64_splits():
+    """One kv head over 40,000 tokens: 79 splits of 512 tokens, merged by the
+    combine kernel with its larger load batch (decode with a tail, and
+    verification with its causal draft tail)."""
+    Hkv, G, T, nq = 1, 4, 40000, 4
+    k, v = random_kv(T, Hkv, seed=1300)
+    c = build_cache([k], [v], Hkv)
+    q = random_bf16((1, Hkv * G, 128), seed=1301)
+    kt = random_bf16((1, 8, Hkv, 128), seed=1302)
+    vt = random_bf16((1, 8, Hkv, 128), seed=1303)
+    out, lse = gpu_anchor_decode_tail(c, q, kt, vt)
+    ref, ref_lse = oracle.anchor_decode(c.OL, Hkv * G, np.array(c.lens), c.table.numpy(),
+                                        c.planes["k_anc"], c.planes["v_anc"], c.meta, bits(q),
+                                        k_tail_bits=bits(kt), v_tail_bits=bits(vt))
+    assert_close(out, ref, what="decode with a tail over 79 splits")
+    np.testing.assert_allclose(lse, ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
+    qv = random_bf16((1, nq, Hkv * G, 128), seed=1304)
+    kn = random_bf16((1, nq, Hkv, 128), seed=1305)
+    vn = random_bf16((1, nq, Hkv, 128), seed=1306)
+    got = gpu_verify(c, qv, kn, vn)
+    want = oracle_verify(c, qv, kn, vn)
+    if isinstance(want, tuple):
+        want = want[0]
+    assert_close(got, want, what="verification over 79 splits")
+
+
 def test_anchor_decode_empty_tail_matches_plain_decode():
     Hkv, G = 2, 4
     kv = [random_kv(T, Hkv, seed=1200 + T) for T in (333, 1024)]
