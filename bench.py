@@ -620,7 +620,7 @@ def overlap_70b_stage(dev):
     merge_verify()
     torch.cuda.synchronize()
     runs, step_us = [], []
-    for _ in range(10):
+    for _ in range(REPS):
         # decode alone (a pair of events around each step too)
         a0, a1 = ev(), ev()
         sev = [(ev(), ev()) for _ in range(steps)]
@@ -774,7 +774,7 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
 
     run()
     piped, wires = [], []
-    for _ in range(10):
+    for _ in range(REPS):
         piped.append(run())
         wires.append(run(kernels=False))
     # medians over the runs (the pinned-host copy rate varies run to run)
@@ -784,7 +784,7 @@ def serdes_pipeline_stage(dev, T, Hkv, K, V, n_layers, side):
     run()
     # each kernel alone: median over blocks of all layers (ms per block)
     def alone(fn):
-        return summary(call_samples(fn, n=20, warm=2))["median"] * 1e-3
+        return summary(call_samples(fn, n=REPS, warm=2))["median"] * 1e-3
     t_ser = alone(lambda: [lynx.lynx_kv_serialize(Hkv, T, K[l], V[l], tx_anc[l % n_tx], tx_res[l])
                            for l in range(n_layers)])
     t_da = alone(lambda: [lynx.lynx_kv_deserialize_anchor(L, 0, 0, T, table, rx["a"][l % 2], recv[l].k_anc,
