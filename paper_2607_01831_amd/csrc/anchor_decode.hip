@@ -658,6 +658,11 @@ hipError_t launch_anchor_decode_mfma(const DecodeArgs &args, int chunks, hipStre
         launch_groups<8>(args, grid, stream);
     } else if (args.groups_per_split == 16) {
         launch_groups<16>(args, grid, stream);
+    } else if (args.groups_per_split == 32 && args.geo.max_blocks == 1) {
+        // the long splits of one-round contiguous batches (plan_attention)
+        launch_layout<0, 32>(args, grid, stream);
+    } else if (args.groups_per_split == 64 && args.geo.max_blocks == 1) {
+        launch_layout<0, 64>(args, grid, stream);
     } else {
         return hipErrorInvalidValue;
     }

@@ -270,6 +270,21 @@ AttnPlan plan_attention(const Geometry &g, int B, int Hq, int nq, int max_seq_le
         if (next * g.Hkv * B < min_workgroups) break;
         p.split_tokens *= 2;
     }
+    if (nq == 1 && !tail && g.max_blocks == 1 && G <= 8) {
+        // A contiguous decode batch that fits one round of workgroups (two per
+        // CU) with longer splits, up to 8192 tokens, takes them: the split
+        // merge then runs in the same launch, and no workgroup waits for a
+        // second round (70B-shaped batch, 4 x 128K tokens: 2048 workgroups of
+        // 2048 tokens and the combine kernel, 112 us; 512 of 8192, 104 us).
+        const int cus = compute_units();
+        for (int st = p.split_tokens; cus > 0 && st <= 8192; st *= 2) {
+            const long long splits = max_seq_len > 0 ? (max_seq_len + st - 1) / st : 1;
+            if (splits * g.Hkv * B <= 2LL * cus) {
+                p.split_tokens = st;
+                break;
+            }
+        }
+    }
     // at least one split, so that empty sequences still get (zero) outputs
     p.n_ctx_splits = max_seq_len > 0 ? (max_seq_len + p.split_tokens - 1) / p.split_tokens : 1;
     p.n_splits = p.n_ctx_splits + (tail ? 1 : 0);

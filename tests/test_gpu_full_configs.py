@@ -14,7 +14,7 @@ import torch
 import oracle
 from paper_2607_01831_amd import inputs, lynx
 from tests._util import LSE_ATOL, LSE_RTOL, assert_close
-from tests.gpu_cases import bits, build_cache, note
+from tests.gpu_cases import bits, build_cache, note, random_bf16, random_kv
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -201,3 +201,18 @@ def test_70b_b4_128k():
     outv = run_verify(c, qv, kn, vn)
     refv = oracle_verify(c, qv, kn, vn, mask)
     check_units(outv, refv, mask, w.G, "70B verify k=4")
+
+
+def test_decode_one_round_long_splits():
+    """A contiguous batch large enough that one round of workgroups (two per
+    CU) needs 4096-token splits: 512K tokens, 4 kv heads, G = 4.  The split
+    merge runs in the same launch; 2 sampled units against the oracle."""
+    Hkv, G, T = 4, 4, 524288
+    k, v = random_kv(T, Hkv, seed=6100)
+    c = build_cache([k], [v], Hkv, merge=False)
+    del k, v
+    q = random_bf16((1, Hkv * G, 128), seed=6101)
+    out, lse = run_decode(c, q)
+    mask = sample_units(1, Hkv, 2, seed=6102)
+    ref, ref_lse = oracle_decode(c, q, mask)
+    check_units(out, ref, mask, G, "one-round decode over 512K tokens", lse, ref_lse)
