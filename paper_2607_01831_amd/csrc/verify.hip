@@ -151,7 +151,7 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
     int Ev = 0;
     {
         float vm = 0.0f;
-#pragma unroll
+#pragma unroll 4
         for (int u = 0; u < kMaxGroups; ++u) {
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
@@ -595,6 +595,10 @@ template <int RT, int LAYOUT>
 void launch_rt(const VerifyArgs &args, int split_groups, dim3 grid, hipStream_t stream) {
     if (split_groups == 4)
         hipLaunchKernelGGL((verify_kernel<RT, LAYOUT, 4>), grid, dim3(kThreads), 0, stream, args);
+    else if (LAYOUT == 0 && split_groups == 32)
+        hipLaunchKernelGGL((verify_kernel<RT, 0, 32>), grid, dim3(kThreads), 0, stream, args);
+    else if (LAYOUT == 0 && split_groups == 64)
+        hipLaunchKernelGGL((verify_kernel<RT, 0, 64>), grid, dim3(kThreads), 0, stream, args);
     else if (split_groups == 8)
         hipLaunchKernelGGL((verify_kernel<RT, LAYOUT, 8>), grid, dim3(kThreads), 0, stream, args);
     else
@@ -614,7 +618,9 @@ void launch_layout(const VerifyArgs &args, int split_groups, dim3 grid, hipStrea
 }  // namespace
 
 hipError_t launch_verify_mfma(const VerifyArgs &args, int split_groups, hipStream_t stream) {
-    if (split_groups != 4 && split_groups != 8 && split_groups != 16) return hipErrorInvalidValue;
+    if (split_groups != 4 && split_groups != 8 && split_groups != 16 &&
+        !(args.geo.max_blocks == 1 && (split_groups == 32 || split_groups == 64)))
+        return hipErrorInvalidValue;
     if (args.rows_total < 1) return hipErrorInvalidValue;
     const int rt = args.rows_total <= 16 ? 1 : 2;
     const int chunks = (args.rows_total + 16 * rt - 1) / (16 * rt);

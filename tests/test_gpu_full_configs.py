@@ -203,16 +203,25 @@ def test_70b_b4_128k():
     check_units(outv, refv, mask, w.G, "70B verify k=4")
 
 
-def test_decode_one_round_long_splits():
+def test_one_round_long_splits():
     """A contiguous batch large enough that one round of workgroups (two per
-    CU) needs 4096-token splits: 512K tokens, 4 kv heads, G = 4.  The split
-    merge runs in the same launch; 2 sampled units against the oracle."""
-    Hkv, G, T = 4, 4, 524288
+    CU) needs 4096-token splits: 512K tokens, 4 kv heads, G = 4.  Decode (its
+    split merge in the same launch) and verification of k = 4 drafts with
+    their tail (16 query rows per workgroup), 2 sampled units each against
+    the oracle."""
+    Hkv, G, T, nq = 4, 4, 524288, 4
     k, v = random_kv(T, Hkv, seed=6100)
-    c = build_cache([k], [v], Hkv, merge=False)
+    c = build_cache([k], [v], Hkv)
     del k, v
     q = random_bf16((1, Hkv * G, 128), seed=6101)
     out, lse = run_decode(c, q)
     mask = sample_units(1, Hkv, 2, seed=6102)
     ref, ref_lse = oracle_decode(c, q, mask)
     check_units(out, ref, mask, G, "one-round decode over 512K tokens", lse, ref_lse)
+    qv = random_bf16((1, nq, Hkv * G, 128), seed=6103)
+    kn = random_bf16((1, nq, Hkv, 128), seed=6104)
+    vn = random_bf16((1, nq, Hkv, 128), seed=6105)
+    outv = run_verify(c, qv, kn, vn)
+    mask = sample_units(1, Hkv, 2, seed=6106)
+    refv = oracle_verify(c, qv, kn, vn, mask)
+    check_units(outv, refv, mask, G, "one-round verification over 512K tokens")
