@@ -51,6 +51,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 from pathlib import Path
@@ -191,6 +192,23 @@ def _short(name: str) -> str:
     return name.split("(")[0][:60]
 
 
+def _variant(name: str) -> str:
+    """A library kernel with its template arguments (the decode of a 32K layer,
+    anchor_decode_kernel<4, 0, 4>, and the 70B-shaped one-round decode,
+    anchor_decode_kernel<8, 0, 64>, launch the same number of work-items);
+    any other kernel by its short name."""
+    m = re.search(r"(\w+_kernel)(<[^()]*>)\(", name)
+    if m and "lynx::" in name:
+        return m.group(1) + m.group(2)
+    return _short(name)
+
+
+# the roofline's call: one 32K-token layer of 8 kv heads, one round of 512
+# workgroups of 4 groups each
+DECODE_32K_VARIANT = "anchor_decode_kernel<4, 0, 4>"
+DECODE_32K_GRID = 512 * 256
+
+
 def _us(r):
     return (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
 
@@ -236,27 +254,27 @@ def summarize_trace(dirname):
     rows = _csv(dirname, "kernel_trace.csv")
     by = {}
     for r in rows:
-        by.setdefault((_short(r["Kernel_Name"]), _grid(r)), []).append(_us(r))
+        by.setdefault((_variant(r["Kernel_Name"]), _grid(r)), []).append(_us(r))
     print("| kernel | grid (work-items) | dispatches | median us | min us | max us | mean us |")
     print("|---|---|---|---|---|---|---|")
     for (n, g), ds in sorted(by.items(), key=lambda kv: -sum(kv[1])):
         med, lo, hi, mean = _stats(ds)
         print(f"| {n} | {g} | {len(ds)} | {med:.2f} | {lo:.2f} | {hi:.2f} | {mean:.2f} |")
     print()
-    print("| call | grid of the first kernel | calls | first kernel median us | combine median us | "
+    print("| first kernel of the call | grid (work-items) | calls | first kernel median us | combine median us | "
           "call (first start to last end) median us |")
     print("|---|---|---|---|---|---|")
-    for first in ("anchor_decode_kernel", "verify_kernel"):
+    for first in ("anchor_decode_kernel", "anchor_split_decode_kernel", "verify_kernel"):
         groups = {}
         for a, b in _calls(rows, first):
-            groups.setdefault(_grid(a), []).append((a, b))
-        for g, cs in sorted(groups.items()):
+            groups.setdefault((_variant(a["Kernel_Name"]), _grid(a)), []).append((a, b))
+        for (v, g), cs in sorted(groups.items()):
             k = _stats([_us(a) for a, _ in cs])[0]
             comb = [_us(b) for _, b in cs if b is not None]
             c = f"{_stats(comb)[0]:.2f}" if comb else "(fused)"
             span = _stats([(int((b or a)["End_Timestamp"]) - int(a["Start_Timestamp"])) / 1e3
                            for a, b in cs])[0]
-            print(f"| {first.replace('_kernel', '')} | {g} | {len(cs)} | {k:.2f} | {c} | {span:.2f} |")
+            print(f"| {v} | {g} | {len(cs)} | {k:.2f} | {c} | {span:.2f} |")
 
 
 def summarize_pmc(fetch_dir, write_dir):
@@ -290,7 +308,7 @@ def summarize_pmc(fetch_dir, write_dir):
     def grouped(table, f):
         g = {}
         for r, v in table.values():
-            g.setdefault((_short(r["Kernel_Name"]), _grid(r)), []).append(v * 1024 * f)
+            g.setdefault((_variant(r["Kernel_Name"]), _grid(r)), []).append(v * 1024 * f)
         return g
 
     gf, gw = grouped(fetch, f_fetch), grouped(write, f_write)
@@ -305,10 +323,9 @@ def summarize_pmc(fetch_dir, write_dir):
     # one 32K-layer decode call: the decode kernel with the 32K layer's grid
     # (and its combine, when the call has one)
     rows_f = [r for r, _ in fetch.values()]
-    grid_32k = 512 * 256
     per = []
     for a, b in _calls(rows_f, "anchor_decode_kernel"):
-        if _grid(a) != grid_32k:
+        if _variant(a["Kernel_Name"]) != DECODE_32K_VARIANT or _grid(a) != DECODE_32K_GRID:
             continue
         ids = [int(a["Dispatch_Id"])] + ([int(b["Dispatch_Id"])] if b is not None else [])
         if all(i in write for i in ids):
@@ -321,27 +338,38 @@ def summarize_pmc(fetch_dir, write_dir):
 
 
 def summarize_copies(dirname):
-    """For every host-to-device copy longer than 1 ms in a rocprofv3
-    --kernel-trace --memory-copy-trace run: the kernels that ran while it
-    was in flight (count, and time inside the copy's window)."""
+    """Host-to-device copies longer than 1 ms in a rocprofv3 --kernel-trace
+    --memory-copy-trace run, grouped by what ran while each was in flight
+    (kernel variants and their dispatch counts) and by duration to the
+    millisecond: copies per group, median duration, median time each kernel
+    spent inside the copy's window."""
     kt = _csv(dirname, "kernel_trace.csv")
     mc = _csv(dirname, "memory_copy_trace.csv")
     big = [r for r in mc if r["Direction"].endswith("HOST_TO_DEVICE")
            and int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) > 1_000_000]
-    print("| H2D copy | duration us | kernels inside its window (kernel [grid] x dispatches: us inside) |")
-    print("|---|---|---|")
-    for i, r in enumerate(big):
+    groups, order = {}, []
+    for r in big:
         s0, e0 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
         inside = {}
         for k in kt:
             ov = min(int(k["End_Timestamp"]), e0) - max(int(k["Start_Timestamp"]), s0)
             if ov > 0:
-                c = inside.setdefault((_short(k["Kernel_Name"]), _grid(k)), [0, 0.0])
+                c = inside.setdefault((_variant(k["Kernel_Name"]), _grid(k)), [0, 0.0])
                 c[0] += 1
                 c[1] += ov / 1e3
-        desc = "; ".join(f"{n} [{g}] x{c}: {t:.1f}" for (n, g), (c, t) in
-                         sorted(inside.items(), key=lambda kv: -kv[1][1])) or "none"
-        print(f"| {i + 1} | {(e0 - s0) / 1e3:.1f} | {desc} |")
+        key = ((e0 - s0) // 1_000_000, tuple(sorted((n, g, c) for (n, g), (c, _) in inside.items())))
+        if key not in groups:
+            groups[key] = []
+            order.append(key)
+        groups[key].append(((e0 - s0) / 1e3, {(n, g): t for (n, g), (_, t) in inside.items()}))
+    print("| H2D copies | median duration us | kernels inside each copy's window (kernel [grid] x dispatches: "
+          "median us inside) |")
+    print("|---|---|---|")
+    for key in order:
+        cs = groups[key]
+        desc = "; ".join(f"{n} [{g}] x{c}: {_stats([t[(n, g)] for _, t in cs])[0]:.1f}"
+                         for n, g, c in key[1]) or "none"
+        print(f"| {len(cs)} | {_stats([d for d, _ in cs])[0]:.1f} | {desc} |")
 
 
 TRANSPORT_CONDITIONS = ("alone", "h2d running", "after encode", "after encode, h2d running")
@@ -398,7 +426,7 @@ def summarize_conditions(dirs):
             name = rs[0]["Kernel_Name"]
             if "FillFunctor<short>" in name:
                 cond = markers.index(_grid(rs[0]))
-            elif cond is not None and _short(name) == "anchor_decode_kernel" and _grid(rs[0]) == 131072:
+            elif cond is not None and _variant(name) == DECODE_32K_VARIANT and _grid(rs[0]) == DECODE_32K_GRID:
                 for r in rs:
                     per.setdefault(r["Counter_Name"], {}).setdefault(cond, []).append(
                         float(r["Counter_Value"]))
