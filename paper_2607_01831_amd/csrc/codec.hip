@@ -305,26 +305,43 @@ __device__ __forceinline__ uint2 merge4(uint32_t a, uint32_t r) {
 
 constexpr int kMergeThreads = 256;
 
-// Each thread merges 16 anchor + 16 residual bytes into 32 code bytes per
-// iteration of a grid-stride loop; 16-byte loads, two 16-byte stores.
+// Wave w of the grid merges pieces (8 anchor + 8 residual bytes -> 16 code
+// bytes) base + lane and base + 64 + lane, base = 128 w, 128 (w + waves), ...:
+// every load instruction reads 512 contiguous bytes and every store
+// instruction writes 1 KB, whole cache lines (two 16-byte stores per lane
+// that interleave inside each line were 10% slower).  The stores are
+// nontemporal: the verification that follows reads the codes much faster
+// when they were not written through the last-level cache (a 70B-shaped
+// verification over 1.1 GB of codes: 278 -> 214 us right after the merge).
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
-    const uint4 *__restrict__ anc, const uint4 *__restrict__ res, uint4 *__restrict__ codes,
-    size_t n16, const uint8_t *__restrict__ anc_b, const uint8_t *__restrict__ res_b,
+    const uint2 *__restrict__ anc, const uint2 *__restrict__ res, uint8_t *__restrict__ codes,
+    size_t n8, const uint8_t *__restrict__ anc_b, const uint8_t *__restrict__ res_b,
     uint8_t *__restrict__ codes_b, size_t n_packed) {
-    const size_t stride = (size_t)gridDim.x * blockDim.x;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) {
-        const uint4 a = anc[i];
-        const uint4 r = res[i];
-        const uint2 c0 = merge4(a.x, r.x);
-        const uint2 c1 = merge4(a.y, r.y);
-        const uint2 c2 = merge4(a.z, r.z);
-        const uint2 c3 = merge4(a.w, r.w);
-        codes[2 * i] = make_uint4(c0.x, c0.y, c1.x, c1.y);
-        codes[2 * i + 1] = make_uint4(c2.x, c2.y, c3.x, c3.y);
+    const int lane = threadIdx.x & 63;
+    const size_t wave = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const size_t n_waves = ((size_t)gridDim.x * blockDim.x) >> 6;
+    u32v4 *out = reinterpret_cast<u32v4 *>(codes);
+    for (size_t base = 128 * wave; base < n8; base += 128 * n_waves) {
+        const size_t p0 = base + lane, p1 = base + 64 + lane;
+        uint2 a0 = make_uint2(0u, 0u), r0 = a0, a1 = a0, r1 = a0;
+        if (p0 < n8) {
+            a0 = anc[p0];
+            r0 = res[p0];
+        }
+        if (p1 < n8) {
+            a1 = anc[p1];
+            r1 = res[p1];
+        }
+        const uint2 x0 = merge4(a0.x, r0.x), y0 = merge4(a0.y, r0.y);
+        const uint2 x1 = merge4(a1.x, r1.x), y1 = merge4(a1.y, r1.y);
+        const u32v4 o0 = {x0.x, x0.y, y0.x, y0.y};
+        const u32v4 o1 = {x1.x, x1.y, y1.x, y1.y};
+        if (p0 < n8) __builtin_nontemporal_store(o0, out + p0);
+        if (p1 < n8) __builtin_nontemporal_store(o1, out + p1);
     }
-    // ragged tail (< 16 bytes)
+    // ragged tail (< 8 bytes)
     if (blockIdx.x == 0 && threadIdx.x == 0) {
-        for (size_t j = n16 * 16; j < n_packed; ++j) {
+        for (size_t j = n8 * 8; j < n_packed; ++j) {
             const uint32_t a = anc_b[j], r = res_b[j];
             codes_b[2 * j] = (uint8_t)(((a & 15u) << 4) | (r & 15u));
             codes_b[2 * j + 1] = (uint8_t)((a & 0xF0u) | (r >> 4));
@@ -477,15 +494,15 @@ hipError_t launch_encode(const Geometry &g, int b, int T, const int32_t *block_t
 hipError_t launch_merge(const uint8_t *anc, const uint8_t *res, uint8_t *codes, size_t n_packed,
                         hipStream_t stream) {
     if (n_packed == 0) return hipSuccess;
-    const size_t n16 = n_packed / 16;
-    // enough workgroups to cover the device several times over; each thread
-    // then loops over the rest
-    size_t blocks = (n16 + kMergeThreads - 1) / kMergeThreads;
+    const size_t n8 = n_packed / 8;
+    // enough workgroups to cover the device several times over (two pieces
+    // per thread and round); each wave then loops over the rest
+    size_t blocks = (n8 + 2 * kMergeThreads - 1) / (2 * kMergeThreads);
     if (blocks > 256 * 32) blocks = 256 * 32;
     if (blocks == 0) blocks = 1;
     hipLaunchKernelGGL(merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, stream,
-                       reinterpret_cast<const uint4 *>(anc), reinterpret_cast<const uint4 *>(res),
-                       reinterpret_cast<uint4 *>(codes), n16, anc, res, codes, n_packed);
+                       reinterpret_cast<const uint2 *>(anc), reinterpret_cast<const uint2 *>(res), codes, n8,
+                       anc, res, codes, n_packed);
     return hipGetLastError();
 }
 
@@ -540,7 +557,8 @@ hipError_t launch_deserialize_residual(const Geometry &g, int b, int t0, int n,
 namespace {
 
 // Merge of A-bit anchor rows and R-bit residual rows: thread per 8 elements
-// of a row (A + R bytes in, 8 code bytes out), grid-stride.
+// of a row (A + R bytes in, 8 code bytes out), grid-stride; nontemporal
+// stores, as in merge_kernel.
 template <int A>
 __global__ __launch_bounds__(kMergeThreads) void merge_split_kernel(const uint8_t *__restrict__ anc,
                                                                     const uint8_t *__restrict__ res,
@@ -563,7 +581,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_split_kernel(const uint8_
             const uint64_t r = (rs >> (R * j)) & ((1u << R) - 1u);
             c |= ((a << R) | r) << (8 * j);
         }
-        *reinterpret_cast<uint2 *>(codes + 8 * i) = make_uint2((uint32_t)c, (uint32_t)(c >> 32));
+        __builtin_nontemporal_store(c, reinterpret_cast<uint64_t *>(codes + 8 * i));
     }
 }
 
