@@ -73,8 +73,11 @@ MERGE_BYTES_PER_ELEM = 2.0                      # read 0.5 + 0.5, write 1
 DECODE_BYTES_PER_TOKEN_HEAD = 64 + 64 + 8 + 8   # K, V nibble rows + V meta + K meta (amortised)
 VERIFY_BYTES_PER_TOKEN_HEAD = 128 + 128 + 8 + 8  # K, V code rows + metadata
 
-# timed samples per stage, after untimed warm-ups
-REPS, WARM = 50, 5
+# timed samples per stage, after untimed warm-ups: at least WARM calls and
+# at least WARM_S seconds of them (the part's clocks take tens of ms of
+# sustained load to settle: the paged batch decode, 50 calls at a time on one
+# pool, runs 157, 143, 141, 140, 138, 137, 135, 133 us from a cold start)
+REPS, WARM, WARM_S = 50, 5, 0.05
 
 
 def summary(samples):
@@ -87,12 +90,18 @@ def summary(samples):
 
 def call_samples(fn, n=REPS, warm=WARM, per=1):
     """us per unit of `fn` (which covers `per` units), one pair of HIP events
-    on the current stream around each of n timed calls after `warm` untimed ones."""
+    on the current stream around each of n timed calls after untimed ones: at
+    least `warm` calls and at least WARM_S seconds of calls."""
     import torch
 
+    t0 = time.perf_counter()
     for _ in range(warm):
         fn()
     torch.cuda.synchronize()
+    while time.perf_counter() - t0 < WARM_S:
+        for _ in range(max(warm, 1)):
+            fn()
+        torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(n)]
     for a, b in evs:
@@ -581,7 +590,7 @@ def paged_decode_stage(calls, dev):
 
 def overlap_70b_stage(dev):
     """The 70B-shaped overlap run (70b-overlap-b4-128k): 4 sequences x 131072
-    tokens, 64 q / 8 kv heads.  Timed with HIP events over ten runs (medians;
+    tokens, 64 q / 8 kv heads.  Timed with HIP events over REPS runs (medians;
     every decode step also alone), each part alone and then overlapped: 16 anchor-decode steps (a fresh query per step); the
     H2D of the residual planes (512 MiB) from pinned host memory on a side
     stream; both at once; then merge of both planes and verification of
@@ -644,9 +653,13 @@ def overlap_70b_stage(dev):
                               qv, kn, vn, outv, ws)
         return m
 
+    t0 = time.perf_counter()
     decode_steps()
     merge_verify()
     torch.cuda.synchronize()
+    while time.perf_counter() - t0 < WARM_S:
+        decode_steps()
+        torch.cuda.synchronize()
     runs, step_us = [], []
     for _ in range(REPS):
         # decode alone (a pair of events around each step too)
@@ -671,6 +684,10 @@ def overlap_70b_stage(dev):
         runs.append({"t_dec": a0.elapsed_time(a1), "t_h2d": h0.elapsed_time(h1),
                      "t_both": b0.elapsed_time(b1), "merge": b1.elapsed_time(m1),
                      "verify": m1.elapsed_time(v1), "e2e": b0.elapsed_time(v1)})
+    # the decode step on its own, called back to back after the warm-up: the
+    # kernel's sustained rate, beside the in-run figure above (whose steps start
+    # after the merge, the verification and the transport's wait)
+    sustained = summary(call_samples(lambda: decode_steps(), n=REPS, per=steps))
     # medians over the runs (ms)
     best = {k: summary([r_[k] for r_ in runs])["median"] for k in runs[0]}
     t_dec, t_h2d, t_both = best["t_dec"], best["t_h2d"], best["t_both"]
@@ -686,6 +703,8 @@ def overlap_70b_stage(dev):
         "decode_us_per_step_min": st_step["min"],
         "decode_us_per_step_max": st_step["max"],
         "decode_steps_timed": st_step["n"],
+        "decode_us_per_step_sustained": sustained["median"],
+        "decode_frac_sustained": round(dec_bytes / (sustained["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
         "decode_GBps": round(dec_bytes / (us_step * 1e-6) / 1e9, 2),
         "decode_frac": round(dec_bytes / (us_step * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
         "decode_16_steps_us": round(t_dec * 1e3, 1),

@@ -127,22 +127,31 @@ __device__ __forceinline__ const void *uniform(const void *p) {
     const uint64_t v = (uint64_t)(uintptr_t)p;
     return (const void *)(uintptr_t)(((uint64_t)uniform((uint32_t)(v >> 32)) << 32) | uniform((uint32_t)v));
 }
+// The global-to-LDS copies take their LDS address in M0, which they set
+// themselves and list as clobbered, so the compiler never assumes a value of
+// its own survives them (it re-initialises M0 before any use and inserts the
+// hazard waits).  M0 is a reserved register to the compiler, which warns that
+// such a clobber is not preserved: that is the intent, and the warning is
+// silenced for these three functions only.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 // 16 bytes per lane from sbase + voff (sbase uniform) to LDS at lds + 16 lane.
 __device__ __forceinline__ void lds_copy16(const void *sbase, uint32_t voff, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(uniform(sbase)),
                  "s"(uniform(lds))
-                 : "memory");
+                 : "memory", "m0");
 }
 // 16 bytes per lane from the lane's own address.
 __device__ __forceinline__ void lds_copy16(const void *addr, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(addr), "s"(uniform(lds))
-                 : "memory");
+                 : "memory", "m0");
 }
 // 4 bytes per lane from the lane's own address to LDS at lds + 4 lane.
 __device__ __forceinline__ void lds_copy4(const void *addr, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(addr), "s"(uniform(lds))
-                 : "memory");
+                 : "memory", "m0");
 }
+#pragma clang diagnostic pop
 // Wait until at most N vector-memory operations of this wavefront are in flight.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
