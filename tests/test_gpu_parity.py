@@ -72,7 +72,11 @@ def test_encode_adversarial_groups():
     assert_codec_equal(c)
 
 
-@pytest.mark.parametrize("n", [1, 15, 16, 17, 4096, 4096 + 5, 1 << 20])
+# sizes around the kernel's 8-byte pieces and its 1 KB wave rounds, and one
+# past the 8192 workgroups x 4 waves x 1 KB of one grid round (so waves loop)
+# with a ragged tail
+@pytest.mark.parametrize("n", [1, 7, 8, 9, 15, 16, 17, 1023, 1024, 1025, 4096, 4096 + 5, 1 << 20,
+                               (32 << 20) + 3 * 1024 + 8 * 5 + 5])
 def test_merge_bit_exact(n):
     g = torch.Generator().manual_seed(n)
     a = torch.randint(0, 256, (n,), generator=g, dtype=torch.uint8)
