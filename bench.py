@@ -17,21 +17,25 @@ One step = the whole hot path over all 32 layers:
      plane kind over all layers                               [main stream]
   5. verification attention of the 8 drafts over the codes    [main stream]
 
-After the timed steps, six stages are timed on their own (reported under
-"stages"): the same decode calls with no transport running; the
-verification of k = 8 drafts at 128K context (32 q / 8 kv heads, one layer,
-merged codes + causal BF16 tail), the configuration the paper's verification
-latency is quoted for; the decode calls once more with the 8 BF16 tokens the
-speculative decoder generated; greedy acceptance of 8 drafts over a
-128256-entry vocabulary; the batched paged decode of 16 sequences of 16K-64K
-tokens in 16-token blocks; and the 70B-shaped overlap run (4 x 128K tokens,
-64 q / 8 kv heads: 16 decode steps against the residual H2D, then merge and
-verification of 4 drafts, with the overlap fraction and end-to-end time).
+After the timed steps, further stages are timed on their own (reported
+under "stages"): the same decode calls with no transport running, and in
+the four transport conditions; the stream ceilings (a device copy and a
+uint8 add); the verification of k = 8 drafts at 128K context (32 q / 8 kv
+heads, one layer, merged codes + causal BF16 tail), the configuration the
+paper's verification latency is quoted for; the decode calls once more with
+the 8 BF16 tokens the speculative decoder generated; greedy and sampled
+acceptance of 8 drafts over a 128256-entry vocabulary; the batched paged
+decode of 16 sequences of 16K-64K tokens in 16-token blocks; the 70B-shaped
+overlap run (4 x 128K tokens, 64 q / 8 kv heads: 16 decode steps against
+the residual H2D, then merge and verification of 4 drafts, with the overlap
+fraction and end-to-end time); the serializer pipeline; the hierarchical
+codec; and the 2 + 6 / 6 + 2 split widths.
 
 Every stage is timed with a pair of HIP events around each call (or block of
-per-layer calls) after untimed warm-ups and reported as the median, with min,
-max and count where the spread matters: 50 samples unless stated (50 steps by
-default; ten runs for the millisecond-long transport pipelines).
+per-layer calls) after untimed warm-ups (at least 5 calls and at least 50 ms
+of them) and reported as the median, with min, max and count: 50 samples
+unless stated (50 steps by default; 50 runs of the millisecond-long
+transport pipelines).
 
 Printed: one JSON line.  `value` is the anchor-decode attention throughput in
 GB/s of algorithmic KV bytes (144 bytes per token per kv head) over all the
@@ -42,6 +46,9 @@ summaries kept under profiles/:
   --summarize-trace DIR          kernel-trace CSVs -> per-kernel durations
   --summarize-pmc FETCH WRITE    FETCH_SIZE / WRITE_SIZE CSVs of a run with
                                  --copy-calibration -> HBM bytes per call
+  --summarize-copies DIR         kernel + memory-copy trace -> the kernels
+                                 inside each host-to-device copy
+  --summarize-conditions DIR...  counter runs of the transport conditions
 """
 from __future__ import annotations
 
