@@ -585,9 +585,16 @@ __global__ __launch_bounds__(kThreads, 2) void verify_kernel(VerifyArgs a) {
             O.w = fmaf(o.w + ob, f, O.w);
         }
         if (any_bad) O = make_float4(NAN, NAN, NAN, NAN);
+        // nontemporal: the combine kernel reads the partials back faster when
+        // they did not go through the last-level cache (32K layer 30.3 ->
+        // 29.8 us per call, 128K 65.2 -> 63.9 us)
         const size_t pi = partial_index(row);
-        reinterpret_cast<float4 *>(a.ws_o + pi * kHeadDim)[d4] = O;
-        if (d4 == 0) a.ws_ml[pi] = make_float2(s_ML[rr][0], s_ML[rr][1]);
+        const f32x4_t ov = {O.x, O.y, O.z, O.w};
+        __builtin_nontemporal_store(ov, reinterpret_cast<f32x4_t *>(a.ws_o + pi * kHeadDim) + d4);
+        if (d4 == 0) {
+            const f32x2_t mlv = {s_ML[rr][0], s_ML[rr][1]};
+            __builtin_nontemporal_store(mlv, reinterpret_cast<f32x2_t *>(a.ws_ml + pi));
+        }
     }
 }
 
