@@ -88,6 +88,29 @@ def test_merge_bit_exact(n):
     assert np.array_equal(codes.cpu().numpy(), oracle.merge(a.numpy(), r.numpy()))
 
 
+@pytest.mark.parametrize("offs", [(16, 48, 32), (4096 + 16, 16, 4096 + 48)])
+def test_merge_at_16_byte_offsets(offs):
+    """Planes and codes that start 16 bytes past an allocation's alignment (the
+    ABI asks for 16): the 8-byte loads and 16-byte stores of the merge stay
+    exact, and nothing outside the codes is written."""
+    oa, orr, oc = offs
+    n = 3 * 1024 + 8 * 3 + 5
+    g = torch.Generator().manual_seed(oa + orr)
+    a = torch.randint(0, 256, (n,), generator=g, dtype=torch.uint8)
+    r = torch.randint(0, 256, (n,), generator=g, dtype=torch.uint8)
+    abuf = torch.zeros(oa + n + 64, dtype=torch.uint8, device="cuda")
+    rbuf = torch.zeros(orr + n + 64, dtype=torch.uint8, device="cuda")
+    cbuf = torch.full((oc + 2 * n + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    abuf[oa:oa + n] = a.cuda()
+    rbuf[orr:orr + n] = r.cuda()
+    note(f"merge n={n} offsets={offs}")
+    lynx.lynx_kv_merge(abuf[oa:oa + n], rbuf[orr:orr + n], cbuf[oc:oc + 2 * n])
+    torch.cuda.synchronize()
+    got = cbuf.cpu().numpy()
+    assert np.array_equal(got[oc:oc + 2 * n], oracle.merge(a.numpy(), r.numpy()))
+    assert (got[:oc] == 0xA5).all() and (got[oc + 2 * n:] == 0xA5).all()
+
+
 def test_merge_of_encoded_planes():
     k, v = random_kv(640, 4, seed=9)
     c = build_cache([k], [v], 4)
